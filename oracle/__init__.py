@@ -1,0 +1,60 @@
+"""CPU oracle for RBS-Attention sparse prefill -- test infrastructure only.
+
+A plain, slow, float64 numpy restatement of the paper's definitions
+(Sec. 2.1 Eq. (1); Sec. 3.1; Sec. 3.2; Sec. 3.3 and Algorithm 1; Sec. 4.4 actual
+density).  It shares no code with the HIP path and exists to check it: only the
+tests, the smoke check and the benchmark's CPU-baseline leg may import it.
+The product path never calls it and has no CPU fallback.
+
+Parity status per function (what pins it, in tests/test_oracle_pins.py):
+  block_stats          pinned: Cauchy-Schwarz bound (Sec. 2.4), App. E examples,
+                       translation/rotation invariance, hand-worked fixtures
+  radius_quantiles /
+  rescue_coefficients  pinned: hand-computed type-7 quantiles, library quantile,
+                       degenerate-radius reading
+  branch_log_scores    pinned: hand-worked needle and aggregation fixtures,
+                       rescue >= base, shift invariance of the aggregation
+  select               pinned: hand-worked fixtures, threshold monotonicity,
+                       alpha = 0 / alpha = 1 special cases, forced blocks
+  attention_on_mask    pinned: brute-force Eq. (1) at full selection, softmax
+                       shift invariance, linearity in V
+  density              pinned: hand-counted masks
+"""
+
+from .rbs import (
+    block_ranges,
+    block_stats,
+    quantile_type7,
+    radius_quantiles,
+    rescue_coefficients,
+    forced_blocks,
+    branch_logits,
+    branch_log_scores,
+    select_row,
+    select,
+    attention_rows,
+    attention_on_mask,
+    dense_causal_attention,
+    density,
+    masks_from_lists,
+    lists_from_masks,
+)
+
+__all__ = [
+    "block_ranges",
+    "block_stats",
+    "quantile_type7",
+    "radius_quantiles",
+    "rescue_coefficients",
+    "forced_blocks",
+    "branch_logits",
+    "branch_log_scores",
+    "select_row",
+    "select",
+    "attention_rows",
+    "attention_on_mask",
+    "dense_causal_attention",
+    "density",
+    "masks_from_lists",
+    "lists_from_masks",
+]

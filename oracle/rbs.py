@@ -1,0 +1,291 @@
+"""Float64 oracle of the RBS-Attention sparse-prefill path (test infrastructure only).
+
+Written from the paper's definitions, step by step, with no blocking or fusion
+beyond what the definitions state.  Conventions (readings of points the paper
+leaves open are marked READING and listed in the design notes):
+
+* Q is [H_q][N][d], K and V are [H_kv][N][d]; query head h uses KV head
+  h // (H_q // H_kv) (READING: selection is made per query head).
+* Blocks: token range [b B, min((b+1) B, N)); the same partition for queries
+  and keys (Sec. 2.1, Sec. 4.4: query and key block size are equal).
+* Candidates of query block i are key blocks 0..i (READING: the diagonal block
+  and forced blocks take part in the maximum of the relative threshold).
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+
+# ---------------------------------------------------------------- partition
+
+def block_ranges(n_tokens: int, block_size: int) -> list:
+    """[(start, end)] of the M = ceil(N / B) blocks (Sec. 2.1)."""
+    return [(s, min(s + block_size, n_tokens)) for s in range(0, n_tokens, block_size)]
+
+
+# ---------------------------------------------------------------- Sec. 3.1
+
+def block_stats(K: np.ndarray, block_size: int):
+    """Centroid c_b = mean of the block's keys and radius r_b = max_k |k - c_b|_2.
+
+    Sec. 3.1, centroid and maximum-radius equations; Algorithm 1, first loop.
+    K: [H_kv][N][d] float64.  Returns centroids [H_kv][M][d], radii [H_kv][M].
+    The mean divides by the block's actual key count |K_b| (a short last block
+    uses its own count).
+    """
+    K = np.asarray(K, dtype=np.float64)
+    H, N, d = K.shape
+    ranges = block_ranges(N, block_size)
+    C = np.zeros((H, len(ranges), d))
+    R = np.zeros((H, len(ranges)))
+    for g in range(H):
+        for b, (s, e) in enumerate(ranges):
+            keys = K[g, s:e]
+            c = keys.sum(axis=0) / (e - s)
+            C[g, b] = c
+            R[g, b] = np.sqrt(((keys - c) ** 2).sum(axis=1)).max()
+    return C, R
+
+
+def quantile_type7(values, p: float) -> float:
+    """Sample quantile by linear interpolation between order statistics.
+
+    READING: the paper writes quantile(r, p) without naming an estimator; this
+    is the common "type 7" rule: with x sorted ascending (0-based) and
+    h = (n - 1) p, Q = x[floor h] + (h - floor h) (x[floor h + 1] - x[floor h]).
+    """
+    x = sorted(float(v) for v in values)
+    n = len(x)
+    h = (n - 1) * p
+    lo = int(math.floor(h))
+    hi = min(lo + 1, n - 1)
+    return x[lo] + (h - lo) * (x[hi] - x[lo])
+
+
+def radius_quantiles(R: np.ndarray):
+    """Per KV head: r_low = quantile(r, 0.5), r_high = quantile(r, 0.9) over
+    all M block radii of the prompt (Sec. 3.1; Algorithm 1).  Returns [H_kv][2]."""
+    R = np.asarray(R, dtype=np.float64)
+    return np.array([[quantile_type7(R[g], 0.5), quantile_type7(R[g], 0.9)]
+                     for g in range(R.shape[0])])
+
+
+def rescue_coefficients(R: np.ndarray):
+    """beta_b = clamp((r_b - r_low) / (r_high - r_low), 0, 1) (Sec. 3.1, Eq. beta).
+
+    READING for r_high <= r_low, where the paper leaves beta undefined: the
+    limit of the clamp, beta_b = 1 if r_b > r_low else 0.
+    Returns (beta [H_kv][M], quantiles [H_kv][2]).
+    """
+    R = np.asarray(R, dtype=np.float64)
+    rq = radius_quantiles(R)
+    beta = np.zeros_like(R)
+    for g in range(R.shape[0]):
+        r_low, r_high = rq[g]
+        if r_high > r_low:
+            beta[g] = np.clip((R[g] - r_low) / (r_high - r_low), 0.0, 1.0)
+        else:
+            beta[g] = (R[g] > r_low).astype(np.float64)
+    return beta, rq
+
+
+# ---------------------------------------------------------------- Sec. 3.2
+
+def branch_logits(Qi: np.ndarray, C: np.ndarray, R: np.ndarray, beta: np.ndarray,
+                  n_candidates: int):
+    """Token-level logits of both branches against candidates 0..n-1.
+
+    Qi: [n_i][d] queries of one query block; C, R, beta: one KV head's
+    statistics.  Base logit l_base(q, b) = q . c_b (Sec. 3.2, Eq. base_score);
+    rescue logit l_rescue(q, b) = q . c_b + |q|_2 r_b beta_b (Eq. rescue_score).
+    Returns (l_base, l_rescue), each [n_i][n_candidates], unscaled.
+    """
+    Qi = np.asarray(Qi, dtype=np.float64)
+    cand = C[:n_candidates]
+    l_base = Qi @ cand.T
+    qnorm = np.sqrt((Qi * Qi).sum(axis=1))
+    l_rescue = l_base + qnorm[:, None] * (R[:n_candidates] * beta[:n_candidates])[None, :]
+    return l_base, l_rescue
+
+
+def branch_log_scores(Qi: np.ndarray, C: np.ndarray, R: np.ndarray, beta: np.ndarray,
+                      n_candidates: int):
+    """Query-block aggregated scores of both branches for candidates 0..n-1.
+
+    The logits of branch_logits are scaled by 1/sqrt(d) and aggregated over the
+    block's tokens with the shared shift of Sec. 3.2, Eq. block_aggregation:
+        m = max_b max_t l(q_t, b)/sqrt(d),  S_b = sum_t exp(l(q_t, b)/sqrt(d) - m).
+    Returns (log S_base, log S_rescue) over the candidates, with log 0 = -inf.
+    """
+    d = np.asarray(Qi).shape[1]
+    out = []
+    for logits in branch_logits(Qi, C, R, beta, n_candidates):
+        x = logits / math.sqrt(d)
+        m = x.max()
+        S = np.exp(x - m).sum(axis=0)
+        with np.errstate(divide="ignore"):
+            out.append(np.log(S))
+    return out[0], out[1]
+
+
+def forced_blocks(i: int, n_blocks: int, n_sink: int, n_local: int, n_recent: int) -> np.ndarray:
+    """Forced set for query block i over candidates 0..i (Sec. 3.2, union).
+
+    READINGS: sink = the first n_sink key blocks; local window = the n_local
+    blocks ending at the diagonal; recent = the last n_recent query blocks keep
+    every causal candidate.
+    """
+    f = np.zeros(i + 1, dtype=bool)
+    f[:min(n_sink, i + 1)] = True
+    f[max(0, i - n_local + 1):i + 1] = True
+    if i >= n_blocks - n_recent:
+        f[:] = True
+    return f
+
+
+def _threshold(log_s: np.ndarray, alpha: float):
+    """Eq. branch_thresholds in log space: S_b >= alpha max S  <=>
+    log S_b >= log alpha + max log S.  Returns (mask, margin) where margin is
+    log S_b - log alpha - max log S (the mask is margin >= 0)."""
+    top = log_s.max()
+    if alpha <= 0.0:
+        return np.ones(log_s.shape, dtype=bool), np.full(log_s.shape, np.inf)
+    with np.errstate(invalid="ignore"):
+        margin = log_s - math.log(alpha) - top
+    margin = np.where(np.isnan(margin), -np.inf, margin)
+    return margin >= 0.0, margin
+
+
+def select_row(Qi, C, R, beta, i: int, n_blocks: int, tau_base: float, tau_rescue: float,
+               n_sink: int, n_local: int, n_recent: int) -> dict:
+    """Final mask of query block i: M_base U M_rescue U forced (Sec. 3.2)."""
+    log_b, log_r = branch_log_scores(Qi, C, R, beta, i + 1)
+    m_base, margin_base = _threshold(log_b, tau_base)
+    m_res, margin_res = _threshold(log_r, tau_rescue)
+    forced = forced_blocks(i, n_blocks, n_sink, n_local, n_recent)
+    return {
+        "base": m_base,
+        "rescue": m_res,
+        "forced": forced,
+        "final": m_base | m_res | forced,
+        "log_s_base": log_b,
+        "log_s_rescue": log_r,
+        "margin_base": margin_base,
+        "margin_rescue": margin_res,
+    }
+
+
+def select(Q, C, R, beta, block_size: int, tau_base: float, tau_rescue: float,
+           n_sink: int, n_local: int, n_recent: int, rows=None) -> dict:
+    """Run select_row for every (query head, query block) in `rows` (default:
+    all).  Q: [H_q][N][d] real values; C, R, beta: per KV head.
+    Returns {(h, i): row dict}."""
+    H_q, n_tokens = Q.shape[0], Q.shape[1]
+    group = H_q // C.shape[0]
+    ranges = block_ranges(n_tokens, block_size)
+    M = len(ranges)
+    if rows is None:
+        rows = [(h, i) for h in range(H_q) for i in range(M)]
+    out = {}
+    for (h, i) in rows:
+        g = h // group
+        s, e = ranges[i]
+        out[(h, i)] = select_row(np.asarray(Q[h, s:e], dtype=np.float64), C[g], R[g], beta[g],
+                                 i, M, tau_base, tau_rescue, n_sink, n_local, n_recent)
+    return out
+
+
+# ---------------------------------------------------------------- Sec. 3.3
+
+def attention_rows(Qh, Kg, Vg, block_size: int, i: int, kv_blocks, scale: float | None = None):
+    """Attention of query block i over the keys of the retained blocks, with
+    token-level causal masking and softmax over the retained causal keys
+    (Sec. 3.3; Eq. (1) restricted to the retained keys).  Float64.
+    Returns [n_i][d]; a query with no retained causal key gets zeros."""
+    Qh = np.asarray(Qh, dtype=np.float64)
+    N, d = Kg.shape
+    if scale is None or scale <= 0:
+        scale = 1.0 / math.sqrt(d)
+    s, e = i * block_size, min((i + 1) * block_size, N)
+    key_pos = np.concatenate([np.arange(b * block_size, min((b + 1) * block_size, N))
+                              for b in sorted(kv_blocks)]) if len(kv_blocks) else np.zeros(0, int)
+    keys = np.asarray(Kg[key_pos], dtype=np.float64)
+    vals = np.asarray(Vg[key_pos], dtype=np.float64)
+    out = np.zeros((e - s, d))
+    for t in range(s, e):
+        keep = key_pos <= t
+        if not keep.any():
+            continue
+        logits = keys[keep] @ Qh[t] * scale
+        p = np.exp(logits - logits.max())
+        out[t - s] = (p @ vals[keep]) / p.sum()
+    return out
+
+
+def attention_on_mask(Qh, Kg, Vg, block_size: int, row_blocks: dict, scale: float | None = None):
+    """Sparse attention for one query head over {i: retained key blocks}.
+    Returns {i: [n_i][d]}."""
+    return {i: attention_rows(Qh, Kg, Vg, block_size, i, blocks, scale)
+            for i, blocks in row_blocks.items()}
+
+
+def dense_causal_attention(Qh, Kg, Vg, scale: float | None = None):
+    """Brute-force causal softmax attention, Eq. (1): for every token t,
+    O_t = sum_{j<=t} softmax_j(q_t . k_j * scale) v_j.  Float64, O(N^2 d)."""
+    Qh = np.asarray(Qh, dtype=np.float64)
+    Kg = np.asarray(Kg, dtype=np.float64)
+    Vg = np.asarray(Vg, dtype=np.float64)
+    N, d = Qh.shape
+    if scale is None or scale <= 0:
+        scale = 1.0 / math.sqrt(d)
+    out = np.zeros((N, d))
+    for t in range(N):
+        logits = Kg[:t + 1] @ Qh[t] * scale
+        w = np.exp(logits - logits.max())
+        out[t] = (w / w.sum()) @ Vg[:t + 1]
+    return out
+
+
+# ---------------------------------------------------------------- Sec. 4.4
+
+def density(final_masks) -> float:
+    """Actual density: selected valid causal block pairs / all valid causal block
+    pairs, forced blocks and branch overlap counted once (Sec. 4.4).
+    final_masks: iterable of per-(head, query block) boolean rows over 0..i."""
+    selected = 0
+    total = 0
+    for row in final_masks:
+        row = np.asarray(row, dtype=bool)
+        selected += int(row.sum())
+        total += row.shape[0]
+    return selected / total if total else 0.0
+
+
+# ---------------------------------------------------------------- list <-> mask
+
+def lists_from_masks(masks: dict, n_heads: int, n_blocks: int):
+    """Ascending per-row index lists in the triangular packing: row (h, i)
+    starts at i (i + 1) / 2 and holds counts[h][i] block ids."""
+    cap = n_blocks * (n_blocks + 1) // 2
+    counts = np.zeros((n_heads, n_blocks), dtype=np.int32)
+    indices = np.full((n_heads, cap), -1, dtype=np.int32)
+    for (h, i), row in masks.items():
+        ids = np.nonzero(np.asarray(row, dtype=bool))[0]
+        counts[h, i] = len(ids)
+        base = i * (i + 1) // 2
+        indices[h, base:base + len(ids)] = ids
+    return counts, indices
+
+
+def masks_from_lists(counts, indices, rows):
+    """Inverse of lists_from_masks for the given (h, i) rows."""
+    out = {}
+    for (h, i) in rows:
+        base = i * (i + 1) // 2
+        row = np.zeros(i + 1, dtype=bool)
+        row[np.asarray(indices[h, base:base + counts[h, i]], dtype=np.int64)] = True
+        out[(h, i)] = row
+    return out

@@ -1,0 +1,371 @@
+"""Pins of the float64 oracle against what the paper and mathematics fix.
+
+Each test names the passage it follows.  None of them compares the oracle with
+itself: expected values are hand-worked closed forms (tests/golden), library
+routines for special cases, inequalities, invariances or brute force.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from tests.conftest import GOLDEN
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _case_rows(case, tau_base=None, tau_rescue=None):
+    K = np.array(case["keys"], dtype=np.float64)[None]
+    Q = np.array(case["queries"], dtype=np.float64)[None]
+    B = case["block_size"]
+    C, R = oracle.block_stats(K, B)
+    beta, rq = oracle.rescue_coefficients(R)
+    rows = oracle.select(Q, C, R, beta, B,
+                         case.get("tau_base", 0.5) if tau_base is None else tau_base,
+                         case.get("tau_rescue", 0.5) if tau_rescue is None else tau_rescue,
+                         case["n_sink"], case["n_local"], case["n_recent"])
+    return C, R, beta, rq, rows
+
+
+def _ids(mask):
+    return [int(x) for x in np.nonzero(mask)[0]]
+
+
+# ------------------------------------------------------------ hand-worked cases
+
+def test_needle_case():
+    """Sec. 2.3 / 3.1 / 3.2: a needle diluted by noise is lost by the centroid
+    score and recovered by the radius uplift."""
+    case = _load("needle_case.json")
+    ex = case["expected"]
+    C, R, beta, rq, rows = _case_rows(case)
+    np.testing.assert_allclose(C[0], ex["centroids"], atol=1e-15)
+    np.testing.assert_allclose(R[0], ex["radii"], atol=1e-15)
+    np.testing.assert_allclose(rq[0], [ex["r_low"], ex["r_high"]], rtol=1e-14)
+    np.testing.assert_allclose(beta[0], ex["beta"], atol=1e-15)
+    r2 = rows[(0, 2)]
+    np.testing.assert_allclose(np.exp(r2["log_s_base"] - r2["log_s_base"].max()), ex["row2_base_ratio"], rtol=1e-12)
+    np.testing.assert_allclose(np.exp(r2["log_s_rescue"] - r2["log_s_rescue"].max()), ex["row2_rescue_ratio"], rtol=1e-12)
+    assert _ids(r2["base"]) == ex["row2_base"]
+    assert _ids(r2["rescue"]) == ex["row2_rescue"]
+    assert [_ids(rows[(0, i)]["final"]) for i in range(3)] == ex["final_rows"]
+    assert _ids(r2["base"] | r2["forced"]) == ex["centroid_only_row2"]
+    # The needle's logit meets the full L2 bound exactly (App. E).
+    q = np.array(case["queries"][8], dtype=np.float64)
+    needle = np.array(case["keys"][0], dtype=np.float64)
+    assert q @ needle == ex["needle_logit"]
+    assert q @ C[0, 0] + np.linalg.norm(q) * R[0, 0] == ex["needle_l2_bound"]
+
+
+def test_aggregation_sums_exponentials_over_tokens():
+    """Sec. 3.2 Eq. block_aggregation: the block score sums exp(logit/sqrt d)
+    over the block's tokens (not a max, not a mean logit)."""
+    case = _load("aggregation_case.json")
+    ex = case["expected"]
+    C, R, beta, rq, rows = _case_rows(case, 0.15, 0.15)
+    np.testing.assert_allclose(beta[0], ex["beta"], atol=0)
+    r1 = rows[(0, 1)]
+    for key in ("log_s_base", "log_s_rescue"):
+        np.testing.assert_allclose(np.exp(r1[key] - r1[key].max()), ex["row1_ratio"], rtol=1e-12)
+    assert _ids(r1["final"]) == ex["row1_final_tau_0.15"]
+    _, _, _, _, rows16 = _case_rows(case, 0.16, 0.16)
+    assert _ids(rows16[(0, 1)]["final"]) == ex["row1_final_tau_0.16"]
+
+
+def test_fractional_beta_case():
+    """Sec. 3.1 Eq. beta and Sec. 3.2 Eq. rescue_score with 0 < beta < 1."""
+    case = _load("fractional_beta_case.json")
+    ex = case["expected"]
+    C, R, beta, rq, rows = _case_rows(case)
+    np.testing.assert_allclose(R[0], ex["radii"], atol=1e-15)
+    np.testing.assert_allclose(rq[0], [ex["r_low"], ex["r_high"]], rtol=1e-14)
+    np.testing.assert_allclose(beta[0], ex["beta"], rtol=1e-12, atol=1e-15)
+    r4 = rows[(0, 4)]
+    np.testing.assert_allclose(np.exp(r4["log_s_base"] - r4["log_s_base"].max()), ex["row4_base_ratio"], rtol=1e-12)
+    np.testing.assert_allclose(np.exp(r4["log_s_rescue"] - r4["log_s_rescue"].max()), ex["row4_rescue_ratio"], rtol=1e-12)
+    assert _ids(r4["final"]) == ex["row4_final"]
+
+
+@pytest.mark.parametrize("idx", [0, 1])
+def test_quantiles_and_beta_hand_computed(idx):
+    """Sec. 3.1: r_low / r_high are the 0.5 / 0.9 quantiles; Eq. beta."""
+    case = _load("quantiles.json")["cases"][idx]
+    R = np.array(case["radii"], dtype=np.float64)[None]
+    beta, rq = oracle.rescue_coefficients(R)
+    np.testing.assert_allclose(rq[0], [case["r_low"], case["r_high"]], rtol=1e-14)
+    np.testing.assert_allclose(beta[0], case["beta"], rtol=1e-12, atol=1e-15)
+
+
+def test_quantile_matches_library_linear_rule():
+    """The type-7 reading equals numpy's default ('linear') quantile."""
+    rng = np.random.default_rng(3)
+    for n in (1, 2, 3, 7, 64, 1000, 1023):
+        x = rng.lognormal(0, 0.7, size=n)
+        for p in (0.5, 0.9):
+            assert oracle.quantile_type7(x, p) == pytest.approx(np.quantile(x, p), rel=1e-14, abs=0)
+
+
+# ------------------------------------------------------------ geometry (Sec. 2.4, App. E)
+
+def test_full_l2_bound_holds_for_every_key():
+    """Sec. 2.4 Eq. full_l2_bound: max_k q.k <= q.c_b + |q| r_b, unattenuated."""
+    rng = np.random.default_rng(7)
+    d, B, N = 16, 8, 8 * 9 + 5
+    scales = np.repeat(rng.lognormal(0, 1.0, size=-(-N // B)), B)[:N]
+    K = rng.standard_normal((1, N, d)) * scales[None, :, None] + rng.standard_normal(d)
+    C, R = oracle.block_stats(K, B)
+    Qs = rng.standard_normal((50, d)) * 3
+    for b, (s, e) in enumerate(oracle.block_ranges(N, B)):
+        logits = Qs @ K[0, s:e].T
+        bound = Qs @ C[0, b] + np.linalg.norm(Qs, axis=1) * R[0, b]
+        assert (logits.max(axis=1) <= bound + 1e-10).all()
+        # The key that defines the radius, queried along its own deviation,
+        # meets the bound exactly (the ball is tight).
+        far = int(np.argmax(np.linalg.norm(K[0, s:e] - C[0, b], axis=1)))
+        u = K[0, s + far] - C[0, b]
+        assert u @ K[0, s + far] == pytest.approx(u @ C[0, b] + np.linalg.norm(u) * R[0, b], rel=1e-12)
+
+
+def test_attenuated_score_is_not_a_bound():
+    """App. E: K = {-u, u}, q = u gives c = 0, r = 1, max logit 1, rescue logit beta."""
+    u = np.array([0.6, 0.8, 0.0])
+    K = np.stack([-u, u])[None]
+    C, R = oracle.block_stats(K, 2)
+    np.testing.assert_allclose(C[0, 0], 0, atol=1e-15)
+    assert R[0, 0] == pytest.approx(1.0, rel=1e-15)
+    for b in (0.0, 0.3, 1.0):
+        lb, lr = oracle.branch_logits(u[None], C[0], R[0], np.array([b]), 1)
+        assert lb[0, 0] == pytest.approx(0.0, abs=1e-15)
+        assert lr[0, 0] == pytest.approx(b, rel=1e-14, abs=1e-15)
+        assert (lr[0, 0] < (K[0] @ u).max()) == (b < 1.0)
+
+
+def _box_bound(q, K):
+    lo, hi = K.min(axis=0), K.max(axis=0)
+    return np.maximum(q * lo, q * hi).sum()
+
+
+def test_l2_ball_versus_coordinate_box_examples():
+    """App. E, Eq. quest_box: neither bound dominates (two 2-D examples)."""
+    e1, e2 = np.eye(2)
+    K = np.stack([e1, -e1, e2, -e2])
+    C, R = oracle.block_stats(K[None], 4)
+    q = np.array([1.0, 1.0])
+    assert q @ C[0, 0] + np.linalg.norm(q) * R[0, 0] == pytest.approx(math.sqrt(2), rel=1e-15)
+    assert _box_bound(q, K) == pytest.approx(2.0)
+    eps = 0.25
+    K = np.stack([e1, -e1, eps * e2, -eps * e2])
+    C, R = oracle.block_stats(K[None], 4)
+    q = e2
+    assert R[0, 0] == pytest.approx(1.0, rel=1e-15)
+    assert q @ C[0, 0] + np.linalg.norm(q) * R[0, 0] == pytest.approx(1.0, rel=1e-15)
+    assert _box_bound(q, K) == pytest.approx(eps)
+
+
+def test_translation_and_rotation_invariance():
+    """App. E: q.c_b and r_b are unchanged under a common orthogonal map; a
+    common shift moves c_b and leaves r_b unchanged."""
+    rng = np.random.default_rng(11)
+    d, B, N = 12, 5, 23
+    K = rng.standard_normal((1, N, d)) * 2
+    q = rng.standard_normal(d)
+    C, R = oracle.block_stats(K, B)
+    Qm, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    C2, R2 = oracle.block_stats(K @ Qm.T, B)
+    np.testing.assert_allclose(R2, R, rtol=1e-12)
+    np.testing.assert_allclose(C2[0] @ (Qm @ q), C[0] @ q, rtol=1e-10, atol=1e-12)
+    shift = rng.standard_normal(d) * 5
+    C3, R3 = oracle.block_stats(K + shift, B)
+    np.testing.assert_allclose(R3, R, rtol=1e-10)
+    np.testing.assert_allclose(C3, C + shift, rtol=1e-12, atol=1e-12)
+
+
+def test_partial_last_block_uses_its_own_count():
+    """Sec. 3.1: c_b divides by |K_b|; a last block of one key has r = 0."""
+    K = np.arange(5 * 3, dtype=np.float64).reshape(1, 5, 3)
+    C, R = oracle.block_stats(K, 4)
+    np.testing.assert_allclose(C[0, 0], K[0, :4].mean(axis=0))
+    np.testing.assert_allclose(C[0, 1], K[0, 4])
+    assert R[0, 1] == 0.0
+
+
+# ------------------------------------------------------------ scoring / selection
+
+def _random_case(seed=0, d=8, B=4, N=4 * 7 + 2, Hq=4, Hkv=2):
+    rng = np.random.default_rng(seed)
+    scales = np.repeat(rng.lognormal(0, 0.8, size=-(-N // B)), B)[:N]
+    K = rng.standard_normal((Hkv, N, d)) * scales[None, :, None] + 2 * rng.standard_normal((Hkv, 1, d))
+    Q = rng.standard_normal((Hq, N, d)) * 1.5
+    C, R = oracle.block_stats(K, B)
+    beta, _ = oracle.rescue_coefficients(R)
+    return Q, K, C, R, beta, B
+
+
+def test_rescue_logit_dominates_base_and_equals_l2_bound_at_beta_one():
+    """Sec. 3.2: l_rescue >= l_base; with beta = 1 it equals U^L2."""
+    Q, K, C, R, beta, B = _random_case()
+    lb, lr = oracle.branch_logits(Q[0, :B], C[0], R[0], beta[0], C.shape[1])
+    assert (lr >= lb).all()
+    lb1, lr1 = oracle.branch_logits(Q[0, :B], C[0], R[0], np.ones_like(beta[0]), C.shape[1])
+    bound = Q[0, :B] @ C[0].T + np.linalg.norm(Q[0, :B], axis=1)[:, None] * R[0][None, :]
+    np.testing.assert_allclose(lr1, bound, rtol=1e-13)
+
+
+def test_shift_choice_does_not_change_masks():
+    """Sec. 3.2: the shared shift cancels; per-block log-sum-exp gives the same
+    relative scores and masks."""
+    Q, K, C, R, beta, B = _random_case(seed=5)
+    M = C.shape[1]
+    for i in range(M):
+        s, e = i * B, min((i + 1) * B, Q.shape[1])
+        lb, lr = oracle.branch_logits(Q[1, s:e], C[0], R[0], beta[0], i + 1)
+        ref_b, ref_r = oracle.branch_log_scores(Q[1, s:e], C[0], R[0], beta[0], i + 1)
+        for logits, ref in ((lb, ref_b), (lr, ref_r)):
+            x = logits / math.sqrt(Q.shape[2])
+            col_max = x.max(axis=0)
+            lse = col_max + np.log(np.exp(x - col_max).sum(axis=0))
+            np.testing.assert_allclose(lse - lse.max(), ref - ref.max(), atol=1e-12)
+
+
+def test_brute_force_scores_on_tiny_input():
+    """Eq. base_score / rescue_score / block_aggregation by explicit loops."""
+    Q, K, C, R, beta, B = _random_case(seed=9, d=3, B=3, N=10, Hq=1, Hkv=1)
+    i = 3
+    toks = range(i * B, min((i + 1) * B, Q.shape[1]))
+    S_b, S_r = [], []
+    for b in range(i + 1):
+        sb = sr = 0.0
+        for t in toks:
+            dot = sum(Q[0, t, j] * C[0, b, j] for j in range(3))
+            nq = math.sqrt(sum(Q[0, t, j] ** 2 for j in range(3)))
+            sb += math.exp(dot / math.sqrt(3))
+            sr += math.exp((dot + nq * R[0, b] * beta[0, b]) / math.sqrt(3))
+        S_b.append(sb)
+        S_r.append(sr)
+    lb, lr = oracle.branch_log_scores(Q[0, list(toks)], C[0], R[0], beta[0], i + 1)
+    np.testing.assert_allclose(lb - lb.max(), np.log(S_b) - max(np.log(S_b)), atol=1e-12)
+    np.testing.assert_allclose(lr - lr.max(), np.log(S_r) - max(np.log(S_r)), atol=1e-12)
+
+
+def test_threshold_monotonicity():
+    """App. E / Sec. 3.2: lowering a threshold cannot shrink its branch's mask."""
+    Q, K, C, R, beta, B = _random_case(seed=2)
+    taus = [1.0, 0.95, 0.8, 0.5, 0.2, 0.05, 0.0]
+    prev = None
+    for t in taus:
+        rows = oracle.select(Q, C, R, beta, B, t, t, 0, 1, 0)
+        cur = {k: (v["base"], v["rescue"]) for k, v in rows.items()}
+        if prev is not None:
+            for k in cur:
+                assert (cur[k][0] >= prev[k][0]).all() and (cur[k][1] >= prev[k][1]).all()
+        prev = cur
+
+
+def test_alpha_one_keeps_argmax_and_alpha_zero_keeps_all():
+    """Eq. branch_thresholds special cases."""
+    Q, K, C, R, beta, B = _random_case(seed=4)
+    rows = oracle.select(Q, C, R, beta, B, 1.0, 1.0, 0, 1, 0)
+    for (h, i), r in rows.items():
+        assert _ids(r["base"]) == [int(np.argmax(r["log_s_base"]))]
+        assert _ids(r["rescue"]) == [int(np.argmax(r["log_s_rescue"]))]
+    rows = oracle.select(Q, C, R, beta, B, 0.0, 0.0, 0, 1, 0)
+    for (h, i), r in rows.items():
+        assert r["final"].all() and r["final"].shape == (i + 1,)
+
+
+def test_ties_are_all_kept():
+    """Eq. branch_thresholds is inclusive: zero queries tie every candidate."""
+    Q, K, C, R, beta, B = _random_case(seed=8)
+    Q[:, :2 * B] = 0.0
+    rows = oracle.select(Q, C, R, beta, B, 0.99, 0.99, 0, 1, 0, rows=[(0, 1), (3, 1)])
+    for r in rows.values():
+        assert r["base"].all() and r["rescue"].all()
+
+
+@pytest.mark.parametrize("sink,local,recent", [(1, 2, 0), (0, 1, 0), (2, 3, 1), (1, 1, 2)])
+def test_forced_blocks_always_present(sink, local, recent):
+    """Sec. 3.2 union with forced sink, local-window and recent blocks."""
+    Q, K, C, R, beta, B = _random_case(seed=6)
+    M = C.shape[1]
+    rows = oracle.select(Q, C, R, beta, B, 1.0, 1.0, sink, local, recent)
+    for (h, i), r in rows.items():
+        f = r["final"]
+        assert f[:min(sink, i + 1)].all()
+        assert f[max(0, i - local + 1):i + 1].all()
+        if i >= M - recent:
+            assert f.all()
+
+
+def test_union_differs_from_both_branches_in_needle_case():
+    """Sec. 3.2 / App. E: rescue-only selection can drop base-selected blocks."""
+    case = _load("needle_case.json")
+    _, _, _, _, rows = _case_rows(case)
+    r = rows[(0, 2)]
+    assert not (r["base"] <= r["rescue"]).all()
+    assert (r["final"] != r["base"]).any() and (r["final"] != r["rescue"]).any()
+
+
+# ------------------------------------------------------------ attention (Eq. (1), Sec. 3.3)
+
+def test_full_selection_equals_brute_force_dense_attention():
+    """alpha = 0 keeps every causal block, so sparse attention reduces to the
+    dense causal softmax attention of Eq. (1), computed here by brute force."""
+    rng = np.random.default_rng(1)
+    d, B, N = 8, 4, 4 * 5 + 3
+    Q, K, V = (rng.standard_normal((N, d)) for _ in range(3))
+    C, R = oracle.block_stats(K[None], B)
+    beta, _ = oracle.rescue_coefficients(R)
+    rows = oracle.select(Q[None], C, R, beta, B, 0.0, 0.0, 0, 1, 0)
+    lists = {i: _ids(rows[(0, i)]["final"]) for i in range(C.shape[1])}
+    sparse = np.concatenate([oracle.attention_on_mask(Q, K, V, B, lists)[i] for i in sorted(lists)])
+    brute = np.zeros((N, d))
+    for t in range(N):
+        w = [math.exp(sum(Q[t, j] * K[s, j] for j in range(d)) / math.sqrt(d)) for s in range(t + 1)]
+        z = sum(w)
+        for s in range(t + 1):
+            brute[t] += w[s] / z * V[s]
+    np.testing.assert_allclose(sparse, brute, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(oracle.dense_causal_attention(Q, K, V), brute, rtol=1e-11, atol=1e-12)
+
+
+def test_attention_invariances():
+    """Softmax over retained keys: a constant added to every key leaves the
+    output unchanged; the output is linear in V; one retained key returns its
+    value; a query with no retained causal key gets zeros."""
+    rng = np.random.default_rng(12)
+    d, B, N = 6, 4, 16
+    Q, K, V, V2 = (rng.standard_normal((N, d)) for _ in range(4))
+    lists = {0: [0], 1: [0, 1], 2: [1, 2], 3: [0, 3]}
+    o1 = oracle.attention_on_mask(Q, K, V, B, lists)
+    o2 = oracle.attention_on_mask(Q, K + rng.standard_normal(d), V, B, lists)
+    for i in lists:
+        np.testing.assert_allclose(o1[i], o2[i], rtol=1e-11, atol=1e-12)
+    a, b = 0.7, -1.3
+    o3 = oracle.attention_on_mask(Q, K, a * V + b * V2, B, lists)
+    o4 = oracle.attention_on_mask(Q, K, V2, B, lists)
+    for i in lists:
+        np.testing.assert_allclose(o3[i], a * o1[i] + b * o4[i], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(o1[0][0], V[0], rtol=1e-14)
+    assert not oracle.attention_rows(Q, K, V, B, 2, [3]).any()
+
+
+def test_density_counts_selected_pairs_once():
+    """Sec. 4.4 Eq. actual_density on hand-counted rows."""
+    rows = [np.array([True]), np.array([True, False]), np.array([True, False, True])]
+    assert oracle.density(rows) == pytest.approx(4 / 6)
+    assert oracle.density([np.ones(k, bool) for k in range(1, 9)]) == 1.0
+
+
+def test_list_mask_roundtrip():
+    rows = {(0, 0): np.array([True]), (0, 2): np.array([True, False, True]), (1, 1): np.array([False, True])}
+    counts, idx = oracle.lists_from_masks(rows, 2, 3)
+    back = oracle.masks_from_lists(counts, idx, rows.keys())
+    for k in rows:
+        assert (back[k] == rows[k]).all()
