@@ -1,0 +1,149 @@
+/*
+ * rbs.h -- C ABI of the RBS-Attention sparse-prefill path on MI355X (gfx950).
+ *
+ * Three calls follow the method's problem statement (Sec. 3, Algorithm 1):
+ *
+ *   rbs_block_stats     key-block centroids, radii, per-KV-head radius
+ *                       quantiles and rescue coefficients    (Sec. 3.1)
+ *   rbs_select          dual-branch block selection, compacted to per
+ *                       query-block key-block index lists     (Sec. 3.2)
+ *   rbs_sparse_prefill  causal GQA block-sparse attention over the selected
+ *                       blocks                                (Sec. 3.3)
+ *
+ * Conventions shared by every call
+ *   - Tensors are dense, row-major, in device memory:
+ *       Q, O   bf16 [H_q][N][d]      K, V   bf16 [H_kv][N][d]
+ *     d (head_dim) must be 128.  Query head h reads KV head h / (H_q / H_kv).
+ *   - Blocks: M = ceil(N / B) blocks of B tokens (the last may be short);
+ *     query and key blocks use the same B, one of 64, 128, 256.
+ *     Limits: 1 <= N <= 262144, M <= 4096.
+ *   - The caller owns and allocates every buffer.  The library allocates
+ *     nothing, never synchronises, and enqueues its kernels on `stream`
+ *     (a hipStream_t; NULL means the default stream).  Results are valid once
+ *     the stream reaches them.
+ *   - Every device pointer must be 16-byte aligned.
+ *   - Arguments are validated on the host before anything is launched; a
+ *     failing call returns a status code, launches nothing and writes nothing.
+ *     RBS_ERR_HIP means a launch was rejected by the runtime.
+ *   - Calls on distinct streams do not share state, except rbs_block_stats's
+ *     completion counters (one array per concurrent stats call).
+ */
+#ifndef RBS_H
+#define RBS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  RBS_OK = 0,
+  RBS_ERR_NULL = 1,        /* a required pointer is NULL                      */
+  RBS_ERR_SHAPE = 2,       /* N < 1, H < 1, H_q % H_kv != 0, limits exceeded  */
+  RBS_ERR_UNSUPPORTED = 3, /* head_dim != 128 or block size not 64/128/256    */
+  RBS_ERR_ARG = 4,         /* tau outside [0,1], negative or zero window, ... */
+  RBS_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned         */
+  RBS_ERR_HIP = 6          /* the HIP runtime rejected a kernel launch        */
+};
+
+typedef struct {
+  int32_t n_tokens;   /* N                          */
+  int32_t n_q_heads;  /* H_q                        */
+  int32_t n_kv_heads; /* H_kv, divides H_q          */
+  int32_t head_dim;   /* d, must be 128             */
+  int32_t block_size; /* B: 64, 128 or 256          */
+} rbs_shape;
+
+/*
+ * Outputs of rbs_block_stats and the input of rbs_select (all device memory).
+ *
+ *   centroids  fp32 [H_kv][M][d]   c_b = mean of block b's keys (Sec. 3.1)
+ *   radii      fp32 [H_kv][M]      r_b = max over the block of |k - c_b|_2
+ *   beta       fp32 [H_kv][M]      beta_b = clamp((r_b - r_low)/(r_high - r_low), 0, 1),
+ *                                  Sec. 3.1 Eq. beta; when r_high <= r_low,
+ *                                  beta_b = 1 if r_b > r_low else 0
+ *   quantiles  fp32 [H_kv][2]      r_low, r_high: 0.5 and 0.9 quantiles of the
+ *                                  head's M radii (linear interpolation between
+ *                                  order statistics)
+ *   summary    rbs_summary_bytes() bytes: the select-ready copy of the summaries
+ *              (centroids as f16 pre-scaled by log2(e)/sqrt(d), and the
+ *              per-block rescue uplift r_b beta_b log2(e)/sqrt(d)).  Opaque;
+ *              written by rbs_block_stats, read by rbs_select.
+ *   counters   uint32 [H_kv] completion counters.  Must be zero before the
+ *              first rbs_block_stats call that uses them; every call leaves
+ *              them zero again.  Do not share one array between stats calls
+ *              that may run concurrently.
+ */
+typedef struct {
+  float* centroids;
+  float* radii;
+  float* beta;
+  float* quantiles;
+  void* summary;
+  uint32_t* counters;
+} rbs_stats;
+
+/* Bytes needed for rbs_stats.summary (0 if the shape is invalid). */
+size_t rbs_summary_bytes(const rbs_shape* shape);
+
+/* Number of int32 slots per query head in an index-list buffer: M (M + 1) / 2.
+ * Row i of head h starts at h * rbs_index_capacity(M) + i (i + 1) / 2 and has
+ * room for i + 1 entries. */
+int64_t rbs_index_capacity(int32_t n_blocks);
+
+/*
+ * Stage 1 (Sec. 3.1; Algorithm 1, statistics loops).
+ * K: bf16 [H_kv][N][d].  Fills every field of *stats (one pass over K; the
+ * quantiles and beta are computed by the last workgroup to finish each head).
+ */
+int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stats, void* stream);
+
+/*
+ * Stage 2 (Sec. 3.2; Algorithm 1, selection loop).
+ * For every query head h and query block i, over candidate key blocks 0..i:
+ *   base logit  q . c_b, rescue logit q . c_b + |q|_2 r_b beta_b   (Eqs. base/rescue score)
+ *   S^z_b = sum over the block's tokens of exp(logit / sqrt(d))   (Eq. block_aggregation)
+ *   M^z   = { b : S^z_b >= tau_z * max_b' S^z_b' }                (Eq. branch_thresholds)
+ *   final = M^base U M^rescue U forced, where forced holds the first n_sink
+ *           blocks, the n_local blocks ending at the diagonal, and every
+ *           candidate when i >= M - n_recent.
+ * Q: bf16 [H_q][N][d]; stats: filled by rbs_block_stats on the same K and shape.
+ * tau_base, tau_rescue in [0, 1]; n_sink >= 0, n_local >= 1, n_recent >= 0.
+ * Outputs: counts int32 [H_q][M]; indices int32 [H_q][rbs_index_capacity(M)],
+ * row (h, i) ascending, unique, all <= i, always containing i.  Slots past
+ * counts[h][i] are left untouched.
+ */
+int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats,
+               float tau_base, float tau_rescue, int32_t n_sink, int32_t n_local,
+               int32_t n_recent, int32_t* counts, int32_t* indices, void* stream);
+
+/*
+ * Stage 3 (Sec. 3.3; Algorithm 1, last step).
+ * For every query token t of query block i and head h:
+ *   O_t = sum_j softmax_j(q_t . k_j * scale) v_j over the keys j <= t of the
+ *   blocks listed in row (h, i); bf16 inputs, fp32 accumulation and softmax,
+ *   O rounded to bf16 (nearest even).
+ * counts/indices: as written by rbs_select or rbs_dense_indices.  The lists are
+ * trusted: entries are clamped to [0, i] so that no access leaves the buffers,
+ * but the result of a malformed list is unspecified.
+ * softmax_scale <= 0 selects 1/sqrt(d).  lse (optional, NULL to skip): fp32
+ * [H_q][N] natural-log sum of exp(scaled logits) per query (-inf when a query
+ * has no retained key, in which case its output row is zero).
+ */
+int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, const void* V,
+                       const int32_t* counts, const int32_t* indices, float softmax_scale,
+                       void* O, float* lse, void* stream);
+
+/* Full causal lists (every block 0..i for every row): the dense path. */
+int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream);
+
+/* Static description of a status code. */
+const char* rbs_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RBS_H */

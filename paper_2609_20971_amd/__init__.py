@@ -1,0 +1,25 @@
+"""RBS-Attention sparse prefill on MI355X (gfx950): HIP kernels behind a C ABI.
+
+    stats = rbs_block_stats(shape, K)                                  # Sec. 3.1
+    counts, indices = rbs_select(shape, Q, stats, tau_b, tau_r, sink, local, recent)  # Sec. 3.2
+    O = rbs_sparse_prefill(shape, Q, K, V, counts, indices)            # Sec. 3.3
+"""
+
+from ._lib import (  # noqa: F401
+    BlockStats,
+    RbsError,
+    allocate_lists,
+    load,
+    make_shape,
+    n_blocks,
+    rbs_block_stats,
+    rbs_dense_indices,
+    rbs_index_capacity,
+    rbs_select,
+    rbs_shape,
+    rbs_sparse_prefill,
+    rbs_stats,
+    rbs_status_str,
+    rbs_summary_bytes,
+    LIB_PATH,
+)

@@ -1,0 +1,188 @@
+"""ctypes binding of librbs.so (the C ABI in include/rbs.h).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  PyTorch provides device memory and the current stream.  The binding
+refuses to run when the library is not built; there is no CPU fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librbs.so")
+
+RBS_OK, RBS_ERR_NULL, RBS_ERR_SHAPE, RBS_ERR_UNSUPPORTED, RBS_ERR_ARG, RBS_ERR_ALIGN, RBS_ERR_HIP = range(7)
+
+
+class RbsError(RuntimeError):
+    def __init__(self, fn: str, status: int, message: str):
+        super().__init__(f"{fn} failed with status {status}: {message}")
+        self.status = status
+
+
+class rbs_shape(ctypes.Structure):
+    _fields_ = [
+        ("n_tokens", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+    ]
+
+
+class rbs_stats(ctypes.Structure):
+    _fields_ = [
+        ("centroids", ctypes.c_void_p),
+        ("radii", ctypes.c_void_p),
+        ("beta", ctypes.c_void_p),
+        ("quantiles", ctypes.c_void_p),
+        ("summary", ctypes.c_void_p),
+        ("counters", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load librbs.so once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_20971_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, F32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_int64, ctypes.c_size_t
+    SP = ctypes.POINTER(rbs_shape)
+    lib.rbs_summary_bytes.argtypes = [SP]
+    lib.rbs_summary_bytes.restype = SZ
+    lib.rbs_index_capacity.argtypes = [I32]
+    lib.rbs_index_capacity.restype = I64
+    lib.rbs_block_stats.argtypes = [SP, P, ctypes.POINTER(rbs_stats), P]
+    lib.rbs_block_stats.restype = ctypes.c_int
+    lib.rbs_select.argtypes = [SP, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, P, P, P]
+    lib.rbs_select.restype = ctypes.c_int
+    lib.rbs_sparse_prefill.argtypes = [SP, P, P, P, P, P, F32, P, P, P]
+    lib.rbs_sparse_prefill.restype = ctypes.c_int
+    lib.rbs_dense_indices.argtypes = [SP, P, P, P]
+    lib.rbs_dense_indices.restype = ctypes.c_int
+    lib.rbs_status_str.argtypes = [ctypes.c_int]
+    lib.rbs_status_str.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def rbs_status_str(status: int) -> str:
+    return load().rbs_status_str(status).decode()
+
+
+def _check(fn: str, status: int):
+    if status != RBS_OK:
+        raise RbsError(fn, status, rbs_status_str(status))
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def make_shape(n_tokens: int, n_q_heads: int, n_kv_heads: int, block_size: int, head_dim: int = 128) -> rbs_shape:
+    return rbs_shape(n_tokens, n_q_heads, n_kv_heads, head_dim, block_size)
+
+
+def n_blocks(shape: rbs_shape) -> int:
+    return -(-shape.n_tokens // shape.block_size)
+
+
+def rbs_index_capacity(m: int) -> int:
+    return int(load().rbs_index_capacity(m))
+
+
+def rbs_summary_bytes(shape: rbs_shape) -> int:
+    return int(load().rbs_summary_bytes(ctypes.byref(shape)))
+
+
+@dataclass
+class BlockStats:
+    """Device buffers of rbs_stats (allocated by the caller: here, torch)."""
+    shape: rbs_shape
+    centroids: torch.Tensor   # fp32 [H_kv][M][d]
+    radii: torch.Tensor       # fp32 [H_kv][M]
+    beta: torch.Tensor        # fp32 [H_kv][M]
+    quantiles: torch.Tensor   # fp32 [H_kv][2]
+    summary: torch.Tensor     # uint8 [rbs_summary_bytes]
+    counters: torch.Tensor    # int32 [H_kv], zero between calls
+
+    @classmethod
+    def allocate(cls, shape: rbs_shape, device="cuda") -> "BlockStats":
+        m, hk, d = n_blocks(shape), shape.n_kv_heads, shape.head_dim
+        f32 = dict(dtype=torch.float32, device=device)
+        nbytes = rbs_summary_bytes(shape)
+        if nbytes == 0:
+            raise RbsError("rbs_summary_bytes", RBS_ERR_SHAPE, "invalid shape")
+        return cls(shape, torch.empty((hk, m, d), **f32), torch.empty((hk, m), **f32),
+                   torch.empty((hk, m), **f32), torch.empty((hk, 2), **f32),
+                   torch.empty(nbytes, dtype=torch.uint8, device=device),
+                   torch.zeros(max(hk, 4), dtype=torch.int32, device=device))
+
+    def as_c(self) -> rbs_stats:
+        return rbs_stats(_ptr(self.centroids), _ptr(self.radii), _ptr(self.beta), _ptr(self.quantiles),
+                         _ptr(self.summary), _ptr(self.counters))
+
+
+def rbs_block_stats(shape: rbs_shape, K: torch.Tensor, stats: BlockStats | None = None, stream=None) -> BlockStats:
+    """Stage 1: centroids, radii, radius quantiles and beta of every key block."""
+    if stats is None:
+        stats = BlockStats.allocate(shape, K.device)
+    c = stats.as_c()
+    _check("rbs_block_stats", load().rbs_block_stats(ctypes.byref(shape), _ptr(K), ctypes.byref(c), _stream(stream)))
+    return stats
+
+
+def allocate_lists(shape: rbs_shape, device="cuda"):
+    m = n_blocks(shape)
+    counts = torch.empty((shape.n_q_heads, m), dtype=torch.int32, device=device)
+    indices = torch.empty((shape.n_q_heads, rbs_index_capacity(m)), dtype=torch.int32, device=device)
+    return counts, indices
+
+
+def rbs_select(shape: rbs_shape, Q: torch.Tensor, stats: BlockStats, tau_base: float, tau_rescue: float,
+               n_sink: int, n_local: int, n_recent: int, counts=None, indices=None, stream=None):
+    """Stage 2: per (query head, query block) ascending key-block index lists."""
+    if counts is None or indices is None:
+        counts, indices = allocate_lists(shape, Q.device)
+    c = stats.as_c()
+    _check("rbs_select", load().rbs_select(ctypes.byref(shape), _ptr(Q), ctypes.byref(c), float(tau_base),
+                                           float(tau_rescue), int(n_sink), int(n_local), int(n_recent),
+                                           _ptr(counts), _ptr(indices), _stream(stream)))
+    return counts, indices
+
+
+def rbs_sparse_prefill(shape: rbs_shape, Q, K, V, counts, indices, softmax_scale: float = 0.0, O=None,
+                       lse=None, stream=None):
+    """Stage 3: causal GQA block-sparse attention; returns O (bf16 [H_q][N][d])."""
+    if O is None:
+        O = torch.empty_like(Q)
+    _check("rbs_sparse_prefill", load().rbs_sparse_prefill(ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V),
+                                                           _ptr(counts), _ptr(indices), float(softmax_scale),
+                                                           _ptr(O), _ptr(lse), _stream(stream)))
+    return O
+
+
+def rbs_dense_indices(shape: rbs_shape, counts=None, indices=None, stream=None, device="cuda"):
+    """Full causal lists: the dense path through the same attention kernel."""
+    if counts is None or indices is None:
+        counts, indices = allocate_lists(shape, device)
+    _check("rbs_dense_indices", load().rbs_dense_indices(ctypes.byref(shape), _ptr(counts), _ptr(indices),
+                                                         _stream(stream)))
+    return counts, indices

@@ -1,0 +1,165 @@
+// C ABI of librbs: argument validation, then kernel launches on the caller's
+// stream.  Validation is host-only and happens before any HIP call, so a
+// rejected call launches and writes nothing.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/rbs.h"
+#include "rbs_launch.hpp"
+
+namespace {
+
+constexpr int kMaxTokens = 262144;
+constexpr int kMaxBlocks = 4096;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int blocks_of(const rbs_shape* s) { return (s->n_tokens + s->block_size - 1) / s->block_size; }
+
+int check_shape(const rbs_shape* s) {
+  if (s == nullptr) return RBS_ERR_NULL;
+  if (s->head_dim != 128) return RBS_ERR_UNSUPPORTED;
+  if (s->block_size != 64 && s->block_size != 128 && s->block_size != 256) return RBS_ERR_UNSUPPORTED;
+  if (s->n_tokens < 1 || s->n_tokens > kMaxTokens) return RBS_ERR_SHAPE;
+  if (s->n_q_heads < 1 || s->n_kv_heads < 1) return RBS_ERR_SHAPE;
+  if (s->n_q_heads % s->n_kv_heads != 0) return RBS_ERR_SHAPE;
+  if (blocks_of(s) > kMaxBlocks) return RBS_ERR_SHAPE;
+  if ((int64_t)s->n_q_heads * blocks_of(s) > INT32_MAX / 2) return RBS_ERR_SHAPE;
+  return RBS_OK;
+}
+
+int check_stats_ptrs(const rbs_stats* st) {
+  if (st == nullptr || st->centroids == nullptr || st->radii == nullptr || st->beta == nullptr ||
+      st->quantiles == nullptr || st->summary == nullptr || st->counters == nullptr)
+    return RBS_ERR_NULL;
+  if (!aligned16(st->centroids) || !aligned16(st->radii) || !aligned16(st->beta) || !aligned16(st->quantiles) ||
+      !aligned16(st->summary) || !aligned16(st->counters))
+    return RBS_ERR_ALIGN;
+  return RBS_OK;
+}
+
+int from_hip(hipError_t e) { return e == hipSuccess ? RBS_OK : RBS_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+size_t rbs_summary_bytes(const rbs_shape* shape) {
+  if (check_shape(shape) != RBS_OK) return 0;
+  return rbs::summary_bytes(shape->n_kv_heads, blocks_of(shape));
+}
+
+int64_t rbs_index_capacity(int32_t n_blocks) {
+  if (n_blocks < 0) return 0;
+  return (int64_t)n_blocks * (n_blocks + 1) / 2;
+}
+
+int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stats, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (K == nullptr) return RBS_ERR_NULL;
+  if ((rc = check_stats_ptrs(stats)) != RBS_OK) return rc;
+  if (!aligned16(K)) return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  rbs::StatsArgs a;
+  a.K = static_cast<const uint16_t*>(K);
+  a.n_tokens = shape->n_tokens;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = M;
+  a.centroids = stats->centroids;
+  a.radii = stats->radii;
+  a.beta = stats->beta;
+  a.quantiles = stats->quantiles;
+  a.cent16 = static_cast<_Float16*>(stats->summary);
+  a.uplift = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
+                                      rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  a.counters = stats->counters;
+  return from_hip(rbs::launch_stats(a, static_cast<hipStream_t>(stream)));
+}
+
+int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats, float tau_base, float tau_rescue,
+               int32_t n_sink, int32_t n_local, int32_t n_recent, int32_t* counts, int32_t* indices,
+               void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (Q == nullptr || counts == nullptr || indices == nullptr || stats == nullptr || stats->summary == nullptr)
+    return RBS_ERR_NULL;
+  if (!(tau_base >= 0.f && tau_base <= 1.f) || !(tau_rescue >= 0.f && tau_rescue <= 1.f)) return RBS_ERR_ARG;
+  if (n_sink < 0 || n_local < 1 || n_recent < 0) return RBS_ERR_ARG;
+  if (!aligned16(Q) || !aligned16(counts) || !aligned16(indices) || !aligned16(stats->summary)) return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  rbs::SelectArgs a;
+  a.Q = static_cast<const uint16_t*>(Q);
+  a.n_tokens = shape->n_tokens;
+  a.n_q_heads = shape->n_q_heads;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = M;
+  a.cent16 = static_cast<const _Float16*>(stats->summary);
+  a.uplift = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
+                                            rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  a.tau_base = tau_base;
+  a.tau_rescue = tau_rescue;
+  a.n_sink = n_sink;
+  a.n_local = n_local;
+  a.n_recent = n_recent;
+  a.counts = counts;
+  a.indices = indices;
+  a.capacity = rbs_index_capacity(M);
+  return from_hip(rbs::launch_select(a, static_cast<hipStream_t>(stream)));
+}
+
+int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, const void* V, const int32_t* counts,
+                       const int32_t* indices, float softmax_scale, void* O, float* lse, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (Q == nullptr || K == nullptr || V == nullptr || counts == nullptr || indices == nullptr || O == nullptr)
+    return RBS_ERR_NULL;
+  if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(counts) || !aligned16(indices) ||
+      !aligned16(O) || (lse != nullptr && !aligned16(lse)))
+    return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  rbs::AttnArgs a;
+  a.Q = static_cast<const uint16_t*>(Q);
+  a.K = static_cast<const uint16_t*>(K);
+  a.V = static_cast<const uint16_t*>(V);
+  a.n_tokens = shape->n_tokens;
+  a.n_q_heads = shape->n_q_heads;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = M;
+  a.counts = counts;
+  a.indices = indices;
+  a.capacity = rbs_index_capacity(M);
+  a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
+  a.O = static_cast<uint16_t*>(O);
+  a.lse = lse;
+  return from_hip(rbs::launch_attention(a, static_cast<hipStream_t>(stream)));
+}
+
+int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (counts == nullptr || indices == nullptr) return RBS_ERR_NULL;
+  if (!aligned16(counts) || !aligned16(indices)) return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  return from_hip(rbs::launch_dense_indices(shape->n_q_heads, M, rbs_index_capacity(M), counts, indices,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+const char* rbs_status_str(int status) {
+  switch (status) {
+    case RBS_OK: return "ok";
+    case RBS_ERR_NULL: return "null pointer argument";
+    case RBS_ERR_SHAPE: return "invalid shape (token/head counts, head ratio or size limits)";
+    case RBS_ERR_UNSUPPORTED: return "unsupported head_dim or block_size (need d = 128, B in {64, 128, 256})";
+    case RBS_ERR_ARG: return "invalid argument (threshold outside [0, 1], window < 1, bad scale)";
+    case RBS_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case RBS_ERR_HIP: return "HIP runtime rejected a kernel launch";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,63 @@
+// Host-side launchers of the RBS kernels (internal to librbs; the public
+// surface is include/rbs.h).  Arguments are assumed validated by api.hip.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rbs {
+
+struct StatsArgs {
+  const uint16_t* K;
+  int n_tokens, n_kv_heads, block_size, n_blocks;
+  float* centroids;
+  float* radii;
+  float* beta;
+  float* quantiles;
+  _Float16* cent16;  // select-ready centroids [H_kv][M][d]
+  float* uplift;     // select-ready rescue uplift [H_kv][M]
+  uint32_t* counters;
+};
+
+struct SelectArgs {
+  const uint16_t* Q;
+  int n_tokens, n_q_heads, n_kv_heads, block_size, n_blocks;
+  const _Float16* cent16;
+  const float* uplift;
+  float tau_base, tau_rescue;
+  int n_sink, n_local, n_recent;
+  int32_t* counts;
+  int32_t* indices;
+  int64_t capacity;
+};
+
+struct AttnArgs {
+  const uint16_t* Q;
+  const uint16_t* K;
+  const uint16_t* V;
+  int n_tokens, n_q_heads, n_kv_heads, block_size, n_blocks;
+  const int32_t* counts;
+  const int32_t* indices;
+  int64_t capacity;
+  float scale;
+  uint16_t* O;
+  float* lse;
+};
+
+// Byte offset of the uplift array inside the select-ready summary.
+inline size_t summary_uplift_offset(int n_kv_heads, int n_blocks) {
+  size_t cent = (size_t)n_kv_heads * n_blocks * 128 * sizeof(_Float16);
+  return (cent + 255) & ~(size_t)255;
+}
+
+inline size_t summary_bytes(int n_kv_heads, int n_blocks) {
+  return summary_uplift_offset(n_kv_heads, n_blocks) + (size_t)n_kv_heads * n_blocks * sizeof(float);
+}
+
+hipError_t launch_stats(const StatsArgs& a, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+hipError_t launch_dense_indices(int n_q_heads, int n_blocks, int64_t capacity, int32_t* counts,
+                                int32_t* indices, hipStream_t s);
+
+}  // namespace rbs

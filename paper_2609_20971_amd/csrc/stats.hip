@@ -1,0 +1,224 @@
+// Stage 1: per-key-block statistics (Sec. 3.1; Algorithm 1, statistics loops).
+//
+// One workgroup per (KV head, key block) streams the block's B x 128 bf16 keys
+// from HBM exactly once, coalesced (16 lanes cover one 256-byte row), keeps
+// them in registers, and produces the centroid (mean over the block's actual
+// key count) and the radius (max L2 distance to the centroid).  The last
+// workgroup to finish a head -- detected with a per-head completion counter --
+// finds that head's 0.5 / 0.9 radius quantiles with an in-LDS radix select and
+// writes beta and the select-ready uplift for every block of the head, so the
+// whole stage is one launch.
+#include "rbs_device.hpp"
+#include "rbs_launch.hpp"
+
+namespace rbs {
+
+constexpr int kStatsThreads = 256;
+constexpr int kMaxBlocks = 4096;
+
+// Values of four order statistics (0-based ranks) of n non-negative floats
+// held as their uint32 bit patterns in LDS.  Non-negative IEEE floats order
+// like their bit patterns, so an MSB-first radix select with 8-bit digits
+// finds each rank in four histogram passes; the four ranks share the passes.
+__device__ void radix_select4(const uint32_t* keys, int n, int rank0, int rank1, int rank2, int rank3,
+                              uint32_t* hist /*4*256*/, uint32_t* prefix /*4*/, int* remaining /*4*/,
+                              uint32_t* out /*4*/) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid < 4) {
+    prefix[tid] = 0u;
+    remaining[tid] = tid == 0 ? rank0 : tid == 1 ? rank1 : tid == 2 ? rank2 : rank3;
+  }
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    const uint32_t hi_mask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
+    for (int e = tid; e < 4 * 256; e += kStatsThreads) hist[e] = 0u;
+    __syncthreads();
+    const uint32_t p0 = prefix[0], p1 = prefix[1], p2 = prefix[2], p3 = prefix[3];
+    for (int e = tid; e < n; e += kStatsThreads) {
+      const uint32_t x = keys[e];
+      const uint32_t hx = x & hi_mask, digit = (x >> shift) & 255u;
+      if (hx == p0) atomicAdd(&hist[0 * 256 + digit], 1u);
+      if (hx == p1) atomicAdd(&hist[1 * 256 + digit], 1u);
+      if (hx == p2) atomicAdd(&hist[2 * 256 + digit], 1u);
+      if (hx == p3) atomicAdd(&hist[3 * 256 + digit], 1u);
+    }
+    __syncthreads();
+    if (wave < 4) {
+      const uint32_t* h = hist + wave * 256 + 4 * lane;
+      const int c0 = (int)h[0], c1 = (int)h[1], c2 = (int)h[2], c3 = (int)h[3];
+      const int own = c0 + c1 + c2 + c3;
+      int incl = own;
+      for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += v;
+      }
+      const int excl = incl - own;
+      const int k = remaining[wave];
+      if (excl <= k && k < incl) {
+        int kr = k - excl, digit = 4 * lane;
+        if (kr >= c0) { kr -= c0; ++digit;
+          if (kr >= c1) { kr -= c1; ++digit;
+            if (kr >= c2) { kr -= c2; ++digit; } } }
+        prefix[wave] |= (uint32_t)digit << shift;
+        remaining[wave] = kr;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid < 4) out[tid] = prefix[tid];
+  __syncthreads();
+}
+
+template <int BS>
+__global__ __launch_bounds__(kStatsThreads) void stats_kernel(
+    const uint16_t* __restrict__ K, int N, int M, float* __restrict__ centroids, float* radii,
+    float* __restrict__ beta, float* __restrict__ quantiles, _Float16* __restrict__ cent16,
+    float* __restrict__ uplift, uint32_t* counters, float sel_scale) {
+  constexpr int kRowsPerThread = BS / 16;
+  __shared__ float red[4][kHeadDim];
+  __shared__ float red_r[4];
+  __shared__ int s_last;
+  __shared__ uint32_t keys[kMaxBlocks];
+  __shared__ uint32_t hist[4 * 256];
+  __shared__ uint32_t sel_prefix[4];
+  __shared__ int sel_remaining[4];
+  __shared__ uint32_t sel_out[4];
+
+  const int b = blockIdx.x, g = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int chunk = tid & 15;  // 8 consecutive dims: 8*chunk .. 8*chunk+7
+  const int rg = tid >> 4;     // row group: rows rg, rg+16, ...
+  const int row0 = b * BS;
+  const int nb = min(BS, N - row0);
+  const uint16_t* kb = K + ((size_t)g * N + row0) * kHeadDim + chunk * 8;
+
+  uint4 raw[kRowsPerThread];
+#pragma unroll
+  for (int k = 0; k < kRowsPerThread; ++k) {
+    const int r = rg + 16 * k;
+    raw[k] = r < nb ? *reinterpret_cast<const uint4*>(kb + (size_t)r * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+  }
+
+  // Column sums: own rows, then the four row groups of this wave, then waves.
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k = 0; k < kRowsPerThread; ++k) {
+    float f[8];
+    unpack8(raw[k], f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] += f[e];
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    s[e] += wave_xor_f(s[e], 16);
+    s[e] += wave_xor_f(s[e], 32);
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[wave][chunk * 8 + e] = s[e];
+  }
+  __syncthreads();
+  float c[8];
+  const float count = (float)nb;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int x = chunk * 8 + e;
+    c[e] = (((red[0][x] + red[1][x]) + red[2][x]) + red[3][x]) / count;
+  }
+
+  // Radius: squared distance per row (16 lanes share a row), max over rows.
+  float best = 0.f;
+#pragma unroll
+  for (int k = 0; k < kRowsPerThread; ++k) {
+    float f[8];
+    unpack8(raw[k], f);
+    float d2 = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float t = f[e] - c[e];
+      d2 = fmaf(t, t, d2);
+    }
+    d2 += wave_xor_f(d2, 1);
+    d2 += wave_xor_f(d2, 2);
+    d2 += wave_xor_f(d2, 4);
+    d2 += wave_xor_f(d2, 8);
+    if (rg + 16 * k < nb) best = fmaxf(best, d2);
+  }
+  best = fmaxf(best, wave_xor_f(best, 16));
+  best = fmaxf(best, wave_xor_f(best, 32));
+  if (lane == 0) red_r[wave] = best;
+  __syncthreads();
+
+  const size_t blk = (size_t)g * M + b;
+  if (tid < 16) {
+    float4* dst = reinterpret_cast<float4*>(centroids + blk * kHeadDim + chunk * 8);
+    dst[0] = make_float4(c[0], c[1], c[2], c[3]);
+    dst[1] = make_float4(c[4], c[5], c[6], c[7]);
+    f16x8 h;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = (_Float16)(c[e] * sel_scale);
+    *reinterpret_cast<f16x8*>(cent16 + blk * kHeadDim + chunk * 8) = h;
+  }
+  if (tid == 0) radii[blk] = sqrtf(fmaxf(fmaxf(red_r[0], red_r[1]), fmaxf(red_r[2], red_r[3])));
+
+  // Publish, then let the last workgroup of this head finish the head.
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) s_last = atomicAdd(&counters[g], 1u) == (uint32_t)(M - 1);
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+
+  const float* rg_radii = radii + (size_t)g * M;
+  for (int e = tid; e < M; e += kStatsThreads) keys[e] = __float_as_uint(__builtin_nontemporal_load(rg_radii + e));
+  __syncthreads();
+
+  // Linear interpolation between order statistics: h = (M - 1) p, done in
+  // integers so the ranks are exact.
+  const int n1 = M - 1;
+  const int k50 = n1 / 2, k90 = (9 * n1) / 10;
+  const float f50 = (n1 % 2) ? 0.5f : 0.0f;
+  const float f90 = (float)((9 * n1) % 10) / 10.0f;
+  radix_select4(keys, M, k50, min(k50 + 1, n1), k90, min(k90 + 1, n1), hist, sel_prefix, sel_remaining,
+                sel_out);
+  const float x50 = __uint_as_float(sel_out[0]), x50b = __uint_as_float(sel_out[1]);
+  const float x90 = __uint_as_float(sel_out[2]), x90b = __uint_as_float(sel_out[3]);
+  const float r_low = x50 + f50 * (x50b - x50);
+  const float r_high = x90 + f90 * (x90b - x90);
+  const bool spread = r_high > r_low;
+  const float span = r_high - r_low;
+  for (int e = tid; e < M; e += kStatsThreads) {
+    const float r = __uint_as_float(keys[e]);
+    float bt;
+    if (spread) bt = fminf(fmaxf((r - r_low) / span, 0.0f), 1.0f);
+    else bt = r > r_low ? 1.0f : 0.0f;
+    beta[(size_t)g * M + e] = bt;
+    uplift[(size_t)g * M + e] = r * bt * sel_scale;
+  }
+  if (tid == 0) {
+    quantiles[2 * g + 0] = r_low;
+    quantiles[2 * g + 1] = r_high;
+    counters[g] = 0u;
+  }
+}
+
+hipError_t launch_stats(const StatsArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_blocks, a.n_kv_heads);
+  const float sel_scale = kLog2e / sqrtf((float)kHeadDim);
+#define RBS_STATS_CASE(BSZ)                                                                               \
+  case BSZ:                                                                                               \
+    hipLaunchKernelGGL(stats_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, a.n_tokens, a.n_blocks,   \
+                       a.centroids, a.radii, a.beta, a.quantiles, a.cent16, a.uplift, a.counters,         \
+                       sel_scale);                                                                        \
+    break;
+  switch (a.block_size) {
+    RBS_STATS_CASE(64)
+    RBS_STATS_CASE(128)
+    RBS_STATS_CASE(256)
+    default: return hipErrorInvalidValue;
+  }
+#undef RBS_STATS_CASE
+  return hipGetLastError();
+}
+
+}  // namespace rbs

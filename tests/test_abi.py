@@ -1,0 +1,134 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol that
+include/rbs.h declares, and rejects invalid arguments on the host before any
+launch (no call here reaches the GPU: each one fails validation first)."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rbs.h")
+
+
+def _lib():
+    import paper_2609_20971_amd as rbs
+    if not os.path.exists(rbs.LIB_PATH):
+        pytest.fail("librbs.so is not built (run __graft_entry__.build())")
+    return rbs, rbs.load()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\w[\w\s\*]*?\b(rbs_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_three_stage_calls():
+    names = _declared()
+    for fn in ("rbs_block_stats", "rbs_select", "rbs_sparse_prefill"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol():
+    _, lib = _lib()
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    rbs, _ = _lib()
+    for code in range(7):
+        assert rbs.rbs_status_str(code)
+    assert rbs.rbs_status_str(99) == "unknown status"
+
+
+def test_capacity_and_summary_sizes():
+    rbs, _ = _lib()
+    assert rbs.rbs_index_capacity(1024) == 1024 * 1025 // 2
+    assert rbs.rbs_index_capacity(0) == 0
+    s = rbs.make_shape(131072, 32, 4, 128)
+    # f16 select-ready centroids + fp32 uplift per block.
+    assert rbs.rbs_summary_bytes(s) == 4 * 1024 * 256 + 4 * 1024 * 4
+    assert rbs.rbs_summary_bytes(rbs.make_shape(100, 2, 1, 96)) == 0
+
+
+FAKE = 0x10000  # aligned, never dereferenced: validation fails before use
+MIS = 0x10001
+
+
+def _stats(rbs, ptr=FAKE, **override):
+    vals = dict(centroids=ptr, radii=ptr, beta=ptr, quantiles=ptr, summary=ptr, counters=ptr)
+    vals.update(override)
+    return rbs.rbs_stats(**vals)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 64, 3), ("block_size", 96, 3), ("block_size", 32, 3), ("n_tokens", 0, 2),
+    ("n_q_heads", 3, 2), ("n_kv_heads", 0, 2), ("n_tokens", 262145, 2),
+])
+def test_shape_validation(field, value, code):
+    rbs, lib = _lib()
+    s = rbs.make_shape(1024, 4, 2, 64)
+    setattr(s, field, value)
+    st = _stats(rbs)
+    assert lib.rbs_block_stats(ctypes.byref(s), FAKE, ctypes.byref(st), None) == code
+    assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, FAKE, FAKE, None) == code
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None) == code
+    assert lib.rbs_dense_indices(ctypes.byref(s), FAKE, FAKE, None) == code
+
+
+def test_largest_shape_passes_shape_validation():
+    rbs, lib = _lib()
+    s = rbs.make_shape(262144, 1, 1, 64)  # M = 4096, the largest allowed
+    st = _stats(rbs)
+    # Passes the shape checks and stops at the NULL key pointer.
+    assert lib.rbs_block_stats(ctypes.byref(s), None, ctypes.byref(st), None) == 1
+
+
+def test_null_and_alignment_errors():
+    rbs, lib = _lib()
+    s = rbs.make_shape(1024, 4, 2, 64)
+    assert lib.rbs_block_stats(None, FAKE, ctypes.byref(_stats(rbs)), None) == 1
+    assert lib.rbs_block_stats(ctypes.byref(s), None, ctypes.byref(_stats(rbs)), None) == 1
+    assert lib.rbs_block_stats(ctypes.byref(s), FAKE, None, None) == 1
+    for field in ("centroids", "radii", "beta", "quantiles", "summary", "counters"):
+        assert lib.rbs_block_stats(ctypes.byref(s), FAKE, ctypes.byref(_stats(rbs, **{field: None})), None) == 1
+        assert lib.rbs_block_stats(ctypes.byref(s), FAKE, ctypes.byref(_stats(rbs, **{field: MIS})), None) == 5
+    assert lib.rbs_block_stats(ctypes.byref(s), MIS, ctypes.byref(_stats(rbs)), None) == 5
+    st = _stats(rbs)
+    assert lib.rbs_select(ctypes.byref(s), None, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, FAKE, FAKE, None) == 1
+    assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, None, FAKE, None) == 1
+    assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, FAKE, MIS, None) == 5
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, None, FAKE, FAKE, 0.0, FAKE, None, None) == 1
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, MIS, None, None) == 5
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, MIS, None) == 5
+    assert lib.rbs_dense_indices(ctypes.byref(s), FAKE, None, None) == 1
+
+
+@pytest.mark.parametrize("tb,tr,sink,local,recent", [
+    (-0.1, 0.5, 1, 1, 0), (0.5, 1.5, 1, 1, 0), (float("nan"), 0.5, 1, 1, 0),
+    (0.5, 0.5, -1, 1, 0), (0.5, 0.5, 1, 0, 0), (0.5, 0.5, 1, 1, -2),
+])
+def test_select_argument_errors(tb, tr, sink, local, recent):
+    rbs, lib = _lib()
+    s = rbs.make_shape(1024, 4, 2, 64)
+    st = _stats(rbs)
+    assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), tb, tr, sink, local, recent, FAKE, FAKE, None) == 4
+
+
+def test_bad_softmax_scale():
+    rbs, lib = _lib()
+    s = rbs.make_shape(1024, 4, 2, 64)
+    for bad in (float("nan"), float("inf")):
+        assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, bad, FAKE, None, None) == 4
+
+
+def test_binding_raises_without_library(monkeypatch, tmp_path):
+    import paper_2609_20971_amd._lib as L
+    monkeypatch.setattr(L, "_lib", None)
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        L.load()

@@ -1,0 +1,172 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle on the
+same seeded inputs.  Tolerances live in tests/rbs_harness.py."""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import WORKLOADS, Workload, f64_from_bf16_bits, make_inputs
+from tests import rbs_harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _run(w: Workload, inputs=None, tau=None, forced=None):
+    import torch
+    import paper_2609_20971_amd as rbs
+    if inputs is None:
+        inputs = make_inputs(w)
+    tb, tr = (w.tau_base, w.tau_rescue) if tau is None else tau
+    sink, local, recent = (w.n_sink, w.n_local, w.n_recent) if forced is None else forced
+    shape = rbs.make_shape(w.seq_len, w.n_q_heads, w.n_kv_heads, w.block_size)
+    Qd, Kd, Vd = (H.to_device(inputs[x]) for x in ("q", "k", "v"))
+    st = rbs.rbs_block_stats(shape, Kd)
+    counts, indices = rbs.rbs_select(shape, Qd, st, tb, tr, sink, local, recent)
+    lse = torch.empty((w.n_q_heads, w.seq_len), dtype=torch.float32, device="cuda")
+    O = rbs.rbs_sparse_prefill(shape, Qd, Kd, Vd, counts, indices, 0.0, lse=lse)
+    torch.cuda.synchronize()
+    return dict(shape=shape, inputs=inputs, Qd=Qd, Kd=Kd, Vd=Vd, stats=st, counts=counts, indices=indices,
+                O=O, lse=lse, tau=(tb, tr), forced=(sink, local, recent))
+
+
+def _full_check(w: Workload, tau=None, forced=None, attn_rows=None, select_rows=None, inputs=None):
+    _say(f"[parity] workload={w.name} N={w.seq_len} Hq={w.n_q_heads} Hkv={w.n_kv_heads} B={w.block_size} "
+         f"tau={tau} forced={forced}")
+    r = _run(w, inputs=inputs, tau=tau, forced=forced)
+    inp = r["inputs"]
+    Kf = f64_from_bf16_bits(inp["k"])
+    C, R = oracle.block_stats(Kf, w.block_size)
+    beta, rq = oracle.rescue_coefficients(R)
+    rep = H.check_stats(r["stats"], C, R, beta, rq)
+    M = w.n_blocks
+    rows = select_rows or [(h, i) for h in range(w.n_q_heads) for i in range(M)]
+    Qf = f64_from_bf16_bits(inp["q"])
+    tb, tr = r["tau"]
+    sink, local, recent = r["forced"]
+    ref = oracle.select(Qf, C, R, beta, w.block_size, tb, tr, sink, local, recent, rows=rows)
+    lists = H.gpu_rows(r["counts"], r["indices"], rows)
+    H.check_lists(lists, M, sink, local, recent)
+    n_rows, compared, near = H.compare_masks(lists, ref)
+    dens_gpu = sum(len(v) for v in lists.values()) / compared
+    dens_ref = oracle.density([ref[k]["final"] for k in rows])
+    arows = attn_rows or rows
+    alists = H.gpu_rows(r["counts"], r["indices"], arows)
+    Og = H.bf16_tensor_to_f64(r["O"])
+    Vf = f64_from_bf16_bits(inp["v"])
+    err = H.max_abs_attention_error(Og, Qf, Kf, Vf, w.group, w.block_size, alists, w.seq_len)
+    _say(f"[parity] {w.name}: stats {rep}; rows {n_rows} blocks {compared} near-threshold flips {near}; "
+         f"density gpu {dens_gpu:.4f} oracle {dens_ref:.4f}; attention max-abs {err:.3e}")
+    assert err <= H.ATTN_ATOL
+    return r, near
+
+
+def test_tiny_workload_full():
+    _full_check(WORKLOADS["tiny-2k"])
+
+
+@pytest.mark.parametrize("variant", [
+    dict(seq_len=1000, block_size=64, n_q_heads=4, n_kv_heads=2, seed=1),          # ragged tail, GQA 2:1
+    dict(seq_len=777, block_size=128, n_q_heads=2, n_kv_heads=2, seed=2),          # no GQA, ragged
+    dict(seq_len=1300, block_size=256, n_q_heads=4, n_kv_heads=1, seed=3),         # B = 256, ragged
+    dict(seq_len=64, block_size=64, n_q_heads=2, n_kv_heads=1, seed=4),            # single block
+    dict(seq_len=5, block_size=128, n_q_heads=1, n_kv_heads=1, seed=5),            # N < B
+])
+def test_edge_shapes(variant):
+    w = WORKLOADS["tiny-2k"].with_(name="edge", needles_per_kv_head=2, **variant)
+    _full_check(w)
+
+
+@pytest.mark.parametrize("tau,forced", [
+    ((0.0, 0.0), (1, 2, 0)),     # alpha = 0: every causal block
+    ((1.0, 1.0), (0, 1, 0)),     # alpha = 1: argmax blocks only
+    ((0.22, 0.18), (1, 2, 0)),   # the paper's default pair
+    ((0.9, 0.95), (2, 3, 1)),    # one recent row
+    ((0.9, 0.95), (0, 1, 2)),    # two recent rows
+])
+def test_threshold_and_forced_variants(tau, forced):
+    w = WORKLOADS["tiny-2k"].with_(seq_len=1536, seed=7)
+    r, _ = _full_check(w, tau=tau, forced=forced)
+    if tau == (0.0, 0.0):
+        counts = r["counts"].cpu().numpy()
+        assert (counts == np.arange(w.n_blocks)[None, :] + 1).all()
+
+
+def test_degenerate_radii_and_zero_queries():
+    """Identical key blocks (r_high == r_low) and all-zero query rows."""
+    w = WORKLOADS["tiny-2k"].with_(seq_len=1024, seed=8)
+    inp = make_inputs(w)
+    blk = inp["k"][:, :w.block_size].copy()
+    inp["k"][:] = np.tile(blk, (1, w.seq_len // w.block_size, 1))
+    inp["q"][:, 128:320] = 0
+    _full_check(w, inputs=inp)
+
+
+def test_dense_path_matches_dense_oracle():
+    import torch
+    import paper_2609_20971_amd as rbs
+    w = WORKLOADS["tiny-2k"].with_(seq_len=640, seed=9)
+    _say(f"[parity] dense path N={w.seq_len}")
+    inp = make_inputs(w)
+    shape = rbs.make_shape(w.seq_len, w.n_q_heads, w.n_kv_heads, w.block_size)
+    Qd, Kd, Vd = (H.to_device(inp[x]) for x in ("q", "k", "v"))
+    counts, indices = rbs.rbs_dense_indices(shape)
+    O = rbs.rbs_sparse_prefill(shape, Qd, Kd, Vd, counts, indices)
+    torch.cuda.synchronize()
+    Og = H.bf16_tensor_to_f64(O)
+    Qf, Kf, Vf = (f64_from_bf16_bits(inp[x]) for x in ("q", "k", "v"))
+    for h in range(w.n_q_heads):
+        ref = oracle.dense_causal_attention(Qf[h], Kf[h // w.group], Vf[h // w.group])
+        assert np.abs(Og[h] - ref).max() <= H.ATTN_ATOL
+
+
+def test_lse_and_determinism():
+    import torch
+    w = WORKLOADS["tiny-2k"].with_(seq_len=1152, seed=10)
+    r1 = _run(w)
+    r2 = _run(w, inputs=r1["inputs"])
+    for key in ("counts", "O", "lse"):
+        assert torch.equal(r1[key], r2[key]), key
+    assert torch.equal(r1["stats"].centroids, r2["stats"].centroids)
+    cnt = r1["counts"].cpu().numpy()
+    idx = r1["indices"].cpu().numpy()
+    for h in range(w.n_q_heads):
+        for i in range(w.n_blocks):
+            base = i * (i + 1) // 2
+            assert (idx[h, base:base + cnt[h, i]] == r2["indices"].cpu().numpy()[h, base:base + cnt[h, i]]).all()
+    # LSE of a sampled row against the oracle definition on the GPU's list.
+    Qf, Kf = (f64_from_bf16_bits(r1["inputs"][x]) for x in ("q", "k"))
+    h, i = 1, w.n_blocks - 1
+    base = i * (i + 1) // 2
+    ids = idx[h, base:base + cnt[h, i]]
+    keys = np.concatenate([np.arange(b * w.block_size, (b + 1) * w.block_size) for b in ids])
+    lse = r1["lse"].cpu().numpy()
+    for t in range(i * w.block_size, (i + 1) * w.block_size, 17):
+        kk = keys[keys <= t]
+        x = Kf[0, kk] @ Qf[h, t] / np.sqrt(128)
+        ref = x.max() + np.log(np.exp(x - x.max()).sum())
+        assert abs(lse[h, t] - ref) <= 1e-3
+
+
+@pytest.mark.slow
+def test_qwen3_30b_32k_select_full_attention_sampled():
+    w = WORKLOADS["qwen3-30b-a3b-32k"]
+    rows_attn = H.sample_rows(w.n_q_heads, w.n_blocks, 12, seed=1)
+    _full_check(w, attn_rows=rows_attn)
+
+
+@pytest.mark.slow
+def test_qwen3_30b_128k_sampled():
+    """The headline shape, in the launch configuration the benchmark times;
+    selection and attention checked on sampled rows."""
+    w = WORKLOADS["qwen3-30b-a3b-128k"]
+    rows = H.sample_rows(w.n_q_heads, w.n_blocks, 24, seed=2, include=[(5, 1023), (31, 700), (0, 3)])
+    _full_check(w, select_rows=rows, attn_rows=rows[:10])
