@@ -1,0 +1,283 @@
+#!/usr/bin/env python
+"""Benchmark of the RBS sparse-prefill hot path on one MI355X.
+
+One step = one pass of the whole path over one attention layer's inputs:
+block statistics -> dual-branch selection -> block-sparse attention, with every
+input already resident in HBM.  The default workload is the 128K
+Qwen3-30B-A3B-shaped layer (32 query / 4 KV heads, d = 128, B = 128), seeded
+synthetic data.  Prints ONE JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "128K sparse prefill-attn ms/layer, speedup vs own dense, MFMA util %"
+PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E, vendor figure
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA, vendor figure (no sparsity)
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "attn_traffic_qwen3-30b-a3b-128k.json")
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="qwen3-30b-a3b-128k")
+    p.add_argument("--dense-reps", type=int, default=2)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-select-rows", type=int, default=256,
+                   help="sampled (head, query block) rows for the oracle's selection timing")
+    p.add_argument("--cpu-attn-rows", type=int, default=24,
+                   help="sampled (head, query block) rows for the oracle's attention timing")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run a 1 GiB device copy (for scaling HBM counters)")
+    return p.parse_args()
+
+
+def algorithmic(w, counts_sum: int):
+    """Bytes / flops each stage must move or compute per launch."""
+    N, Hq, Hkv, d, B = w.seq_len, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size
+    M = w.n_blocks
+    pairs = Hq * M * (M + 1) // 2
+    stats_bytes = Hkv * N * d * 2 + Hkv * M * d * 4 + Hkv * M * d * 2 + Hkv * M * 4 * 3 + Hkv * 8
+    select_bytes = Hq * N * d * 2 + Hkv * M * (d * 2 + 4) + Hq * M * 4 + counts_sum * 4
+    select_flops = 2 * B * d * pairs            # q . c_b for every causal (token, block) pair
+    attn_flops = 4 * B * B * d * counts_sum     # QK^T and PV over every executed block pair
+    dense_flops = 4 * B * B * d * pairs
+    return dict(stats_bytes=stats_bytes, select_bytes=select_bytes, select_flops=select_flops,
+                attn_flops=attn_flops, dense_flops=dense_flops, pairs=pairs)
+
+
+def cpu_baseline(w, inp, counts_np, indices_np, n_select: int, n_attn: int):
+    """Time the float64 oracle on a bounded sample of the same workload and
+    scale it to one layer (ms/layer)."""
+    import numpy as np
+    import oracle
+    from synth import f64_from_bf16_bits
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    M, B, G = w.n_blocks, w.block_size, w.group
+    rng = np.random.default_rng(123)
+    rows = [(int(rng.integers(w.n_q_heads)), int(rng.integers(M))) for _ in range(max(n_select, n_attn))]
+
+    t0 = time.perf_counter()
+    Kf0 = f64_from_bf16_bits(inp["k"][:1])
+    C0, R0 = oracle.block_stats(Kf0, B)
+    oracle.rescue_coefficients(R0)
+    t_stats = (time.perf_counter() - t0) * w.n_kv_heads          # one KV head, scaled to all
+
+    Kf = [f64_from_bf16_bits(inp["k"][g]) for g in range(w.n_kv_heads)]
+    Vf = [f64_from_bf16_bits(inp["v"][g]) for g in range(w.n_kv_heads)]
+    C, R = oracle.block_stats(np.stack(Kf), B)
+    beta, _ = oracle.rescue_coefficients(R)
+    t_sel = 0.0
+    t_att = 0.0
+    for k, (h, i) in enumerate(rows):
+        s, e = i * B, min((i + 1) * B, w.seq_len)
+        qi = f64_from_bf16_bits(inp["q"][h, s:e])
+        if k < n_select:
+            t0 = time.perf_counter()
+            oracle.select_row(qi, C[h // G], R[h // G], beta[h // G], i, M, w.tau_base, w.tau_rescue,
+                              w.n_sink, w.n_local, w.n_recent)
+            t_sel += time.perf_counter() - t0
+        if k >= n_attn:
+            continue
+        base = i * (i + 1) // 2
+        ids = indices_np[h, base:base + counts_np[h, i]].tolist()
+        qh = np.zeros((e, w.head_dim))
+        qh[s:e] = qi
+        t0 = time.perf_counter()
+        oracle.attention_rows(qh, Kf[h // G], Vf[h // G], B, i, ids)
+        t_att += time.perf_counter() - t0
+    total_rows = w.n_q_heads * M
+    ms = (t_stats + t_sel / n_select * total_rows + t_att / n_attn * total_rows) * 1e3
+    return {"value": ms, "unit": "ms/layer", "cores": int(cores), "kind": "oracle",
+            "sample": (f"float64 numpy oracle: block stats of 1 of {w.n_kv_heads} KV heads (x{w.n_kv_heads}); "
+                       f"selection for {n_select} and attention (on the GPU's lists) for {n_attn} random "
+                       f"(head, query block) rows of {total_rows}, each scaled to all rows"),
+            "measured_s": t_stats / w.n_kv_heads + t_sel + t_att}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the RBS hot path is built and "
+                                   "measured per GPU (heads would shard across GPUs with no communication)",
+                          "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_20971_amd as rbs
+    from synth import workload, make_inputs
+
+    w = workload(args.workload)
+    _log(f"[bench] workload {w.name}: N={w.seq_len} Hq={w.n_q_heads} Hkv={w.n_kv_heads} B={w.block_size}")
+    t0 = time.perf_counter()
+    inp = make_inputs(w)
+    _log(f"[bench] inputs generated in {time.perf_counter() - t0:.1f}s")
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+
+    def up(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    Q, K, V = up(inp["q"]), up(inp["k"]), up(inp["v"])
+    shape = rbs.make_shape(w.seq_len, w.n_q_heads, w.n_kv_heads, w.block_size)
+    stats = rbs.BlockStats.allocate(shape, dev)
+    counts, indices = rbs.allocate_lists(shape, dev)
+    O = torch.empty_like(Q)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        rbs.rbs_block_stats(shape, K, stats, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        rbs.rbs_select(shape, Q, stats, w.tau_base, w.tau_rescue, w.n_sink, w.n_local, w.n_recent,
+                       counts, indices, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        rbs.rbs_sparse_prefill(shape, Q, K, V, counts, indices, 0.0, O, stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    _log(f"[bench] warmup done ({args.warmup} steps)")
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
+    stage_ms = np.zeros(3)
+    for ev in events:
+        stage_ms += [ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])]
+    stage_ms /= args.steps
+    ms_per_step = float(stage_ms.sum())
+    _log(f"[bench] timed {args.steps} steps: stats {stage_ms[0]:.3f} ms, select {stage_ms[1]:.3f} ms, "
+         f"attention {stage_ms[2]:.3f} ms (wall {wall_ms:.3f} ms/step)")
+
+    counts_np = counts.cpu().numpy()
+    counts_sum = int(counts_np.sum())
+    alg = algorithmic(w, counts_sum)
+    density = counts_sum / alg["pairs"]
+
+    # Own dense path: same attention kernel over every causal block.
+    dcounts, dindices = rbs.allocate_lists(shape, dev)
+    rbs.rbs_dense_indices(shape, dcounts, dindices, stream=stream)
+    Od = torch.empty_like(Q)
+    rbs.rbs_sparse_prefill(shape, Q, K, V, dcounts, dindices, 0.0, Od, stream=stream)
+    torch.cuda.synchronize()
+    dense_ms = []
+    for _ in range(args.dense_reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        rbs.rbs_sparse_prefill(shape, Q, K, V, dcounts, dindices, 0.0, Od, stream=stream)
+        b.record(stream)
+        b.synchronize()
+        dense_ms.append(a.elapsed_time(b))
+    dense_ms = float(np.median(dense_ms))
+    _log(f"[bench] dense attention {dense_ms:.3f} ms")
+    del Od, dcounts, dindices
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    attn_tflops = alg["attn_flops"] / (stage_ms[2] * 1e-3) / 1e12
+    dense_tflops = alg["dense_flops"] / (dense_ms * 1e-3) / 1e12
+    stats_gbps = alg["stats_bytes"] / (stage_ms[0] * 1e-3) / 1e9
+    select_gbps = alg["select_bytes"] / (stage_ms[1] * 1e-3) / 1e9
+    select_tflops = alg["select_flops"] / (stage_ms[1] * 1e-3) / 1e12
+
+    traffic = None
+    if os.path.exists(PROFILE_TRAFFIC):
+        with open(PROFILE_TRAFFIC) as f:
+            prof = json.load(f)
+        if prof.get("workload") == w.name and prof.get("kernel_source_sha") == _attn_source_sha():
+            traffic = prof.get("bytes_per_launch")
+
+    result = {
+        "metric": METRIC,
+        "value": round(ms_per_step, 4),
+        "unit": "ms/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "seq_len": w.seq_len, "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads,
+                   "head_dim": w.head_dim, "block_size": w.block_size, "tau_base": w.tau_base,
+                   "tau_rescue": w.tau_rescue, "n_sink": w.n_sink, "n_local": w.n_local,
+                   "n_recent": w.n_recent, "seed": w.seed},
+        "speedup_vs_dense": round(dense_ms / ms_per_step, 3),
+        "attn_speedup_vs_dense": round(dense_ms / stage_ms[2], 3),
+        "mfma_util_pct": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
+        "density": round(density, 6),
+        "dense_attn_ms": round(dense_ms, 3),
+        "dense_mfma_util_pct": round(100.0 * dense_tflops / PEAK_BF16_TFLOPS, 2),
+        "wall_ms_per_step": round(wall_ms, 4),
+        "stages": {
+            "stats": {"ms": round(float(stage_ms[0]), 4), "alg_bytes": alg["stats_bytes"],
+                      "GBps": round(stats_gbps, 1), "hbm_frac": round(stats_gbps / PEAK_HBM_GBPS, 4)},
+            "select": {"ms": round(float(stage_ms[1]), 4), "alg_bytes": alg["select_bytes"],
+                       "GBps": round(select_gbps, 1), "hbm_frac": round(select_gbps / PEAK_HBM_GBPS, 4),
+                       "alg_flops": alg["select_flops"], "TFLOPs": round(select_tflops, 1),
+                       "mfma_frac": round(select_tflops / PEAK_BF16_TFLOPS, 4)},
+            "attn": {"ms": round(float(stage_ms[2]), 4), "alg_flops": alg["attn_flops"],
+                     "TFLOPs": round(attn_tflops, 1), "executed_pairs": counts_sum},
+        },
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic},
+    }
+
+    if not args.no_cpu_baseline:
+        _log(f"[bench] timing the CPU oracle on sampled rows")
+        cb = cpu_baseline(w, inp, counts_np, indices.cpu().numpy(), args.cpu_select_rows, args.cpu_attn_rows)
+        _log(f"[bench] CPU oracle measured {cb.pop('measured_s'):.1f}s")
+        result["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in cb.items()}
+    print(json.dumps(result), flush=True)
+
+
+def _attn_source_sha():
+    import hashlib
+    with open(os.path.join(ROOT, "paper_2609_20971_amd", "csrc", "attn.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    main()

@@ -25,8 +25,8 @@
  *   - Arguments are validated on the host before anything is launched; a
  *     failing call returns a status code, launches nothing and writes nothing.
  *     RBS_ERR_HIP means a launch was rejected by the runtime.
- *   - Calls on distinct streams do not share state, except rbs_block_stats's
- *     completion counters (one array per concurrent stats call).
+ *   - The library keeps no state between calls; calls on distinct streams are
+ *     independent.
  */
 #ifndef RBS_H
 #define RBS_H
@@ -71,10 +71,6 @@ typedef struct {
  *              (centroids as f16 pre-scaled by log2(e)/sqrt(d), and the
  *              per-block rescue uplift r_b beta_b log2(e)/sqrt(d)).  Opaque;
  *              written by rbs_block_stats, read by rbs_select.
- *   counters   uint32 [H_kv] completion counters.  Must be zero before the
- *              first rbs_block_stats call that uses them; every call leaves
- *              them zero again.  Do not share one array between stats calls
- *              that may run concurrently.
  */
 typedef struct {
   float* centroids;
@@ -82,7 +78,6 @@ typedef struct {
   float* beta;
   float* quantiles;
   void* summary;
-  uint32_t* counters;
 } rbs_stats;
 
 /* Bytes needed for rbs_stats.summary (0 if the shape is invalid). */
@@ -95,8 +90,8 @@ int64_t rbs_index_capacity(int32_t n_blocks);
 
 /*
  * Stage 1 (Sec. 3.1; Algorithm 1, statistics loops).
- * K: bf16 [H_kv][N][d].  Fills every field of *stats (one pass over K; the
- * quantiles and beta are computed by the last workgroup to finish each head).
+ * K: bf16 [H_kv][N][d].  Fills every field of *stats: one pass over K for the
+ * centroids and radii, then one workgroup per KV head for the quantiles and beta.
  */
 int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stats, void* stream);
 

@@ -42,7 +42,6 @@ class rbs_stats(ctypes.Structure):
         ("beta", ctypes.c_void_p),
         ("quantiles", ctypes.c_void_p),
         ("summary", ctypes.c_void_p),
-        ("counters", ctypes.c_void_p),
     ]
 
 
@@ -121,7 +120,6 @@ class BlockStats:
     beta: torch.Tensor        # fp32 [H_kv][M]
     quantiles: torch.Tensor   # fp32 [H_kv][2]
     summary: torch.Tensor     # uint8 [rbs_summary_bytes]
-    counters: torch.Tensor    # int32 [H_kv], zero between calls
 
     @classmethod
     def allocate(cls, shape: rbs_shape, device="cuda") -> "BlockStats":
@@ -132,12 +130,11 @@ class BlockStats:
             raise RbsError("rbs_summary_bytes", RBS_ERR_SHAPE, "invalid shape")
         return cls(shape, torch.empty((hk, m, d), **f32), torch.empty((hk, m), **f32),
                    torch.empty((hk, m), **f32), torch.empty((hk, 2), **f32),
-                   torch.empty(nbytes, dtype=torch.uint8, device=device),
-                   torch.zeros(max(hk, 4), dtype=torch.int32, device=device))
+                   torch.empty(nbytes, dtype=torch.uint8, device=device))
 
     def as_c(self) -> rbs_stats:
         return rbs_stats(_ptr(self.centroids), _ptr(self.radii), _ptr(self.beta), _ptr(self.quantiles),
-                         _ptr(self.summary), _ptr(self.counters))
+                         _ptr(self.summary))
 
 
 def rbs_block_stats(shape: rbs_shape, K: torch.Tensor, stats: BlockStats | None = None, stream=None) -> BlockStats:

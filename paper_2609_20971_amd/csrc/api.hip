@@ -30,10 +30,10 @@ int check_shape(const rbs_shape* s) {
 
 int check_stats_ptrs(const rbs_stats* st) {
   if (st == nullptr || st->centroids == nullptr || st->radii == nullptr || st->beta == nullptr ||
-      st->quantiles == nullptr || st->summary == nullptr || st->counters == nullptr)
+      st->quantiles == nullptr || st->summary == nullptr)
     return RBS_ERR_NULL;
   if (!aligned16(st->centroids) || !aligned16(st->radii) || !aligned16(st->beta) || !aligned16(st->quantiles) ||
-      !aligned16(st->summary) || !aligned16(st->counters))
+      !aligned16(st->summary))
     return RBS_ERR_ALIGN;
   return RBS_OK;
 }
@@ -74,7 +74,6 @@ int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stat
   a.cent16 = static_cast<_Float16*>(stats->summary);
   a.uplift = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
                                       rbs::summary_uplift_offset(shape->n_kv_heads, M));
-  a.counters = stats->counters;
   return from_hip(rbs::launch_stats(a, static_cast<hipStream_t>(stream)));
 }
 

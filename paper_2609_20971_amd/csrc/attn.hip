@@ -6,14 +6,17 @@
 // query: S^T = K Q^T and O^T = V^T P^T on the bf16 32x32x16 MFMA, with Q held
 // in registers as the B operand.  Row softmax (max, exp2, sum) is then
 // lane-local plus one exchange with lane^32, and the O rescale is lane-local.
-// For each listed key block, K and V tiles are staged in LDS with padded rows
-// (K: 272 B, V: 288 B per 256-byte row) so that the 16-lane groups of a read
-// hit distinct banks while every per-tile offset stays a compile-time
-// constant; K feeds the A operand with plain 128-bit reads, V^T is read
-// directly from row-major V with the gfx950 LDS transpose read
-// (ds_read_b64_tr_b16).  Online softmax in fp32 with exp2;
-// P is rounded to bf16 for the PV product.  Causal masking is applied on the
-// diagonal block only; keys past N are masked in a short last block.
+//
+// K and V tiles of each listed key block go straight from global memory to
+// LDS (global_load_lds_dwordx4: no registers), 256-byte rows with 16-byte
+// chunks XOR-swizzled per row so that MFMA operand reads are bank-conflict
+// free.  K feeds the A operand with 128-bit reads; V^T is read from row-major
+// V with the gfx950 LDS transpose read (ds_read_b64_tr_b16).  The two tiles
+// are pipelined against compute: the next block's K is fetched while this
+// block's softmax and PV run, the next V while the next QK^T runs.  Online
+// softmax in fp32 with exp2; P is rounded to bf16 for the PV product.  Causal
+// masking is applied on the diagonal block only; keys past N are masked in a
+// short last block (their rows are loaded as copies of the last valid key).
 #include "rbs_device.hpp"
 #include "rbs_launch.hpp"
 
@@ -21,26 +24,70 @@ namespace rbs {
 
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int kPitchK = 272;  // bytes per staged K row (256 + 16)
-constexpr int kPitchV = 288;  // bytes per staged V row (256 + 32)
+// Physical 16-byte chunk of logical chunk c in staged row r.
+__device__ __forceinline__ int kswz(int r, int c) { return c ^ (r & 15); }
+__device__ __forceinline__ int vswz(int r, int c) { return c ^ ((r & 3) << 2); }
+
+// vmcnt(n) with expcnt/lgkmcnt left unconstrained (gfx9 encoding).
+#define RBS_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | 0x0F70)
+
+// Workgroup id -> logical work item, so that groups of 8 consecutive items
+// (the query heads of one KV group, same query block) run on the same XCD
+// (workgroups are dealt to the 8 XCDs round-robin by id).
+__device__ __forceinline__ int xcd_remap(int id, int total) {
+  const int full = total & ~63;
+  if (id >= full) return id;
+  const int x = id & 7, s = id >> 3;
+  return ((s >> 3) << 6) + (x << 3) + (s & 7);
+}
+
+// One 16-byte-per-lane global -> LDS copy: lane l's 16 bytes from
+// gbase + voff land at LDS byte lds_addr + 16 l.  Issued from inline assembly
+// so that the compiler's wait-count pass does not treat every later LDS read as
+// dependent on it (it would wait for all outstanding copies); the kernel waits
+// for the copies it needs with explicit vmcnt counts instead.  Later-issued
+// vector loads only make the compiler's own waits more conservative.
+__device__ __forceinline__ void lds_dma16(const void* gbase, uint32_t voff, uint32_t lds_addr) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
+      : "v"(voff), "s"(gbase), "s"(lds_addr)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)p;
+}
+
+// Wave w copies rows 32w .. 32w + 31 of a B x 128 bf16 tile (8 copies of
+// 4 rows each).  Rows at or past nk repeat row nk - 1 (masked later).
+__device__ __forceinline__ void issue_tile(const uint16_t* tile_base, int nk, uint32_t lds_base, int wave, int lane,
+                                           bool is_v) {
+  const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds_base + (uint32_t)(32 * wave) * 256u);
+  const int pc = lane & 15;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int row = 32 * wave + 4 * j + (lane >> 4);
+    const int c = is_v ? vswz(row, pc) : kswz(row, pc);
+    const uint32_t voff = (uint32_t)min(row, nk - 1) * 256u + 16u * (uint32_t)c;
+    lds_dma16(tile_base, voff, lds_wave + (uint32_t)j * 1024u);
+  }
+}
 
 template <int BS>
-__global__ __launch_bounds__(BS * 2) void attn_kernel(
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V, int N, int M,
     int Hq, int group, const int32_t* __restrict__ counts, const int32_t* __restrict__ indices, int64_t capacity,
     float scale_log2, uint16_t* __restrict__ O, float* __restrict__ lse) {
-  constexpr int NW = BS / 32;
-  constexpr int NT = NW * kWave;
   constexpr int SUB = BS < 128 ? BS : 128;  // keys per softmax step
   constexpr int KT = SUB / 32;              // 32-key MFMA tiles per step
-  constexpr int kRowsPerPass = NT / 16;
-  constexpr int kPasses = BS / kRowsPerPass;
-  __shared__ __align__(16) unsigned char k_lds[BS * kPitchK];
-  __shared__ __align__(16) unsigned char v_lds[BS * kPitchV];
+  __shared__ __align__(1024) unsigned char k_lds[BS * 256];
+  __shared__ __align__(1024) unsigned char v_lds[BS * 256];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
-  const int work = blockIdx.x;
+  const int work = xcd_remap(blockIdx.x, gridDim.x);
   const int i = M - 1 - work / Hq;
   const int h = work % Hq;
   const int g = h / group;
@@ -57,6 +104,10 @@ __global__ __launch_bounds__(BS * 2) void attn_kernel(
       __builtin_memcpy(&qreg[ks], &v, 16);
     }
   }
+  // Q must be resident before any tile copy is issued: the copies are
+  // invisible to the compiler, so a wait it placed for Q inside the loop
+  // would also wait for them.
+  RBS_WAIT_VMCNT(0);
 
   const int count = min(max(counts[(size_t)h * M + i], 0), i + 1);
   const int32_t* list = indices + (int64_t)h * capacity + (int64_t)i * (i + 1) / 2;
@@ -68,25 +119,28 @@ __global__ __launch_bounds__(BS * 2) void attn_kernel(
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
 
-  const int ld_chunk = tid & 15, ld_row = tid >> 4;
+  // Per-lane LDS read bases.  K: row 32mt + l32 of the step, chunk 2ks + half.
+  // V (transposed read): lane sources row 16c + 4 half + (lane%16)/4 (and +8),
+  // dims 32dt + 16((lane/16)%2) + 4(lane%4); it receives dim 32dt + l32.
+  const int vq = (lane & 15) >> 2;
+  const int vsub = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);  // chunk within the dt group
+  const int vbyte = 8 * (lane & 1);
+
+  const uint32_t k_base = lds_offset(k_lds), v_base = lds_offset(v_lds);
+  int kb = count > 0 ? min(max(list[0], 0), i) : 0;
+  if (count > 0) {
+    const int nk0 = min(BS, N - kb * BS);
+    issue_tile(kg + (size_t)kb * BS * kHeadDim, nk0, k_base, wave, lane, false);
+    issue_tile(vg + (size_t)kb * BS * kHeadDim, nk0, v_base, wave, lane, true);
+  }
   for (int n = 0; n < count; ++n) {
-    const int kb = min(max(list[n], 0), i);
-    const int key0 = kb * BS;
-    const int nk = min(BS, N - key0);
-    __syncthreads();
-#pragma unroll
-    for (int p = 0; p < kPasses; ++p) {
-      const int r = ld_row + p * kRowsPerPass;
-      uint4 kv = make_uint4(0u, 0u, 0u, 0u), vv = make_uint4(0u, 0u, 0u, 0u);
-      if (r < nk) {
-        kv = *reinterpret_cast<const uint4*>(kg + (size_t)(key0 + r) * kHeadDim + 8 * ld_chunk);
-        vv = *reinterpret_cast<const uint4*>(vg + (size_t)(key0 + r) * kHeadDim + 8 * ld_chunk);
-      }
-      *reinterpret_cast<uint4*>(k_lds + r * kPitchK + 16 * ld_chunk) = kv;
-      *reinterpret_cast<uint4*>(v_lds + r * kPitchV + 16 * ld_chunk) = vv;
-    }
-    __syncthreads();
+    const bool has_next = n + 1 < count;
+    const int kb_next = has_next ? min(max(list[n + 1], 0), i) : 0;
+    const int nk = min(BS, N - kb * BS);
     const bool diag = kb == i;
+
+    RBS_WAIT_VMCNT(8);  // this block's K has landed (its V may still be in flight)
+    __syncthreads();
 
 #pragma unroll
     for (int sub = 0; sub < BS / SUB; ++sub) {
@@ -95,14 +149,20 @@ __global__ __launch_bounds__(BS * 2) void attn_kernel(
 #pragma unroll
       for (int mt = 0; mt < KT; ++mt) {
         s[mt] = f32x16{};
-        const unsigned char* krow = k_lds + (kbase + 32 * mt + l32) * kPitchK + 16 * half;
+        const int row = kbase + 32 * mt + l32;
+        const unsigned char* krow = k_lds + row * 256;
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
-          const uint4 raw = *reinterpret_cast<const uint4*>(krow + 32 * ks);
+          const uint4 raw = *reinterpret_cast<const uint4*>(krow + 16 * kswz(row, 2 * ks + half));
           bf16x8 a;
           __builtin_memcpy(&a, &raw, 16);
           s[mt] = mfma_bf16(a, qreg[ks], s[mt]);
         }
+      }
+      if (sub == BS / SUB - 1) {
+        __syncthreads();  // every wave is done with this K tile
+        if (has_next)
+          issue_tile(kg + (size_t)kb_next * BS * kHeadDim, min(BS, N - kb_next * BS), k_base, wave, lane, false);
       }
       if (diag || nk < BS) {
 #pragma unroll
@@ -139,21 +199,23 @@ __global__ __launch_bounds__(BS * 2) void attn_kernel(
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
       }
+      if (sub == 0) {
+        if (has_next) RBS_WAIT_VMCNT(8); else RBS_WAIT_VMCNT(0);  // this block's V has landed
+        __syncthreads();
+      }
 #pragma unroll
       for (int c = 0; c < SUB / 16; ++c) {
         bf16x8 pb;
 #pragma unroll
         for (int e = 0; e < 8; ++e) pb[e] = (__bf16)s[c >> 1][8 * (c & 1) + e];
-        // Transposed read of V: lane l sources row 16c + 4(l/32) + (l%16)/4 (and +8),
-        // dims 32dt + 16((l/16)%2) + 4(l%4); it receives 4 keys of dim 32dt + l%32.
-        const unsigned char* vrow = v_lds + (kbase + 16 * c + 4 * half + ((lane & 15) >> 2)) * kPitchV +
-                                    2 * (16 * ((lane >> 4) & 1) + 4 * (lane & 3));
+        const int row0 = kbase + 16 * c + 4 * half + vq;
+        const unsigned char* v0 = v_lds + row0 * 256 + vbyte;
+        const unsigned char* v1 = v0 + 8 * 256;
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
-          const unsigned char* p0 = vrow + 64 * dt;
-          const unsigned char* p1 = p0 + 8 * kPitchV;
-          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p0);
-          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p1);
+          const int pc = 16 * vswz(row0, 4 * dt + vsub);  // row0 and row0 + 8 share the swizzle
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v0 + pc));
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v1 + pc));
           bf16x8 a;
           __builtin_memcpy(&a, &lo, 8);
           __builtin_memcpy(reinterpret_cast<unsigned char*>(&a) + 8, &hi, 8);
@@ -161,6 +223,10 @@ __global__ __launch_bounds__(BS * 2) void attn_kernel(
         }
       }
     }
+    __syncthreads();  // every wave is done with this V tile
+    if (has_next)
+      issue_tile(vg + (size_t)kb_next * BS * kHeadDim, min(BS, N - kb_next * BS), v_base, wave, lane, true);
+    kb = kb_next;
   }
 
   const float l_tot = l_run + wave_xor_f(l_run, 32);

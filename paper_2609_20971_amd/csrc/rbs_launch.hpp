@@ -16,7 +16,6 @@ struct StatsArgs {
   float* quantiles;
   _Float16* cent16;  // select-ready centroids [H_kv][M][d]
   float* uplift;     // select-ready rescue uplift [H_kv][M]
-  uint32_t* counters;
 };
 
 struct SelectArgs {

@@ -1,13 +1,16 @@
 // Stage 1: per-key-block statistics (Sec. 3.1; Algorithm 1, statistics loops).
 //
-// One workgroup per (KV head, key block) streams the block's B x 128 bf16 keys
-// from HBM exactly once, coalesced (16 lanes cover one 256-byte row), keeps
-// them in registers, and produces the centroid (mean over the block's actual
-// key count) and the radius (max L2 distance to the centroid).  The last
-// workgroup to finish a head -- detected with a per-head completion counter --
-// finds that head's 0.5 / 0.9 radius quantiles with an in-LDS radix select and
-// writes beta and the select-ready uplift for every block of the head, so the
-// whole stage is one launch.
+// stats_kernel: one workgroup per (KV head, key block) streams the block's
+// B x 128 bf16 keys from HBM exactly once, coalesced (16 lanes cover one
+// 256-byte row), keeps them in registers, and produces the centroid (mean over
+// the block's actual key count) and the radius (max L2 distance to the
+// centroid), plus the select-ready f16 copy of the centroid.
+//
+// quantile_kernel: one workgroup per KV head finds the head's 0.5 / 0.9 radius
+// quantiles with an in-LDS radix select over its M radii and writes beta and
+// the select-ready uplift of every block.  It is a separate launch because a
+// device-wide "last workgroup" hand-off would need an agent-scope release per
+// workgroup, which on a multi-XCD gfx950 writes back the whole L2 each time.
 #include "rbs_device.hpp"
 #include "rbs_launch.hpp"
 
@@ -70,19 +73,13 @@ __device__ void radix_select4(const uint32_t* keys, int n, int rank0, int rank1,
 }
 
 template <int BS>
-__global__ __launch_bounds__(kStatsThreads) void stats_kernel(
-    const uint16_t* __restrict__ K, int N, int M, float* __restrict__ centroids, float* radii,
-    float* __restrict__ beta, float* __restrict__ quantiles, _Float16* __restrict__ cent16,
-    float* __restrict__ uplift, uint32_t* counters, float sel_scale) {
+__global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __restrict__ K, int N, int M,
+                                                             float* __restrict__ centroids,
+                                                             float* __restrict__ radii,
+                                                             _Float16* __restrict__ cent16, float sel_scale) {
   constexpr int kRowsPerThread = BS / 16;
   __shared__ float red[4][kHeadDim];
   __shared__ float red_r[4];
-  __shared__ int s_last;
-  __shared__ uint32_t keys[kMaxBlocks];
-  __shared__ uint32_t hist[4 * 256];
-  __shared__ uint32_t sel_prefix[4];
-  __shared__ int sel_remaining[4];
-  __shared__ uint32_t sel_out[4];
 
   const int b = blockIdx.x, g = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -160,17 +157,20 @@ __global__ __launch_bounds__(kStatsThreads) void stats_kernel(
     *reinterpret_cast<f16x8*>(cent16 + blk * kHeadDim + chunk * 8) = h;
   }
   if (tid == 0) radii[blk] = sqrtf(fmaxf(fmaxf(red_r[0], red_r[1]), fmaxf(red_r[2], red_r[3])));
+}
 
-  // Publish, then let the last workgroup of this head finish the head.
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = atomicAdd(&counters[g], 1u) == (uint32_t)(M - 1);
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-
+__global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __restrict__ radii, int M,
+                                                                float* __restrict__ beta,
+                                                                float* __restrict__ quantiles,
+                                                                float* __restrict__ uplift, float sel_scale) {
+  __shared__ uint32_t keys[kMaxBlocks];
+  __shared__ uint32_t hist[4 * 256];
+  __shared__ uint32_t sel_prefix[4];
+  __shared__ int sel_remaining[4];
+  __shared__ uint32_t sel_out[4];
+  const int g = blockIdx.x, tid = threadIdx.x;
   const float* rg_radii = radii + (size_t)g * M;
-  for (int e = tid; e < M; e += kStatsThreads) keys[e] = __float_as_uint(__builtin_nontemporal_load(rg_radii + e));
+  for (int e = tid; e < M; e += kStatsThreads) keys[e] = __float_as_uint(rg_radii[e]);
   __syncthreads();
 
   // Linear interpolation between order statistics: h = (M - 1) p, done in
@@ -198,7 +198,6 @@ __global__ __launch_bounds__(kStatsThreads) void stats_kernel(
   if (tid == 0) {
     quantiles[2 * g + 0] = r_low;
     quantiles[2 * g + 1] = r_high;
-    counters[g] = 0u;
   }
 }
 
@@ -208,8 +207,7 @@ hipError_t launch_stats(const StatsArgs& a, hipStream_t s) {
 #define RBS_STATS_CASE(BSZ)                                                                               \
   case BSZ:                                                                                               \
     hipLaunchKernelGGL(stats_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, a.n_tokens, a.n_blocks,   \
-                       a.centroids, a.radii, a.beta, a.quantiles, a.cent16, a.uplift, a.counters,         \
-                       sel_scale);                                                                        \
+                       a.centroids, a.radii, a.cent16, sel_scale);                                        \
     break;
   switch (a.block_size) {
     RBS_STATS_CASE(64)
@@ -218,6 +216,10 @@ hipError_t launch_stats(const StatsArgs& a, hipStream_t s) {
     default: return hipErrorInvalidValue;
   }
 #undef RBS_STATS_CASE
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(quantile_kernel, dim3(a.n_kv_heads), dim3(kStatsThreads), 0, s, a.radii, a.n_blocks, a.beta,
+                     a.quantiles, a.uplift, sel_scale);
   return hipGetLastError();
 }
 

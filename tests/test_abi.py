@@ -60,7 +60,7 @@ MIS = 0x10001
 
 
 def _stats(rbs, ptr=FAKE, **override):
-    vals = dict(centroids=ptr, radii=ptr, beta=ptr, quantiles=ptr, summary=ptr, counters=ptr)
+    vals = dict(centroids=ptr, radii=ptr, beta=ptr, quantiles=ptr, summary=ptr)
     vals.update(override)
     return rbs.rbs_stats(**vals)
 
@@ -94,7 +94,7 @@ def test_null_and_alignment_errors():
     assert lib.rbs_block_stats(None, FAKE, ctypes.byref(_stats(rbs)), None) == 1
     assert lib.rbs_block_stats(ctypes.byref(s), None, ctypes.byref(_stats(rbs)), None) == 1
     assert lib.rbs_block_stats(ctypes.byref(s), FAKE, None, None) == 1
-    for field in ("centroids", "radii", "beta", "quantiles", "summary", "counters"):
+    for field in ("centroids", "radii", "beta", "quantiles", "summary"):
         assert lib.rbs_block_stats(ctypes.byref(s), FAKE, ctypes.byref(_stats(rbs, **{field: None})), None) == 1
         assert lib.rbs_block_stats(ctypes.byref(s), FAKE, ctypes.byref(_stats(rbs, **{field: MIS})), None) == 5
     assert lib.rbs_block_stats(ctypes.byref(s), MIS, ctypes.byref(_stats(rbs)), None) == 5
