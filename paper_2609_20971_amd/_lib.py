@@ -14,7 +14,9 @@ from dataclasses import dataclass
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "librbs.so")
+# RBS_LIB_PATH points the binding at another build of the same library (for
+# comparing builds); the default is the in-tree one.
+LIB_PATH = os.environ.get("RBS_LIB_PATH") or os.path.join(_HERE, "librbs.so")
 
 RBS_OK, RBS_ERR_NULL, RBS_ERR_SHAPE, RBS_ERR_UNSUPPORTED, RBS_ERR_ARG, RBS_ERR_ALIGN, RBS_ERR_HIP = range(7)
 

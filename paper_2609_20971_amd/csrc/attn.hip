@@ -14,7 +14,8 @@
 // V with the gfx950 LDS transpose read (ds_read_b64_tr_b16).  The two tiles
 // are pipelined against compute: the next block's K is fetched while this
 // block's softmax and PV run, the next V while the next QK^T runs.  Online
-// softmax in fp32 with exp2; P is rounded to bf16 for the PV product.  Causal
+// softmax in fp32 with exp2; P is rounded to bf16 for the PV product, and the
+// softmax denominator sums exactly those rounded values (v_dot2 with ones).  Causal
 // masking is applied on the diagonal block only; keys past N are masked in a
 // short last block (their rows are loaded as copies of the last valid key).
 #include "rbs_device.hpp"
@@ -128,6 +129,9 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
 
   const uint32_t k_base = lds_offset(k_lds), v_base = lds_offset(v_lds);
   int kb = count > 0 ? min(max(list[0], 0), i) : 0;
+  // The index of block n + 1 is read one iteration ahead so that its scalar
+  // load is off the critical path.
+  int kb_ahead = count > 1 ? list[1] : 0;
   if (count > 0) {
     const int nk0 = min(BS, N - kb * BS);
     issue_tile(kg + (size_t)kb * BS * kHeadDim, nk0, k_base, wave, lane, false);
@@ -135,7 +139,8 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   }
   for (int n = 0; n < count; ++n) {
     const bool has_next = n + 1 < count;
-    const int kb_next = has_next ? min(max(list[n + 1], 0), i) : 0;
+    const int kb_next = has_next ? min(max(kb_ahead, 0), i) : 0;
+    kb_ahead = n + 2 < count ? list[n + 2] : 0;
     const int nk = min(BS, N - kb * BS);
     const bool diag = kb == i;
 
@@ -182,16 +187,11 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       const float m_new = fmaxf(m_run, mx);
       const float ms = m_new == -INFINITY ? 0.f : m_new * scale_log2;
       const float alpha = fast_exp2(m_run * scale_log2 - ms);
-      float psum = 0.f;
 #pragma unroll
       for (int mt = 0; mt < KT; ++mt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(fmaf(s[mt][r], scale_log2, -ms));
-          s[mt][r] = p;
-          psum += p;
-        }
-      l_run = l_run * alpha + psum;
+        for (int r = 0; r < 16; ++r) s[mt][r] = fast_exp2(fmaf(s[mt][r], scale_log2, -ms));
+      l_run = l_run * alpha;
       m_run = m_new;
       if (__any(alpha != 1.f)) {
 #pragma unroll
@@ -208,6 +208,15 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         bf16x8 pb;
 #pragma unroll
         for (int e = 0; e < 8; ++e) pb[e] = (__bf16)s[c >> 1][8 * (c & 1) + e];
+        {
+          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+          const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bf16x2 pair = {pb[2 * e], pb[2 * e + 1]};
+            l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+          }
+        }
         const int row0 = kbase + 16 * c + 4 * half + vq;
         const unsigned char* v0 = v_lds + row0 * 256 + vbyte;
         const unsigned char* v1 = v0 + 8 * 256;
