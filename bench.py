@@ -26,7 +26,7 @@ if ROOT not in sys.path:
 METRIC = "128K sparse prefill-attn ms/layer, speedup vs own dense, MFMA util %"
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E, vendor figure
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA, vendor figure (no sparsity)
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "attn_traffic_qwen3-30b-a3b-128k.json")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def _log(msg):
@@ -190,22 +190,10 @@ def main():
     density = counts_sum / alg["pairs"]
 
     # Own dense path: same attention kernel over every causal block.
-    dcounts, dindices = rbs.allocate_lists(shape, dev)
-    rbs.rbs_dense_indices(shape, dcounts, dindices, stream=stream)
-    Od = torch.empty_like(Q)
-    rbs.rbs_sparse_prefill(shape, Q, K, V, dcounts, dindices, 0.0, Od, stream=stream)
-    torch.cuda.synchronize()
-    dense_ms = []
-    for _ in range(args.dense_reps):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        rbs.rbs_sparse_prefill(shape, Q, K, V, dcounts, dindices, 0.0, Od, stream=stream)
-        b.record(stream)
-        b.synchronize()
-        dense_ms.append(a.elapsed_time(b))
-    dense_ms = float(np.median(dense_ms))
-    _log(f"[bench] dense attention {dense_ms:.3f} ms")
-    del Od, dcounts, dindices
+    dense_ms = None
+    if args.dense_reps > 0:
+        dense_ms = _time_dense(rbs, torch, np, shape, Q, K, V, stream, args.dense_reps)
+        _log(f"[bench] dense attention {dense_ms:.3f} ms")
 
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -215,17 +203,12 @@ def main():
         del src, dst
 
     attn_tflops = alg["attn_flops"] / (stage_ms[2] * 1e-3) / 1e12
-    dense_tflops = alg["dense_flops"] / (dense_ms * 1e-3) / 1e12
+    dense_tflops = alg["dense_flops"] / (dense_ms * 1e-3) / 1e12 if dense_ms else None
     stats_gbps = alg["stats_bytes"] / (stage_ms[0] * 1e-3) / 1e9
     select_gbps = alg["select_bytes"] / (stage_ms[1] * 1e-3) / 1e9
     select_tflops = alg["select_flops"] / (stage_ms[1] * 1e-3) / 1e12
 
-    traffic = None
-    if os.path.exists(PROFILE_TRAFFIC):
-        with open(PROFILE_TRAFFIC) as f:
-            prof = json.load(f)
-        if prof.get("workload") == w.name and prof.get("kernel_source_sha") == _attn_source_sha():
-            traffic = prof.get("bytes_per_launch")
+    traffic = _profiled_traffic("attn_kernel", w.name, "attn.hip")
 
     result = {
         "metric": METRIC,
@@ -244,12 +227,12 @@ def main():
                    "head_dim": w.head_dim, "block_size": w.block_size, "tau_base": w.tau_base,
                    "tau_rescue": w.tau_rescue, "n_sink": w.n_sink, "n_local": w.n_local,
                    "n_recent": w.n_recent, "seed": w.seed},
-        "speedup_vs_dense": round(dense_ms / ms_per_step, 3),
-        "attn_speedup_vs_dense": round(dense_ms / stage_ms[2], 3),
+        "speedup_vs_dense": round(dense_ms / ms_per_step, 3) if dense_ms else None,
+        "attn_speedup_vs_dense": round(dense_ms / stage_ms[2], 3) if dense_ms else None,
         "mfma_util_pct": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
         "density": round(density, 6),
-        "dense_attn_ms": round(dense_ms, 3),
-        "dense_mfma_util_pct": round(100.0 * dense_tflops / PEAK_BF16_TFLOPS, 2),
+        "dense_attn_ms": round(dense_ms, 3) if dense_ms else None,
+        "dense_mfma_util_pct": round(100.0 * dense_tflops / PEAK_BF16_TFLOPS, 2) if dense_ms else None,
         "wall_ms_per_step": round(wall_ms, 4),
         "stages": {
             "stats": {"ms": round(float(stage_ms[0]), 4), "alg_bytes": alg["stats_bytes"],
@@ -273,10 +256,45 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def _attn_source_sha():
+def _time_dense(rbs, torch, np, shape, Q, K, V, stream, reps: int) -> float:
+    """Median time of the attention kernel over every causal block (the
+    build's own dense path), HIP events on the launch stream."""
+    dcounts, dindices = rbs.allocate_lists(shape, Q.device)
+    rbs.rbs_dense_indices(shape, dcounts, dindices, stream=stream)
+    Od = torch.empty_like(Q)
+    rbs.rbs_sparse_prefill(shape, Q, K, V, dcounts, dindices, 0.0, Od, stream=stream)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        rbs.rbs_sparse_prefill(shape, Q, K, V, dcounts, dindices, 0.0, Od, stream=stream)
+        b.record(stream)
+        b.synchronize()
+        times.append(a.elapsed_time(b))
+    del Od, dcounts, dindices
+    return float(np.median(times))
+
+
+def _profiled_traffic(kernel: str, workload: str, source: str):
+    """HBM bytes per launch from the committed rocprofv3 summary of this kernel
+    on this workload, or None when there is none or the kernel source changed
+    since the counters were taken."""
     import hashlib
-    with open(os.path.join(ROOT, "paper_2609_20971_amd", "csrc", "attn.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    path = os.path.join(PROFILES, f"{kernel}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ": " in line and not line.startswith(" "):
+                k, v = line.split(": ", 1)
+                fields[k.strip()] = v.strip()
+    with open(os.path.join(ROOT, "paper_2609_20971_amd", "csrc", source), "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    if fields.get("source_sha") != sha or "traffic_bytes_per_launch" not in fields:
+        return None
+    return int(float(fields["traffic_bytes_per_launch"]))
 
 
 if __name__ == "__main__":
