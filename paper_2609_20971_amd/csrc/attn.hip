@@ -34,7 +34,9 @@ __device__ __forceinline__ int vswz(int r, int c) { return c ^ ((r & 3) << 2); }
 
 // Workgroup id -> logical work item, so that groups of 8 consecutive items
 // (the query heads of one KV group, same query block) run on the same XCD
-// (workgroups are dealt to the 8 XCDs round-robin by id).
+// (workgroups are dealt to the 8 XCDs round-robin by id) and share its L2.
+// Items are ordered KV-group-major, so all XCDs work on one KV head's K/V
+// (64 MiB at 128K) at a time and the Infinity Cache holds it.
 __device__ __forceinline__ int xcd_remap(int id, int total) {
   const int full = total & ~63;
   if (id >= full) return id;
@@ -89,9 +91,12 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
   const int work = xcd_remap(blockIdx.x, gridDim.x);
-  const int i = M - 1 - work / Hq;
-  const int h = work % Hq;
-  const int g = h / group;
+  // KV-group-major order: all rows of one KV group run before the next group's.
+  const int per_group = M * group;
+  const int g = work / per_group;
+  const int rem = work - g * per_group;
+  const int i = M - 1 - rem / group;
+  const int h = g * group + rem % group;
   const int q_local = 32 * wave + l32;  // query index inside the block
   const int qpos = i * BS + q_local;
   const bool q_ok = qpos < N;
