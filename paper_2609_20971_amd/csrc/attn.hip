@@ -78,6 +78,9 @@ __device__ __forceinline__ void issue_tile(const uint16_t* tile_base, int nk, ui
   }
 }
 
+// Rescale threshold of the online softmax, in log2 units.
+constexpr float kRescaleSlack = 8.0f;
+
 template <int BS>
 __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V, int N, int M,
@@ -120,7 +123,8 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const uint16_t* kg = K + (size_t)g * N * kHeadDim;
   const uint16_t* vg = V + (size_t)g * N * kHeadDim;
 
-  float m_run = -INFINITY, l_run = 0.f;
+  float ms_run = -INFINITY;  // running reference maximum, log2 units
+  float l_run = 0.f;         // this lane's share of the softmax denominator
   f32x16 o[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
@@ -189,23 +193,29 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
       mx = fmaxf(mx, wave_xor_f(mx, 32));
-      const float m_new = fmaxf(m_run, mx);
-      const float ms = m_new == -INFINITY ? 0.f : m_new * scale_log2;
-      const float alpha = fast_exp2(m_run * scale_log2 - ms);
-#pragma unroll
-      for (int mt = 0; mt < KT; ++mt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[mt][r] = fast_exp2(fmaf(s[mt][r], scale_log2, -ms));
-      l_run = l_run * alpha;
-      m_run = m_new;
-      if (__any(alpha != 1.f)) {
+      // Lazily raised reference maximum (log2 units): O and the denominator
+      // are rescaled only when some row's maximum exceeds the reference by
+      // more than kRescaleSlack, so the exponentials stay below 2^kRescaleSlack.
+      const float mxs = mx * scale_log2;
+      if (__any(mxs > ms_run + kRescaleSlack)) {
+        const float ms_new = fmaxf(ms_run, mxs);
+        const float alpha = ms_new == ms_run ? 1.f : fast_exp2(ms_run - ms_new);
+        ms_run = ms_new;
+        l_run *= alpha;
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
       }
+      const float shift = ms_run == -INFINITY ? 0.f : ms_run;
+#pragma unroll
+      for (int mt = 0; mt < KT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[mt][r] = fast_exp2(fmaf(s[mt][r], scale_log2, -shift));
       if (sub == 0) {
-        if (has_next) RBS_WAIT_VMCNT(8); else RBS_WAIT_VMCNT(0);  // this block's V has landed
+        // This block's V has landed.  The next block's K copies are already
+        // in flight behind it only when the block has a single step.
+        if (has_next && BS / SUB == 1) RBS_WAIT_VMCNT(8); else RBS_WAIT_VMCNT(0);
         __syncthreads();
       }
 #pragma unroll
@@ -260,7 +270,7 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         *reinterpret_cast<uint2*>(orow + d0) = packed;
       }
     if (lse != nullptr && half == 0)
-      lse[(size_t)h * N + qpos] = l_tot > 0.f ? (m_run * scale_log2 + log2f(l_tot)) / kLog2e : -INFINITY;
+      lse[(size_t)h * N + qpos] = l_tot > 0.f ? (ms_run + log2f(l_tot)) / kLog2e : -INFINITY;
   }
 }
 
