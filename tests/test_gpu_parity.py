@@ -85,6 +85,20 @@ def test_edge_shapes(variant):
     _full_check(w)
 
 
+@pytest.mark.parametrize("variant", [
+    dict(seq_len=6000, block_size=64, n_q_heads=4, n_kv_heads=2, seed=11),         # 94 blocks, ragged
+    dict(seq_len=9000, block_size=256, n_q_heads=4, n_kv_heads=1, seed=12),        # 36 blocks, two softmax steps per block
+    dict(seq_len=8191, block_size=128, n_q_heads=8, n_kv_heads=2, seed=13),        # 64 blocks, one row short
+])
+def test_multiblock_rows(variant):
+    """Rows spanning many key blocks at every block size: selection on all rows,
+    attention on a sample that includes the ragged last row."""
+    w = WORKLOADS["tiny-2k"].with_(name="multiblock", needles_per_kv_head=6, **variant)
+    M = w.n_blocks
+    attn = H.sample_rows(w.n_q_heads, M, 16, seed=variant["seed"], include=[(0, M - 1), (w.n_q_heads - 1, M - 2)])
+    _full_check(w, attn_rows=attn)
+
+
 @pytest.mark.parametrize("tau,forced", [
     ((0.0, 0.0), (1, 2, 0)),     # alpha = 0: every causal block
     ((1.0, 1.0), (0, 1, 0)),     # alpha = 1: argmax blocks only
@@ -170,3 +184,24 @@ def test_qwen3_30b_128k_sampled():
     w = WORKLOADS["qwen3-30b-a3b-128k"]
     rows = H.sample_rows(w.n_q_heads, w.n_blocks, 24, seed=2, include=[(5, 1023), (31, 700), (0, 3)])
     _full_check(w, select_rows=rows, attn_rows=rows[:10])
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["qwen3-30b-a3b-128k-b64", "qwen3-30b-a3b-128k-b256"])
+def test_qwen3_30b_128k_other_block_sizes_sampled(name):
+    """The 128K layer at 64- and 256-token blocks; sampled rows."""
+    w = WORKLOADS[name]
+    M = w.n_blocks
+    rows = H.sample_rows(w.n_q_heads, M, 16, seed=3, include=[(7, M - 1), (0, 1)])
+    attn = H.sample_rows(w.n_q_heads, M, 4, seed=5, include=[(7, M - 1), (0, 1)])
+    _full_check(w, select_rows=rows, attn_rows=attn)
+
+
+@pytest.mark.slow
+def test_qwen3_32b_64k_sampled():
+    """64 query heads over 8 KV heads, two key-noise regimes; sampled rows."""
+    w = WORKLOADS["qwen3-32b-64k"]
+    M = w.n_blocks
+    rows = H.sample_rows(w.n_q_heads, M, 24, seed=4, include=[(0, M - 1), (63, 300), (40, 2)])
+    attn = H.sample_rows(w.n_q_heads, M, 5, seed=6, include=[(0, M - 1), (63, 300), (40, 2)])
+    _full_check(w, select_rows=rows, attn_rows=attn)
