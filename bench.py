@@ -45,6 +45,8 @@ def parse():
                    help="sampled (head, query block) rows for the oracle's selection timing")
     p.add_argument("--cpu-attn-rows", type=int, default=24,
                    help="sampled (head, query block) rows for the oracle's attention timing")
+    p.add_argument("--fused-steps", type=int, default=5,
+                   help="also time this many steps through the fused select-then-attend entry (0 skips)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a 1 GiB device copy (for scaling HBM counters)")
     return p.parse_args()
@@ -184,6 +186,38 @@ def main():
     _log(f"[bench] timed {args.steps} steps: stats {stage_ms[0]:.3f} ms, select {stage_ms[1]:.3f} ms, "
          f"attention {stage_ms[2]:.3f} ms (wall {wall_ms:.3f} ms/step)")
 
+    # The fused entry point over the same steps (same results, one pass).
+    fused_ms = None
+    if args.fused_steps > 0:
+        fcounts, findices = rbs.allocate_lists(shape, dev)
+        Of = torch.empty_like(Q)
+
+        def fstep(ev=None):
+            if ev is not None:
+                ev[0].record(stream)
+            rbs.rbs_block_stats(shape, K, stats, stream=stream)
+            if ev is not None:
+                ev[1].record(stream)
+            rbs.rbs_select_attend(shape, Q, K, V, stats, w.tau_base, w.tau_rescue, w.n_sink, w.n_local,
+                                  w.n_recent, 0.0, fcounts, findices, Of, stream=stream)
+            if ev is not None:
+                ev[2].record(stream)
+
+        for _ in range(min(args.warmup, 2)):
+            fstep()
+        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.fused_steps)]
+        for k in range(args.fused_steps):
+            fstep(fev[k])
+        torch.cuda.synchronize()
+        f = np.zeros(2)
+        for ev in fev:
+            f += [ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])]
+        f /= args.fused_steps
+        fused_ms = (float(f[0]), float(f[1]))
+        _log(f"[bench] fused path: stats {f[0]:.3f} ms, select+attention {f[1]:.3f} ms "
+             f"(total {f.sum():.3f} ms/step)")
+        del Of, fcounts, findices
+
     counts_np = counts.cpu().numpy()
     counts_sum = int(counts_np.sum())
     alg = algorithmic(w, counts_sum)
@@ -244,6 +278,9 @@ def main():
             "attn": {"ms": round(float(stage_ms[2]), 4), "alg_flops": alg["attn_flops"],
                      "TFLOPs": round(attn_tflops, 1), "executed_pairs": counts_sum},
         },
+        "fused": ({"ms_per_step": round(sum(fused_ms), 4), "stats_ms": round(fused_ms[0], 4),
+                   "select_attend_ms": round(fused_ms[1], 4), "steps": args.fused_steps}
+                  if fused_ms else None),
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic},
     }

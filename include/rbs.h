@@ -9,6 +9,8 @@
  *                       query-block key-block index lists     (Sec. 3.2)
  *   rbs_sparse_prefill  causal GQA block-sparse attention over the selected
  *                       blocks                                (Sec. 3.3)
+ *   rbs_select_attend   both in one pass (Algorithm 1 from the selection loop
+ *                       on), same results as the two calls in sequence
  *
  * Conventions shared by every call
  *   - Tensors are dense, row-major, in device memory:
@@ -130,6 +132,19 @@ int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats,
 int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, const void* V,
                        const int32_t* counts, const int32_t* indices, float softmax_scale,
                        void* O, float* lse, void* stream);
+
+/* rbs_select then rbs_sparse_prefill in one pass (Algorithm 1, selection loop
+ * and attention; Sec. 3.2-3.3): each (query head, query block) selects its key
+ * blocks and attends over them at once, the list kept on chip.  Arguments as
+ * in the two calls; counts/indices are still written (same layout and values
+ * as rbs_select), and O/lse equal those of rbs_sparse_prefill on those lists.
+ * Saves the second read of Q and the round trip of the lists through memory.
+ * Validation and errors: the union of the two calls' rules.
+ */
+int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, const void* V,
+                      const rbs_stats* stats, float tau_base, float tau_rescue, int32_t n_sink,
+                      int32_t n_local, int32_t n_recent, float softmax_scale, int32_t* counts,
+                      int32_t* indices, void* O, float* lse, void* stream);
 
 /* Full causal lists (every block 0..i for every row): the dense path. */
 int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream);

@@ -3,6 +3,7 @@
     stats = rbs_block_stats(shape, K)                                  # Sec. 3.1
     counts, indices = rbs_select(shape, Q, stats, tau_b, tau_r, sink, local, recent)  # Sec. 3.2
     O = rbs_sparse_prefill(shape, Q, K, V, counts, indices)            # Sec. 3.3
+    counts, indices, O = rbs_select_attend(shape, Q, K, V, stats, ...)   # Sec. 3.2-3.3 in one pass
 """
 
 from ._lib import (  # noqa: F401
@@ -16,6 +17,7 @@ from ._lib import (  # noqa: F401
     rbs_dense_indices,
     rbs_index_capacity,
     rbs_select,
+    rbs_select_attend,
     rbs_shape,
     rbs_sparse_prefill,
     rbs_stats,

@@ -138,6 +138,57 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
   return from_hip(rbs::launch_attention(a, static_cast<hipStream_t>(stream)));
 }
 
+int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, const void* V, const rbs_stats* stats,
+                      float tau_base, float tau_rescue, int32_t n_sink, int32_t n_local, int32_t n_recent,
+                      float softmax_scale, int32_t* counts, int32_t* indices, void* O, float* lse, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (Q == nullptr || K == nullptr || V == nullptr || O == nullptr || counts == nullptr || indices == nullptr ||
+      stats == nullptr || stats->summary == nullptr)
+    return RBS_ERR_NULL;
+  if (!(tau_base >= 0.f && tau_base <= 1.f) || !(tau_rescue >= 0.f && tau_rescue <= 1.f)) return RBS_ERR_ARG;
+  if (n_sink < 0 || n_local < 1 || n_recent < 0) return RBS_ERR_ARG;
+  if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(counts) ||
+      !aligned16(indices) || !aligned16(stats->summary) || (lse != nullptr && !aligned16(lse)))
+    return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  rbs::SelectArgs sa;
+  sa.Q = static_cast<const uint16_t*>(Q);
+  sa.n_tokens = shape->n_tokens;
+  sa.n_q_heads = shape->n_q_heads;
+  sa.n_kv_heads = shape->n_kv_heads;
+  sa.block_size = shape->block_size;
+  sa.n_blocks = M;
+  sa.cent16 = static_cast<const _Float16*>(stats->summary);
+  sa.uplift = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
+                                             rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  sa.tau_base = tau_base;
+  sa.tau_rescue = tau_rescue;
+  sa.n_sink = n_sink;
+  sa.n_local = n_local;
+  sa.n_recent = n_recent;
+  sa.counts = counts;
+  sa.indices = indices;
+  sa.capacity = rbs_index_capacity(M);
+  rbs::AttnArgs aa;
+  aa.Q = sa.Q;
+  aa.K = static_cast<const uint16_t*>(K);
+  aa.V = static_cast<const uint16_t*>(V);
+  aa.n_tokens = shape->n_tokens;
+  aa.n_q_heads = shape->n_q_heads;
+  aa.n_kv_heads = shape->n_kv_heads;
+  aa.block_size = shape->block_size;
+  aa.n_blocks = M;
+  aa.counts = counts;
+  aa.indices = indices;
+  aa.capacity = sa.capacity;
+  aa.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
+  aa.O = static_cast<uint16_t*>(O);
+  aa.lse = lse;
+  return from_hip(rbs::launch_select_attend(sa, aa, static_cast<hipStream_t>(stream)));
+}
+
 int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream) {
   int rc = check_shape(shape);
   if (rc != RBS_OK) return rc;

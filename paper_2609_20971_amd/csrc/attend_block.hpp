@@ -1,0 +1,311 @@
+// Stage 3 device code: causal GQA block-sparse attention of one query block
+// (Sec. 3.3; Algorithm 1, last step), shared by the stand-alone attention
+// kernel and the fused select-then-attend kernel.
+//
+// One workgroup per (query head, query block); wave w owns 32 query tokens.
+// The kernel works in the transposed orientation so that every lane owns one
+// query: S^T = K Q^T and O^T = V^T P^T on the bf16 32x32x16 MFMA, with Q held
+// in registers as the B operand.  Row softmax (max, exp2, sum) is then
+// lane-local plus one exchange with lane^32, and the O rescale is lane-local.
+//
+// K and V tiles of each listed key block go straight from global memory to
+// LDS (global_load_lds_dwordx4: no registers), 256-byte rows with 16-byte
+// chunks XOR-swizzled per row so that MFMA operand reads are bank-conflict
+// free.  K feeds the A operand with 128-bit reads; V^T is read from row-major
+// V with the gfx950 LDS transpose read (ds_read_b64_tr_b16).  The two tiles
+// are pipelined against compute: the next block's K is fetched while this
+// block's softmax and PV run, the next V while the next QK^T runs.  Online
+// softmax in fp32 with exp2; P is rounded to bf16 for the PV product, and the
+// softmax denominator sums exactly those rounded values (v_dot2 with ones).  Causal
+// masking is applied on the diagonal block only; keys past N are masked in a
+// short last block (their rows are loaded as copies of the last valid key).
+#pragma once
+
+#include "rbs_device.hpp"
+#include "rbs_launch.hpp"
+
+namespace rbs {
+
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// Physical 16-byte chunk of logical chunk c in staged row r.
+__device__ __forceinline__ int kswz(int r, int c) { return c ^ (r & 15); }
+__device__ __forceinline__ int vswz(int r, int c) { return c ^ ((r & 3) << 2); }
+
+// vmcnt(n) with expcnt/lgkmcnt left unconstrained (gfx9 encoding).
+#define RBS_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | 0x0F70)
+
+// Workgroup id -> logical work item, so that groups of 8 consecutive items
+// (the query heads of one KV group, same query block) run on the same XCD
+// (workgroups are dealt to the 8 XCDs round-robin by id) and share its L2.
+// Items are ordered KV-group-major, so all XCDs work on one KV head's K/V
+// (64 MiB at 128K) at a time and the Infinity Cache holds it.
+__device__ __forceinline__ int xcd_remap(int id, int total) {
+  const int full = total & ~63;
+  if (id >= full) return id;
+  const int x = id & 7, s = id >> 3;
+  return ((s >> 3) << 6) + (x << 3) + (s & 7);
+}
+
+// One 16-byte-per-lane global -> LDS copy: lane l's 16 bytes from
+// gbase + voff land at LDS byte lds_addr + 16 l.  Issued from inline assembly
+// so that the compiler's wait-count pass does not treat every later LDS read as
+// dependent on it (it would wait for all outstanding copies); the kernel waits
+// for the copies it needs with explicit vmcnt counts instead.  Later-issued
+// vector loads only make the compiler's own waits more conservative.
+__device__ __forceinline__ void lds_dma16(const void* gbase, uint32_t voff, uint32_t lds_addr) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
+      : "v"(voff), "s"(gbase), "s"(lds_addr)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)p;
+}
+
+// Wave w copies rows 32w .. 32w + 31 of a B x 128 bf16 tile (8 copies of
+// 4 rows each).  Rows at or past nk repeat row nk - 1 (masked later).
+__device__ __forceinline__ void issue_tile(const uint16_t* tile_base, int nk, uint32_t lds_base, int wave, int lane,
+                                           bool is_v) {
+  const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds_base + (uint32_t)(32 * wave) * 256u);
+  const int pc = lane & 15;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int row = 32 * wave + 4 * j + (lane >> 4);
+    const int c = is_v ? vswz(row, pc) : kswz(row, pc);
+    const uint32_t voff = (uint32_t)min(row, nk - 1) * 256u + 16u * (uint32_t)c;
+    lds_dma16(tile_base, voff, lds_wave + (uint32_t)j * 1024u);
+  }
+}
+
+// Rescale threshold of the online softmax, in log2 units.
+constexpr float kRescaleSlack = 8.0f;
+
+// Arguments of one attention pass, shared by the stand-alone and the fused kernel.
+struct AttnCore {
+  const uint16_t* Q;
+  const uint16_t* K;
+  const uint16_t* V;
+  int N, M, group;
+  float scale_log2;
+  uint16_t* O;
+  float* lse;
+};
+
+// Attention of query block i of query head h over the count key blocks that
+// list_at(0 .. count - 1) returns (wave-uniform, ascending, each <= i), by the
+// B/32 waves of the calling workgroup.  k_lds and v_lds: B * 256 bytes of LDS
+// each, 256-byte aligned.
+template <int BS, typename ListAt>
+__device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, int count, ListAt list_at,
+                                             unsigned char* k_lds, unsigned char* v_lds) {
+  constexpr int SUB = BS < 128 ? BS : 128;  // keys per softmax step
+  constexpr int KT = SUB / 32;              // 32-key MFMA tiles per step
+  const uint16_t* __restrict__ Q = c.Q;
+  const int N = c.N;
+  const float scale_log2 = c.scale_log2;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int g = h / c.group;
+  const int q_local = 32 * wave + l32;  // query index inside the block
+  const int qpos = i * BS + q_local;
+  const bool q_ok = qpos < N;
+
+  bf16x8 qreg[8];
+  {
+    const uint16_t* qrow = Q + ((size_t)h * N + qpos) * kHeadDim + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      const uint4 v = q_ok ? *reinterpret_cast<const uint4*>(qrow + 16 * ks) : make_uint4(0u, 0u, 0u, 0u);
+      __builtin_memcpy(&qreg[ks], &v, 16);
+    }
+  }
+  // Q must be resident before any tile copy is issued: the copies are
+  // invisible to the compiler, so a wait it placed for Q inside the loop
+  // would also wait for them.
+  RBS_WAIT_VMCNT(0);
+
+  const uint16_t* kg = c.K + (size_t)g * N * kHeadDim;
+  const uint16_t* vg = c.V + (size_t)g * N * kHeadDim;
+
+  float ms_run = -INFINITY;  // running reference maximum, log2 units
+  float l_run = 0.f;         // this lane's share of the softmax denominator
+  f32x16 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
+
+  // Per-lane LDS read bases.  K: row 32mt + l32 of the step, chunk 2ks + half.
+  // V (transposed read): lane sources row 16c + 4 half + (lane%16)/4 (and +8),
+  // dims 32dt + 16((lane/16)%2) + 4(lane%4); it receives dim 32dt + l32.
+  const int vq = (lane & 15) >> 2;
+  const int vsub = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);  // chunk within the dt group
+  const int vbyte = 8 * (lane & 1);
+
+  const uint32_t k_base = lds_offset(k_lds), v_base = lds_offset(v_lds);
+  int kb = count > 0 ? min(max(list_at(0), 0), i) : 0;
+  // The index of block n + 1 is read one iteration ahead so that its scalar
+  // load is off the critical path.
+  int kb_ahead = count > 1 ? list_at(1) : 0;
+  if (count > 0) {
+    const int nk0 = min(BS, N - kb * BS);
+    issue_tile(kg + (size_t)kb * BS * kHeadDim, nk0, k_base, wave, lane, false);
+    issue_tile(vg + (size_t)kb * BS * kHeadDim, nk0, v_base, wave, lane, true);
+  }
+  for (int n = 0; n < count; ++n) {
+    const bool has_next = n + 1 < count;
+    const int kb_next = has_next ? min(max(kb_ahead, 0), i) : 0;
+    kb_ahead = n + 2 < count ? list_at(n + 2) : 0;
+    const int nk = min(BS, N - kb * BS);
+    const bool diag = kb == i;
+
+    RBS_WAIT_VMCNT(8);  // this block's K has landed (its V may still be in flight)
+    __syncthreads();
+
+#pragma unroll
+    for (int sub = 0; sub < BS / SUB; ++sub) {
+      const int kbase = sub * SUB;
+      f32x16 s[KT];
+#pragma unroll
+      for (int mt = 0; mt < KT; ++mt) {
+        s[mt] = f32x16{};
+        const int row = kbase + 32 * mt + l32;
+        const unsigned char* krow = k_lds + row * 256;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+          const uint4 raw = *reinterpret_cast<const uint4*>(krow + 16 * kswz(row, 2 * ks + half));
+          bf16x8 a;
+          __builtin_memcpy(&a, &raw, 16);
+          s[mt] = mfma_bf16(a, qreg[ks], s[mt]);
+        }
+      }
+      if (sub == BS / SUB - 1) {
+        __syncthreads();  // every wave is done with this K tile
+        if (has_next)
+          issue_tile(kg + (size_t)kb_next * BS * kHeadDim, min(BS, N - kb_next * BS), k_base, wave, lane, false);
+      }
+      if (diag || nk < BS) {
+#pragma unroll
+        for (int mt = 0; mt < KT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kbase + 32 * mt + mfma_row(r, lane);
+            if (key >= nk || (diag && key > q_local)) s[mt][r] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < KT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
+      mx = fmaxf(mx, wave_xor_f(mx, 32));
+      // Lazily raised reference maximum (log2 units): O and the denominator
+      // are rescaled only when some row's maximum exceeds the reference by
+      // more than kRescaleSlack, so the exponentials stay below 2^kRescaleSlack.
+      const float mxs = mx * scale_log2;
+      if (__any(mxs > ms_run + kRescaleSlack)) {
+        const float ms_new = fmaxf(ms_run, mxs);
+        const float alpha = ms_new == ms_run ? 1.f : fast_exp2(ms_run - ms_new);
+        ms_run = ms_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+      }
+      const float shift = ms_run == -INFINITY ? 0.f : ms_run;
+#pragma unroll
+      for (int mt = 0; mt < KT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[mt][r] = fast_exp2(fmaf(s[mt][r], scale_log2, -shift));
+      if (sub == 0) {
+        // This block's V has landed.  The next block's K copies are already
+        // in flight behind it only when the block has a single step.
+        if (has_next && BS / SUB == 1) RBS_WAIT_VMCNT(8); else RBS_WAIT_VMCNT(0);
+        __syncthreads();
+      }
+#pragma unroll
+      for (int c = 0; c < SUB / 16; ++c) {
+        bf16x8 pb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[e] = (__bf16)s[c >> 1][8 * (c & 1) + e];
+        {
+          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+          const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bf16x2 pair = {pb[2 * e], pb[2 * e + 1]};
+            l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+          }
+        }
+        const int row0 = kbase + 16 * c + 4 * half + vq;
+        const unsigned char* v0 = v_lds + row0 * 256 + vbyte;
+        const unsigned char* v1 = v0 + 8 * 256;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) {
+          const int pc = 16 * vswz(row0, 4 * dt + vsub);  // row0 and row0 + 8 share the swizzle
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v0 + pc));
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v1 + pc));
+          bf16x8 a;
+          __builtin_memcpy(&a, &lo, 8);
+          __builtin_memcpy(reinterpret_cast<unsigned char*>(&a) + 8, &hi, 8);
+          o[dt] = mfma_bf16(a, pb, o[dt]);
+        }
+      }
+    }
+    __syncthreads();  // every wave is done with this V tile
+    if (has_next)
+      issue_tile(vg + (size_t)kb_next * BS * kHeadDim, min(BS, N - kb_next * BS), v_base, wave, lane, true);
+    kb = kb_next;
+  }
+
+  const float l_tot = l_run + wave_xor_f(l_run, 32);
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+  if (q_ok) {
+    uint16_t* orow = c.O + ((size_t)h * N + qpos) * kHeadDim;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int d0 = 32 * dt + 8 * rq + 4 * half;
+        __bf16 v4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(o[dt][4 * rq + e] * inv);
+        uint2 packed;
+        __builtin_memcpy(&packed, v4, 8);
+        *reinterpret_cast<uint2*>(orow + d0) = packed;
+      }
+    if (c.lse != nullptr && half == 0)
+      c.lse[(size_t)h * N + qpos] = l_tot > 0.f ? (ms_run + log2f(l_tot)) / kLog2e : -INFINITY;
+  }
+}
+
+
+// Workgroup id -> (query head, query block): KV-group-major, late rows first
+// within a group, the group's query heads adjacent (and on one XCD).
+__device__ __forceinline__ void work_item(int M, int group, int& h, int& i) {
+  const int work = xcd_remap(blockIdx.x, gridDim.x);
+  const int per_group = M * group;
+  const int g = work / per_group;
+  const int rem = work - g * per_group;
+  i = M - 1 - rem / group;
+  h = g * group + rem % group;
+}
+
+inline AttnCore make_attn_core(const AttnArgs& a) {
+  AttnCore c;
+  c.Q = a.Q;
+  c.K = a.K;
+  c.V = a.V;
+  c.N = a.n_tokens;
+  c.M = a.n_blocks;
+  c.group = a.n_q_heads / a.n_kv_heads;
+  c.scale_log2 = a.scale * kLog2e;
+  c.O = a.O;
+  c.lse = a.lse;
+  return c;
+}
+
+}  // namespace rbs

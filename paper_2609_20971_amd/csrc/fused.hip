@@ -1,0 +1,71 @@
+// Stages 2 and 3 fused (the select-then-attend entry point): one workgroup
+// per (query head, query block) selects its key blocks (Sec. 3.2) and attends
+// over them at once (Sec. 3.3), with the compacted list kept in LDS.  The list
+// is also written out, so the results are those of rbs_select followed by
+// rbs_sparse_prefill: the same device code runs, on the same inputs.  The
+// second read of Q and the index round trip through HBM go away, and a
+// workgroup's exp-bound selection can overlap other workgroups' MFMA-bound
+// attention on the same compute unit.
+#include "attend_block.hpp"
+#include "rbs_launch.hpp"
+#include "select_block.hpp"
+
+namespace rbs {
+
+// Bytes of the LDS region shared by the selection scratch and the K/V tiles;
+// the list (M int32) follows it.
+template <int BS>
+constexpr size_t fused_region_bytes(int M) {
+  const size_t tiles = 2 * (size_t)BS * 256, sel = select_smem_bytes<BS>(M);
+  return ((tiles > sel ? tiles : sel) + 255) & ~(size_t)255;
+}
+
+template <int BS>
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void select_attend_kernel(
+    SelectCore sc, AttnCore ac) {
+  extern __shared__ __align__(1024) unsigned char smem[];
+  int h, i;
+  work_item(ac.M, ac.group, h, i);
+  typedef __attribute__((address_space(3))) int32_t lds_i32;
+  lds_i32* list_lds = (lds_i32*)(smem + fused_region_bytes<BS>(ac.M));
+  const int count = select_block<BS>(sc, h, i, smem, list_lds);
+  __syncthreads();  // the list is complete; the selection scratch is free for the tiles
+  attend_block<BS>(
+      ac, h, i, min(max(count, 0), i + 1),
+      [&](int n) __attribute__((always_inline)) { return __builtin_amdgcn_readfirstlane(list_lds[n]); }, smem,
+      smem + BS * 256);
+}
+
+size_t fused_smem_bytes(int block_size, int n_blocks) {
+  switch (block_size) {
+    case 64: return fused_region_bytes<64>(n_blocks) + (size_t)n_blocks * 4;
+    case 128: return fused_region_bytes<128>(n_blocks) + (size_t)n_blocks * 4;
+    case 256: return fused_region_bytes<256>(n_blocks) + (size_t)n_blocks * 4;
+    default: return 0;
+  }
+}
+
+hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStream_t s) {
+  const dim3 grid(sa.n_blocks * sa.n_q_heads);
+  const SelectCore sc = make_select_core(sa);
+  const AttnCore ac = make_attn_core(aa);
+  const size_t smem = fused_smem_bytes(sa.block_size, sa.n_blocks);
+#define RBS_FUSED_CASE(BSZ)                                                                                   \
+  case BSZ: {                                                                                                 \
+    hipError_t e = hipFuncSetAttribute((const void*)select_attend_kernel<BSZ>,                                \
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);                \
+    if (e != hipSuccess) return e;                                                                            \
+    hipLaunchKernelGGL(select_attend_kernel<BSZ>, grid, dim3(BSZ * 2), smem, s, sc, ac);                      \
+    break;                                                                                                    \
+  }
+  switch (sa.block_size) {
+    RBS_FUSED_CASE(64)
+    RBS_FUSED_CASE(128)
+    RBS_FUSED_CASE(256)
+    default: return hipErrorInvalidValue;
+  }
+#undef RBS_FUSED_CASE
+  return hipGetLastError();
+}
+
+}  // namespace rbs

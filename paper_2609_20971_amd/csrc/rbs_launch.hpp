@@ -56,6 +56,8 @@ inline size_t summary_bytes(int n_kv_heads, int n_blocks) {
 hipError_t launch_stats(const StatsArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStream_t s);
+size_t fused_smem_bytes(int block_size, int n_blocks);
 hipError_t launch_dense_indices(int n_q_heads, int n_blocks, int64_t capacity, int32_t* counts,
                                 int32_t* indices, hipStream_t s);
 

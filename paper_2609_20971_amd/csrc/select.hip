@@ -1,263 +1,30 @@
 // Stage 2: dual-branch block selection (Sec. 3.2; Algorithm 1, selection loop).
-//
-// One workgroup per (query head h, query block i), B/32 waves; wave w owns the
-// 32 query tokens 32w..32w+31 of the block.  Q_i is read from HBM once and
-// held in registers as f16 (bf16 -> f16 is exact in the normal range).
-// Candidate key blocks 0..i are scored in tiles of 32 centroids staged through
-// LDS (double buffered, one barrier per tile):
-//
-//   S = Q_i C'^T on the f16 MFMA (32x32x16), where C' = c_b log2(e)/sqrt(d)
-//   is the select-ready centroid written by the statistics stage, so S holds
-//   base logits / sqrt(d) in log2 units.  Rescue logits add |q_t| u_b with the
-//   per-block uplift u_b = r_b beta_b log2(e)/sqrt(d) (Eq. rescue_score).
-//
-// Each wave reduces its 32 tokens per centroid to a (shift, sum of exp2) pair
-// per branch; the pairs of the waves are merged into the block score
-// L_b = log2 S_b (the local log-sum-exp form allowed by Eq. block_aggregation).
-// After the last tile: row maxima, relative thresholds in log2 space
-// (L_b >= max L + log2 tau, Eq. branch_thresholds), union with the forced
-// blocks, and in-kernel compaction of the mask to an ascending index list
-// with wave ballots and a cross-wave prefix.
-#include "rbs_device.hpp"
+// One workgroup per (query head, query block); the work of a block is
+// select_block (select_block.hpp).
 #include "rbs_launch.hpp"
+#include "select_block.hpp"
 
 namespace rbs {
 
-constexpr int kTile = 32;  // centroids per tile
-
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
-
 template <int BS>
-__global__ __launch_bounds__(BS * 2) void select_kernel(
-    const uint16_t* __restrict__ Q, int N, int M, int Hq, int group, const _Float16* __restrict__ cent16,
-    const float* __restrict__ uplift, float log2_tau_base, float log2_tau_rescue, int base_all,
-    int rescue_all, int n_sink, int n_local, int n_recent, int32_t* __restrict__ counts,
-    int32_t* __restrict__ indices, int64_t capacity) {
-  constexpr int NW = BS / 32;
-  constexpr int NT = NW * kWave;
+__global__ __launch_bounds__(BS * 2) void select_kernel(SelectCore c, int Hq) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  // Layout: cbuf[2][32 rows][16 chunks of 8 f16] | stage[2][NW][32][4] | nq[BS] | L_base[M] | L_res[M]
-  uint4* cbuf = reinterpret_cast<uint4*>(smem_raw);
-  float4* stage = reinterpret_cast<float4*>(smem_raw + 2 * kTile * 256);
-  float* nq_s = reinterpret_cast<float*>(smem_raw + 2 * kTile * 256 + 2 * NW * kTile * 16);
-  float* L_base = nq_s + BS;
-  float* L_res = L_base + M;
-  __shared__ float red_f[2 * NW];
-  __shared__ int red_i[NW];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int half = lane >> 5, l32 = lane & 31;
   const int work = blockIdx.x;
-  const int i = M - 1 - work / Hq;  // late (long) rows first
+  const int i = c.M - 1 - work / Hq;  // late (long) rows first
   const int h = work % Hq;
-  const int g = h / group;
-  const int row0 = i * BS;
-  const int nb = min(BS, N - row0);
-  const int n_cand = i + 1;
-  const int n_tiles = (n_cand + kTile - 1) / kTile;
-  const _Float16* cg = cent16 + (size_t)g * M * kHeadDim;
-  const float* ug = uplift + (size_t)g * M;
-
-  // ---- Q rows of this wave as MFMA A operands (row = 32*wave + l32).
-  const int t_local = 32 * wave + l32;
-  const bool row_ok = t_local < nb;
-  f16x8 qa[8];
-  float sq = 0.f;
-  {
-    const uint16_t* qrow = Q + ((size_t)h * N + row0 + t_local) * kHeadDim + 8 * half;
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-      uint4 v = row_ok ? *reinterpret_cast<const uint4*>(qrow + 16 * ks) : make_uint4(0u, 0u, 0u, 0u);
-      float f[8];
-      unpack8(v, f);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        qa[ks][e] = (_Float16)f[e];
-        sq = fmaf(f[e], f[e], sq);
-      }
-    }
-  }
-  sq += wave_xor_f(sq, 32);
-  const float nq = sqrtf(sq);
-  if (half == 0) nq_s[t_local] = nq;
-  float nq_max = row_ok ? nq : 0.f;
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) nq_max = fmaxf(nq_max, wave_xor_f(nq_max, m));
-  const bool wave_active = 32 * wave < nb;
-  const bool wave_partial = 32 * wave + 32 > nb;
-
-  // ---- Stage centroid tile 0.
-  const int ld_row = tid >> 4, ld_chunk = tid & 15;  // NT >= 128 threads: rows ld_row, ld_row + NT/16, ...
-  constexpr int kLdRowsPerPass = NT / 16;
-  constexpr int kLdPasses = (kTile + kLdRowsPerPass - 1) / kLdRowsPerPass;
-  uint4 pre[kLdPasses];
-  auto fetch = [&](int tile) {
-#pragma unroll
-    for (int p = 0; p < kLdPasses; ++p) {
-      const int r = ld_row + p * kLdRowsPerPass;
-      const int bb = tile * kTile + r;
-      pre[p] = (r < kTile && bb < M) ? *reinterpret_cast<const uint4*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk)
-                                     : make_uint4(0u, 0u, 0u, 0u);
-    }
-  };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int p = 0; p < kLdPasses; ++p) {
-      const int r = ld_row + p * kLdRowsPerPass;
-      if (r < kTile) cbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = pre[p];
-    }
-  };
-  fetch(0);
-  store(0);
-  __syncthreads();
-
-  // Per-element token norms minus the wave maximum (rescue exponent offsets).
-  float nqd[16];
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int t = 32 * wave + mfma_row(r, lane);
-    nqd[r] = (t < nb) ? nq_s[t] - nq_max : 0.f;
-  }
-
-  for (int tile = 0; tile < n_tiles; ++tile) {
-    const int buf = tile & 1;
-    if (tile + 1 < n_tiles) fetch(tile + 1);
-    const int b = tile * kTile + l32;
-    if (wave_active) {
-      f32x16 acc = {};
-      const uint4* cb = cbuf + buf * kTile * 16 + l32 * 16;
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const uint4 raw = cb[swz(l32, 2 * ks + half)];
-        f16x8 bfrag;
-        __builtin_memcpy(&bfrag, &raw, 16);
-        acc = mfma_f16(qa[ks], bfrag, acc);
-      }
-      if (wave_partial) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (32 * wave + mfma_row(r, lane) >= nb) acc[r] = -INFINITY;
-      }
-      float mx = acc[0];
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, acc[r]);
-      mx = fmaxf(mx, wave_xor_f(mx, 32));
-      float sb = 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
-      const float u = (b < M) ? ug[b] : 0.f;
-      float mr = mx, sr = sb;
-      if (__any(u != 0.f)) {
-        mr = mx + nq_max * u;
-        sr = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sr += fast_exp2(fmaf(nqd[r], u, acc[r] - mx));
-      }
-      sb += wave_xor_f(sb, 32);
-      sr += wave_xor_f(sr, 32);
-      if (half == 0) stage[(buf * NW + wave) * kTile + l32] = make_float4(mx, sb, mr, sr);
-    } else if (half == 0) {
-      stage[(buf * NW + wave) * kTile + l32] = make_float4(-INFINITY, 0.f, -INFINITY, 0.f);
-    }
-    if (tile + 1 < n_tiles) store(buf ^ 1);
-    __syncthreads();
-    // Merge the waves' partial sums of this tile (wave 0: lanes 0-31 base, 32-63 rescue).
-    if (wave == 0 && b < n_cand) {
-      float top = -INFINITY;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        const float4 p = stage[(buf * NW + w) * kTile + l32];
-        top = fmaxf(top, half ? p.z : p.x);
-      }
-      float sum = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        const float4 p = stage[(buf * NW + w) * kTile + l32];
-        const float m = half ? p.z : p.x, sv = half ? p.w : p.y;
-        if (sv > 0.f) sum += sv * fast_exp2(m - top);
-      }
-      (half ? L_res : L_base)[b] = top + log2f(sum);
-    }
-  }
-  __syncthreads();
-
-  // ---- Row maxima of both branches.
-  float mb = -INFINITY, mres = -INFINITY;
-  for (int b = tid; b < n_cand; b += NT) {
-    mb = fmaxf(mb, L_base[b]);
-    mres = fmaxf(mres, L_res[b]);
-  }
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) {
-    mb = fmaxf(mb, wave_xor_f(mb, m));
-    mres = fmaxf(mres, wave_xor_f(mres, m));
-  }
-  if (lane == 0) {
-    red_f[wave] = mb;
-    red_f[NW + wave] = mres;
-  }
-  __syncthreads();
-  mb = red_f[0];
-  mres = red_f[NW];
-#pragma unroll
-  for (int w = 1; w < NW; ++w) {
-    mb = fmaxf(mb, red_f[w]);
-    mres = fmaxf(mres, red_f[NW + w]);
-  }
-  const float thr_base = mb + log2_tau_base;
-  const float thr_res = mres + log2_tau_rescue;
-  const bool recent_row = i >= M - n_recent;
-
-  // ---- Union with forced blocks and compaction to an ascending list.
-  int32_t* out = indices + (int64_t)h * capacity + (int64_t)i * (i + 1) / 2;
-  int total = 0;
-  for (int base = 0; base < n_cand; base += NT) {
-    const int b = base + tid;
-    bool sel = false;
-    if (b < n_cand) {
-      sel = recent_row || b < n_sink || b > i - n_local || base_all || rescue_all ||
-            L_base[b] >= thr_base || L_res[b] >= thr_res;
-    }
-    const uint64_t ballot = __ballot(sel);
-    const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(ballot >> 32),
-                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)ballot, 0u));
-    if (lane == 0) red_i[wave] = __popcll(ballot);
-    __syncthreads();
-    int off = total, pass_total = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const int c = red_i[w];
-      if (w < wave) off += c;
-      pass_total += c;
-    }
-    if (sel) out[off + before] = b;
-    total += pass_total;
-    __syncthreads();
-  }
-  if (tid == 0) counts[(size_t)h * M + i] = total;
-}
-
-template <int BS>
-static size_t select_smem(int M) {
-  constexpr int NW = BS / 32;
-  return 2 * kTile * 256 + 2 * NW * kTile * 16 + BS * 4 + 2 * (size_t)M * 4;
+  select_block<BS>(c, h, i, smem_raw, nullptr);
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
   const dim3 grid(a.n_blocks * a.n_q_heads);
-  const int group = a.n_q_heads / a.n_kv_heads;
-  const float l2b = a.tau_base > 0.f ? log2f(a.tau_base) : -INFINITY;
-  const float l2r = a.tau_rescue > 0.f ? log2f(a.tau_rescue) : -INFINITY;
-  const int base_all = a.tau_base <= 0.f, res_all = a.tau_rescue <= 0.f;
+  const SelectCore c = make_select_core(a);
 #define RBS_SELECT_CASE(BSZ)                                                                                  \
   case BSZ: {                                                                                                 \
-    const size_t smem = select_smem<BSZ>(a.n_blocks);                                                         \
+    const size_t smem = select_smem_bytes<BSZ>(a.n_blocks);                                                   \
     hipError_t e = hipFuncSetAttribute((const void*)select_kernel<BSZ>,                                       \
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);                \
     if (e != hipSuccess) return e;                                                                            \
-    hipLaunchKernelGGL(select_kernel<BSZ>, grid, dim3(BSZ * 2), smem, s, a.Q, a.n_tokens, a.n_blocks,         \
-                       a.n_q_heads, group, a.cent16, a.uplift, l2b, l2r, base_all, res_all, a.n_sink,         \
-                       a.n_local, a.n_recent, a.counts, a.indices, a.capacity);                               \
+    hipLaunchKernelGGL(select_kernel<BSZ>, grid, dim3(BSZ * 2), smem, s, c, a.n_q_heads);                     \
     break;                                                                                                    \
   }
   switch (a.block_size) {

@@ -28,7 +28,7 @@ def _declared():
 
 def test_header_declares_the_three_stage_calls():
     names = _declared()
-    for fn in ("rbs_block_stats", "rbs_select", "rbs_sparse_prefill"):
+    for fn in ("rbs_block_stats", "rbs_select", "rbs_sparse_prefill", "rbs_select_attend"):
         assert fn in names
 
 
@@ -78,6 +78,13 @@ def test_shape_validation(field, value, code):
     assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, FAKE, FAKE, None) == code
     assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None) == code
     assert lib.rbs_dense_indices(ctypes.byref(s), FAKE, FAKE, None) == code
+    assert _fused(lib, s, st) == code
+
+
+def _fused(lib, s, st, Q=FAKE, K=FAKE, V=FAKE, tb=0.9, tr=0.9, sink=1, local=1, recent=0, scale=0.0, counts=FAKE,
+           indices=FAKE, O=FAKE, lse=None):
+    return lib.rbs_select_attend(ctypes.byref(s), Q, K, V, ctypes.byref(st) if st is not None else None, tb, tr,
+                                 sink, local, recent, scale, counts, indices, O, lse, None)
 
 
 def test_largest_shape_passes_shape_validation():
@@ -106,6 +113,13 @@ def test_null_and_alignment_errors():
     assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, MIS, None, None) == 5
     assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, MIS, None) == 5
     assert lib.rbs_dense_indices(ctypes.byref(s), FAKE, None, None) == 1
+    for arg in ("Q", "K", "V", "counts", "indices", "O"):
+        assert _fused(lib, s, st, **{arg: None}) == 1
+        assert _fused(lib, s, st, **{arg: MIS}) == 5
+    assert _fused(lib, s, None) == 1
+    assert _fused(lib, s, _stats(rbs, summary=None)) == 1
+    assert _fused(lib, s, _stats(rbs, summary=MIS)) == 5
+    assert _fused(lib, s, st, lse=MIS) == 5
 
 
 @pytest.mark.parametrize("tb,tr,sink,local,recent", [
@@ -117,6 +131,7 @@ def test_select_argument_errors(tb, tr, sink, local, recent):
     s = rbs.make_shape(1024, 4, 2, 64)
     st = _stats(rbs)
     assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), tb, tr, sink, local, recent, FAKE, FAKE, None) == 4
+    assert _fused(lib, s, st, tb=tb, tr=tr, sink=sink, local=local, recent=recent) == 4
 
 
 def test_bad_softmax_scale():
@@ -124,6 +139,7 @@ def test_bad_softmax_scale():
     s = rbs.make_shape(1024, 4, 2, 64)
     for bad in (float("nan"), float("inf")):
         assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, bad, FAKE, None, None) == 4
+        assert _fused(lib, s, _stats(rbs), scale=bad) == 4
 
 
 def test_binding_raises_without_library(monkeypatch, tmp_path):

@@ -205,3 +205,50 @@ def test_qwen3_32b_64k_sampled():
     rows = H.sample_rows(w.n_q_heads, M, 24, seed=4, include=[(0, M - 1), (63, 300), (40, 2)])
     attn = H.sample_rows(w.n_q_heads, M, 5, seed=6, include=[(0, M - 1), (63, 300), (40, 2)])
     _full_check(w, select_rows=rows, attn_rows=attn)
+
+
+def _fused_matches_two_calls(w: Workload, tau=None, forced=None):
+    """The fused entry point against rbs_select + rbs_sparse_prefill on the same
+    inputs: lists, O and LSE bit for bit."""
+    import torch
+    import paper_2609_20971_amd as rbs
+    r = _run(w, tau=tau, forced=forced)
+    tb, tr = r["tau"]
+    sink, local, recent = r["forced"]
+    lse = torch.empty_like(r["lse"])
+    counts, indices, O = rbs.rbs_select_attend(r["shape"], r["Qd"], r["Kd"], r["Vd"], r["stats"], tb, tr, sink,
+                                               local, recent, 0.0, lse=lse)
+    torch.cuda.synchronize()
+    M = w.n_blocks
+    assert torch.equal(counts, r["counts"])
+    rows = [(h, i) for h in range(w.n_q_heads) for i in range(M)]
+    assert H.gpu_rows(counts, indices, rows) == H.gpu_rows(r["counts"], r["indices"], rows)
+    assert torch.equal(O.view(torch.int16), r["O"].view(torch.int16))
+    assert torch.equal(lse, r["lse"])
+    _say(f"[parity] fused {w.name} N={w.seq_len} B={w.block_size}: lists, O and LSE identical to the two calls")
+    return r
+
+
+@pytest.mark.parametrize("variant", [
+    dict(),
+    dict(seq_len=1000, block_size=64, n_q_heads=4, n_kv_heads=2, seed=1),
+    dict(seq_len=777, block_size=128, n_q_heads=2, n_kv_heads=2, seed=2),
+    dict(seq_len=1300, block_size=256, n_q_heads=4, n_kv_heads=1, seed=3),
+    dict(seq_len=5, block_size=128, n_q_heads=1, n_kv_heads=1, seed=5),
+    dict(seq_len=8191, block_size=128, n_q_heads=8, n_kv_heads=2, seed=13),
+])
+def test_fused_select_attend_matches_two_calls(variant):
+    w = WORKLOADS["tiny-2k"].with_(name="fused", **variant)
+    _fused_matches_two_calls(w)
+
+
+def test_fused_select_attend_forced_and_dense_rows():
+    w = WORKLOADS["tiny-2k"].with_(seq_len=1536, seed=7)
+    _fused_matches_two_calls(w, tau=(0.0, 0.0), forced=(1, 2, 0))
+    _fused_matches_two_calls(w, tau=(0.9, 0.95), forced=(0, 1, 2))
+
+
+@pytest.mark.slow
+def test_fused_select_attend_128k_matches_two_calls():
+    """The headline layer through the fused entry point: identical to the two calls."""
+    _fused_matches_two_calls(WORKLOADS["qwen3-30b-a3b-128k"])
