@@ -242,7 +242,7 @@ def main():
     select_gbps = alg["select_bytes"] / (stage_ms[1] * 1e-3) / 1e9
     select_tflops = alg["select_flops"] / (stage_ms[1] * 1e-3) / 1e12
 
-    traffic = _profiled_traffic("attn_kernel", w.name, "attn.hip")
+    traffic = _profiled_traffic("attn_kernel", w.name)
 
     result = {
         "metric": METRIC,
@@ -313,11 +313,30 @@ def _time_dense(rbs, torch, np, shape, Q, K, V, stream, reps: int) -> float:
     return float(np.median(times))
 
 
-def _profiled_traffic(kernel: str, workload: str, source: str):
-    """HBM bytes per launch from the committed rocprofv3 summary of this kernel
-    on this workload, or None when there is none or the kernel source changed
-    since the counters were taken."""
+# Sources each kernel is built from (their joint hash identifies the kernel in
+# the committed rocprofv3 summaries).
+KERNEL_SOURCES = {
+    "stats_kernel": ["stats.hip", "rbs_device.hpp"],
+    "quantile_kernel": ["stats.hip", "rbs_device.hpp"],
+    "select_kernel": ["select.hip", "select_block.hpp", "rbs_device.hpp"],
+    "attn_kernel": ["attn.hip", "attend_block.hpp", "rbs_device.hpp"],
+    "select_attend_kernel": ["fused.hip", "select_block.hpp", "attend_block.hpp", "rbs_device.hpp"],
+}
+
+
+def source_sha(kernel: str) -> str:
     import hashlib
+    h = hashlib.sha256()
+    for src in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2609_20971_amd", "csrc", src), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def _profiled_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 summary of this kernel
+    on this workload, or None when there is none or the kernel sources changed
+    since the counters were taken."""
     path = os.path.join(PROFILES, f"{kernel}_{workload}.md")
     if not os.path.exists(path):
         return None
@@ -327,9 +346,7 @@ def _profiled_traffic(kernel: str, workload: str, source: str):
             if ": " in line and not line.startswith(" "):
                 k, v = line.split(": ", 1)
                 fields[k.strip()] = v.strip()
-    with open(os.path.join(ROOT, "paper_2609_20971_amd", "csrc", source), "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()[:16]
-    if fields.get("source_sha") != sha or "traffic_bytes_per_launch" not in fields:
+    if fields.get("source_sha") != source_sha(kernel) or "traffic_bytes_per_launch" not in fields:
         return None
     return int(float(fields["traffic_bytes_per_launch"]))
 
