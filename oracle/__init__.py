@@ -19,6 +19,13 @@ Parity status per function (what pins it, in tests/test_oracle_pins.py):
   attention_on_mask    pinned: brute-force Eq. (1) at full selection, softmax
                        shift invariance, linearity in V
   density              pinned: hand-counted masks
+  block_box /
+  variant_log_scores   pinned: App. geometry worked examples (box 2 vs L2 sqrt 2;
+                       box eps vs L2 1), box and full-L2 bounds dominate every
+                       token logit, single-key blocks reduce to q . k, rotation
+                       invariance of centroid / full-L2 and its failure for the box
+  select_variant       pinned: budget fractions 1 and ~0, monotone budgets, forced
+                       blocks, relative thresholds 0 and 1
 """
 
 from .rbs import (
@@ -32,6 +39,13 @@ from .rbs import (
     branch_log_scores,
     select_row,
     select,
+    SELECTOR_VARIANTS,
+    block_box,
+    variant_logits,
+    variant_log_scores,
+    top_fraction,
+    select_variant_row,
+    select_variant,
     attention_rows,
     attention_on_mask,
     dense_causal_attention,

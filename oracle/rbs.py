@@ -198,6 +198,119 @@ def select(Q, C, R, beta, block_size: int, tau_base: float, tau_rescue: float,
     return out
 
 
+# ------------------------------------- supporting selectors (Table selector_ablation)
+#
+# The paper compares the dual-branch selector with three alternatives in the
+# same prefill backend (Sec. 4, supporting selector comparison; App.
+# geometry): centroid-only scoring, the unattenuated full-L2 bound, and a
+# Quest-style coordinate-wise box.  READINGS: each alternative is a single
+# branch whose token-level logits are aggregated over the query block exactly
+# as in Eq. block_aggregation; centroid-only and full-L2 keep the relative
+# threshold of Eq. branch_thresholds, the Quest-style policy keeps a fixed
+# budget (the k = max(1, ceil(rho |C_i|)) highest scores, ties with the k-th
+# kept); forced blocks are added to every variant.
+
+SELECTOR_VARIANTS = ("centroid", "full_l2", "box")
+
+
+def block_box(K: np.ndarray, block_size: int):
+    """Coordinate-wise key minima a_b and maxima u_b of every block (App.
+    geometry, Eq. quest_box), returned as the box centre v_b = (u_b + a_b)/2
+    and half-width h_b = (u_b - a_b)/2, each [H_kv][M][d]."""
+    K = np.asarray(K, dtype=np.float64)
+    H, N, d = K.shape
+    ranges = block_ranges(N, block_size)
+    Vc = np.zeros((H, len(ranges), d))
+    Hw = np.zeros((H, len(ranges), d))
+    for g in range(H):
+        for b, (s, e) in enumerate(ranges):
+            lo = K[g, s:e].min(axis=0)
+            hi = K[g, s:e].max(axis=0)
+            Vc[g, b] = (hi + lo) / 2.0
+            Hw[g, b] = (hi - lo) / 2.0
+    return Vc, Hw
+
+
+def variant_logits(Qi: np.ndarray, C: np.ndarray, R: np.ndarray, Vc: np.ndarray, Hw: np.ndarray,
+                   n_candidates: int, variant: str) -> np.ndarray:
+    """Token-level logits [n_i][n_candidates] (unscaled) of one supporting selector:
+        centroid  q . c_b                                  (Eq. base_score)
+        full_l2   q . c_b + |q|_2 r_b                      (Eq. full_l2_bound)
+        box       sum_j max(q_j a_bj, q_j u_bj)            (Eq. quest_box)
+    One KV head's statistics; Vc, Hw (box centre and half-width) are used by
+    the box only and may be None otherwise."""
+    Qi = np.asarray(Qi, dtype=np.float64)
+    n = n_candidates
+    if variant == "centroid":
+        return Qi @ C[:n].T
+    if variant == "full_l2":
+        qnorm = np.sqrt((Qi * Qi).sum(axis=1))
+        return Qi @ C[:n].T + qnorm[:, None] * R[:n][None, :]
+    if variant == "box":
+        lo = Vc[:n] - Hw[:n]
+        hi = Vc[:n] + Hw[:n]
+        return np.maximum(Qi[:, None, :] * lo[None, :, :], Qi[:, None, :] * hi[None, :, :]).sum(axis=2)
+    raise ValueError(variant)
+
+
+def variant_log_scores(Qi, C, R, Vc, Hw, n_candidates: int, variant: str) -> np.ndarray:
+    """log S_b of a supporting selector: the logits of variant_logits scaled by
+    1/sqrt(d) and aggregated over the block's tokens with the shared shift of
+    Eq. block_aggregation (log 0 = -inf)."""
+    d = np.asarray(Qi).shape[1]
+    x = variant_logits(Qi, C, R, Vc, Hw, n_candidates, variant) / math.sqrt(d)
+    m = x.max()
+    S = np.exp(x - m).sum(axis=0)
+    with np.errstate(divide="ignore"):
+        return np.log(S)
+
+
+def top_fraction(log_s: np.ndarray, rho: float):
+    """Fixed-budget selection: the k = max(1, ceil(rho n)) largest scores, ties
+    with the k-th kept.  Returns (mask, margin) with margin = log S_b minus the
+    k-th largest log S (the mask is margin >= 0)."""
+    n = log_s.shape[0]
+    k = min(n, max(1, int(math.ceil(rho * n - 1e-12))))
+    kth = np.sort(log_s)[::-1][k - 1]
+    with np.errstate(invalid="ignore"):
+        margin = log_s - kth
+    margin = np.where(np.isnan(margin), -np.inf, margin)
+    return margin >= 0.0, margin
+
+
+def select_variant_row(Qi, C, R, Vc, Hw, i: int, n_blocks: int, variant: str, param: float,
+                       n_sink: int, n_local: int, n_recent: int) -> dict:
+    """Mask of query block i under a supporting selector: its single branch
+    (relative threshold param for centroid / full_l2, budget fraction param for
+    box) united with the forced blocks."""
+    log_s = variant_log_scores(Qi, C, R, Vc, Hw, i + 1, variant)
+    if variant == "box":
+        mask, margin = top_fraction(log_s, param)
+    else:
+        mask, margin = _threshold(log_s, param)
+    forced = forced_blocks(i, n_blocks, n_sink, n_local, n_recent)
+    return {"branch": mask, "forced": forced, "final": mask | forced, "log_s": log_s, "margin": margin}
+
+
+def select_variant(Q, C, R, Vc, Hw, block_size: int, variant: str, param: float,
+                   n_sink: int, n_local: int, n_recent: int, rows=None) -> dict:
+    """select_variant_row for every (query head, query block) in `rows`."""
+    H_q, n_tokens = Q.shape[0], Q.shape[1]
+    group = H_q // C.shape[0]
+    ranges = block_ranges(n_tokens, block_size)
+    M = len(ranges)
+    if rows is None:
+        rows = [(h, i) for h in range(H_q) for i in range(M)]
+    out = {}
+    for (h, i) in rows:
+        g = h // group
+        s, e = ranges[i]
+        out[(h, i)] = select_variant_row(np.asarray(Q[h, s:e], dtype=np.float64), C[g], R[g],
+                                         None if Vc is None else Vc[g], None if Hw is None else Hw[g],
+                                         i, M, variant, param, n_sink, n_local, n_recent)
+    return out
+
+
 # ---------------------------------------------------------------- Sec. 3.3
 
 def attention_rows(Qh, Kg, Vg, block_size: int, i: int, kv_blocks, scale: float | None = None):

@@ -369,3 +369,105 @@ def test_list_mask_roundtrip():
     back = oracle.masks_from_lists(counts, idx, rows.keys())
     for k in rows:
         assert (back[k] == rows[k]).all()
+
+
+# ------------------------------------------------ supporting selectors (Table selector_ablation)
+
+def _variant_scores(K_block, q, variant):
+    """Unscaled logit of one query against one block, through the oracle."""
+    K = np.asarray(K_block, dtype=np.float64)[None]
+    C, R = oracle.block_stats(K, K.shape[1])
+    Vc, Hw = oracle.block_box(K, K.shape[1])
+    return oracle.variant_logits(np.asarray(q, dtype=np.float64)[None], C[0], R[0], Vc[0], Hw[0], 1, variant)[0, 0]
+
+
+def test_variant_logits_on_the_appendix_examples():
+    """App. geometry: K = {e1, -e1, e2, -e2}, q = (1, 1): full-L2 sqrt 2, box 2;
+    K = {e1, -e1, eps e2, -eps e2}, q = e2: full-L2 1, box eps; centroid 0 in both."""
+    e1, e2 = np.eye(2)
+    K = np.stack([e1, -e1, e2, -e2])
+    q = np.array([1.0, 1.0])
+    assert _variant_scores(K, q, "full_l2") == pytest.approx(math.sqrt(2), rel=1e-15)
+    assert _variant_scores(K, q, "box") == pytest.approx(2.0, rel=1e-15)
+    assert _variant_scores(K, q, "centroid") == pytest.approx(0.0, abs=1e-15)
+    eps = 0.25
+    K = np.stack([e1, -e1, eps * e2, -eps * e2])
+    assert _variant_scores(K, e2, "full_l2") == pytest.approx(1.0, rel=1e-15)
+    assert _variant_scores(K, e2, "box") == pytest.approx(eps, rel=1e-15)
+
+
+def test_box_and_full_l2_dominate_every_token_logit():
+    """Both are upper bounds of max_k q.k over the block (App. geometry); the box
+    is attained when the block holds its own extreme corner."""
+    rng = np.random.default_rng(21)
+    for _ in range(50):
+        K = rng.standard_normal((7, 5)) * rng.uniform(0.1, 3.0)
+        q = rng.standard_normal(5)
+        top = (K @ q).max()
+        assert _variant_scores(K, q, "box") >= top - 1e-12
+        assert _variant_scores(K, q, "full_l2") >= top - 1e-12
+        assert _variant_scores(K, q, "centroid") <= top + 1e-12
+    lo, hi = np.array([-1.0, 0.5, -2.0]), np.array([2.0, 1.5, -1.0])
+    q = np.array([1.0, -1.0, 2.0])
+    corner = np.where(q >= 0, hi, lo)
+    K = np.stack([lo, hi, corner])
+    assert _variant_scores(K, q, "box") == pytest.approx(q @ corner, rel=1e-15)
+
+
+def test_single_key_blocks_reduce_every_variant_to_the_token_logit():
+    rng = np.random.default_rng(22)
+    k, q = rng.standard_normal(6), rng.standard_normal(6)
+    for v in oracle.SELECTOR_VARIANTS:
+        assert _variant_scores(k[None], q, v) == pytest.approx(q @ k, rel=1e-12)
+
+
+def test_rotation_keeps_centroid_and_l2_scores_but_not_the_box():
+    """App. geometry: centroid dot product and radius are invariant under a common
+    orthogonal transform; the coordinate-wise box is not."""
+    e1, e2 = np.eye(2)
+    K = np.stack([e1, -e1, e2, -e2])
+    q = np.array([1.0, 1.0])
+    c, s = math.cos(math.pi / 4), math.sin(math.pi / 4)
+    Rot = np.array([[c, -s], [s, c]])
+    for v in ("centroid", "full_l2"):
+        assert _variant_scores(K @ Rot.T, Rot @ q, v) == pytest.approx(_variant_scores(K, q, v), abs=1e-12)
+    assert _variant_scores(K @ Rot.T, Rot @ q, "box") != pytest.approx(_variant_scores(K, q, "box"), abs=1e-3)
+
+
+def test_budget_selection_fractions():
+    """Fixed budget: rho = 1 keeps all, a tiny rho keeps the argmax (ties too),
+    and a larger budget never drops a block."""
+    log_s = np.log(np.array([0.2, 0.9, 0.1, 0.9, 0.5, 0.05]))
+    assert oracle.top_fraction(log_s, 1.0)[0].all()
+    m, _ = oracle.top_fraction(log_s, 1e-6)
+    assert m.tolist() == [False, True, False, True, False, False]
+    prev = np.zeros(6, bool)
+    for rho in (0.1, 0.3, 0.5, 0.7, 0.9, 1.0):
+        m, margin = oracle.top_fraction(log_s, rho)
+        assert m.sum() >= math.ceil(rho * 6)
+        assert (m | ~prev).all() and (m == (margin >= 0)).all()
+        prev = m
+
+
+def test_variant_rows_keep_forced_blocks_and_threshold_extremes():
+    rng = np.random.default_rng(23)
+    d, B, N = 8, 4, 40
+    Q = rng.standard_normal((1, N, d))
+    K = rng.standard_normal((1, N, d))
+    C, R = oracle.block_stats(K, B)
+    Vc, Hw = oracle.block_box(K, B)
+    M = N // B
+    for v, param in (("centroid", 0.5), ("full_l2", 0.5), ("box", 0.2)):
+        rows = oracle.select_variant(Q, C, R, Vc, Hw, B, v, param, 1, 2, 0)
+        for (h, i), r in rows.items():
+            assert (r["final"][r["forced"]]).all() and r["final"][0] and r["final"][i]
+            assert (r["final"] == (r["branch"] | r["forced"])).all()
+    for v in ("centroid", "full_l2"):
+        all_rows = oracle.select_variant(Q, C, R, Vc, Hw, B, v, 0.0, 0, 1, 0)
+        assert all(r["final"].all() for r in all_rows.values())
+        top_rows = oracle.select_variant(Q, C, R, Vc, Hw, B, v, 1.0, 0, 1, 0)
+        for r in top_rows.values():
+            assert r["branch"].sum() == 1 and r["branch"][np.argmax(r["log_s"])]
+    box_all = oracle.select_variant(Q, C, R, Vc, Hw, B, "box", 1.0, 0, 1, 0)
+    assert all(r["final"].all() for r in box_all.values())
+    assert len(box_all) == M
