@@ -11,6 +11,9 @@
  *                       blocks                                (Sec. 3.3)
  *   rbs_select_attend   both in one pass (Algorithm 1 from the selection loop
  *                       on), same results as the two calls in sequence
+ *   rbs_block_box,      the supporting selectors of the paper's selector
+ *   rbs_select_variant  comparison (centroid-only, full-L2 bound, Quest-style
+ *                       box; Table selector_ablation, App. geometry)
  *
  * Conventions shared by every call
  *   - Tensors are dense, row-major, in device memory:
@@ -145,6 +148,52 @@ int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, cons
                       const rbs_stats* stats, float tau_base, float tau_rescue, int32_t n_sink,
                       int32_t n_local, int32_t n_recent, float softmax_scale, int32_t* counts,
                       int32_t* indices, void* O, float* lse, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Supporting selectors (the paper's selector comparison, Table
+ * selector_ablation; bounds of App. geometry).  Each is a single branch whose
+ * token logits are aggregated over the query block as in Eq.
+ * block_aggregation, then united with the forced blocks, written in the list
+ * layout of rbs_select:
+ *   RBS_SELECTOR_CENTROID  logits q . c_b (Eq. base_score); keeps blocks with
+ *                          S_b >= param * max S (relative threshold, param in [0, 1])
+ *   RBS_SELECTOR_FULL_L2   logits q . c_b + |q|_2 r_b (Eq. full_l2_bound, the
+ *                          rescue score with beta = 1); relative threshold param
+ *   RBS_SELECTOR_BOX       logits sum_j max(q_j a_bj, q_j u_bj) (Eq. quest_box,
+ *                          a/u the block's coordinate-wise key minima/maxima);
+ *                          keeps the k = max(1, ceil(param * (i + 1))) highest
+ *                          scores of row i, ties with the k-th included
+ *                          (fixed budget, param in (0, 1])
+ */
+enum { RBS_SELECTOR_CENTROID = 1, RBS_SELECTOR_FULL_L2 = 2, RBS_SELECTOR_BOX = 3 };
+
+/*
+ * Box statistics for RBS_SELECTOR_BOX (device memory):
+ *   center   fp32 [H_kv][M][d]   (u_b + a_b) / 2
+ *   half     fp32 [H_kv][M][d]   (u_b - a_b) / 2
+ *   summary  rbs_box_summary_bytes() bytes: f16 copies for the selector
+ */
+typedef struct {
+  float* center;
+  float* half;
+  void* summary;
+} rbs_box;
+
+/* Bytes needed for rbs_box.summary (0 if the shape is invalid). */
+size_t rbs_box_summary_bytes(const rbs_shape* shape);
+
+/* Per-block coordinate-wise key minima and maxima (App. geometry, Eq. quest_box),
+ * written as box centre and half-width.  K as in rbs_block_stats. */
+int rbs_block_box(const rbs_shape* shape, const void* K, const rbs_box* box, void* stream);
+
+/* A supporting selector (see above).  stats: from rbs_block_stats (the centroid
+ * and full-L2 selectors read its summary and radii); box: from rbs_block_box,
+ * required for RBS_SELECTOR_BOX and ignored otherwise.  Forced blocks, outputs
+ * and errors as in rbs_select; an unknown selector or a param outside its range
+ * returns RBS_ERR_ARG. */
+int rbs_select_variant(const rbs_shape* shape, const void* Q, const rbs_stats* stats, const rbs_box* box,
+                       int32_t selector, float param, int32_t n_sink, int32_t n_local, int32_t n_recent,
+                       int32_t* counts, int32_t* indices, void* stream);
 
 /* Full causal lists (every block 0..i for every row): the dense path. */
 int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream);

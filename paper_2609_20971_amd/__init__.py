@@ -4,10 +4,16 @@
     counts, indices = rbs_select(shape, Q, stats, tau_b, tau_r, sink, local, recent)  # Sec. 3.2
     O = rbs_sparse_prefill(shape, Q, K, V, counts, indices)            # Sec. 3.3
     counts, indices, O = rbs_select_attend(shape, Q, K, V, stats, ...)   # Sec. 3.2-3.3 in one pass
+    box = rbs_block_box(shape, K); rbs_select_variant(shape, Q, stats, "box", rho, ..., box=box)  # supporting selectors
 """
 
 from ._lib import (  # noqa: F401
     BlockStats,
+    BoxStats,
+    SELECTORS,
+    rbs_block_box,
+    rbs_box,
+    rbs_select_variant,
     RbsError,
     allocate_lists,
     load,

@@ -47,6 +47,17 @@ class rbs_stats(ctypes.Structure):
     ]
 
 
+class rbs_box(ctypes.Structure):
+    _fields_ = [
+        ("center", ctypes.c_void_p),
+        ("half", ctypes.c_void_p),
+        ("summary", ctypes.c_void_p),
+    ]
+
+
+RBS_SELECTOR_CENTROID, RBS_SELECTOR_FULL_L2, RBS_SELECTOR_BOX = 1, 2, 3
+SELECTORS = {"centroid": RBS_SELECTOR_CENTROID, "full_l2": RBS_SELECTOR_FULL_L2, "box": RBS_SELECTOR_BOX}
+
 _lib = None
 
 
@@ -73,6 +84,13 @@ def load() -> ctypes.CDLL:
     lib.rbs_select_attend.argtypes = [SP, P, P, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, F32, P, P, P,
                                       P, P]
     lib.rbs_select_attend.restype = ctypes.c_int
+    lib.rbs_box_summary_bytes.argtypes = [SP]
+    lib.rbs_box_summary_bytes.restype = SZ
+    lib.rbs_block_box.argtypes = [SP, P, ctypes.POINTER(rbs_box), P]
+    lib.rbs_block_box.restype = ctypes.c_int
+    lib.rbs_select_variant.argtypes = [SP, P, ctypes.POINTER(rbs_stats), ctypes.POINTER(rbs_box), I32, F32, I32,
+                                       I32, I32, P, P, P]
+    lib.rbs_select_variant.restype = ctypes.c_int
     lib.rbs_dense_indices.argtypes = [SP, P, P, P]
     lib.rbs_dense_indices.restype = ctypes.c_int
     lib.rbs_status_str.argtypes = [ctypes.c_int]
@@ -149,6 +167,52 @@ def rbs_block_stats(shape: rbs_shape, K: torch.Tensor, stats: BlockStats | None 
     c = stats.as_c()
     _check("rbs_block_stats", load().rbs_block_stats(ctypes.byref(shape), _ptr(K), ctypes.byref(c), _stream(stream)))
     return stats
+
+
+@dataclass
+class BoxStats:
+    """Device buffers of rbs_box (allocated by the caller: here, torch)."""
+    shape: rbs_shape
+    center: torch.Tensor   # fp32 [H_kv][M][d]
+    half: torch.Tensor     # fp32 [H_kv][M][d]
+    summary: torch.Tensor  # uint8 [rbs_box_summary_bytes]
+
+    @classmethod
+    def allocate(cls, shape: rbs_shape, device="cuda") -> "BoxStats":
+        m, hk, d = n_blocks(shape), shape.n_kv_heads, shape.head_dim
+        nbytes = int(load().rbs_box_summary_bytes(ctypes.byref(shape)))
+        if nbytes == 0:
+            raise RbsError("rbs_box_summary_bytes", RBS_ERR_SHAPE, "invalid shape")
+        f32 = dict(dtype=torch.float32, device=device)
+        return cls(shape, torch.empty((hk, m, d), **f32), torch.empty((hk, m, d), **f32),
+                   torch.empty(nbytes, dtype=torch.uint8, device=device))
+
+    def as_c(self) -> rbs_box:
+        return rbs_box(_ptr(self.center), _ptr(self.half), _ptr(self.summary))
+
+
+def rbs_block_box(shape: rbs_shape, K: torch.Tensor, box: BoxStats | None = None, stream=None) -> BoxStats:
+    """Coordinate-wise key box of every block (centre, half-width)."""
+    if box is None:
+        box = BoxStats.allocate(shape, K.device)
+    c = box.as_c()
+    _check("rbs_block_box", load().rbs_block_box(ctypes.byref(shape), _ptr(K), ctypes.byref(c), _stream(stream)))
+    return box
+
+
+def rbs_select_variant(shape: rbs_shape, Q: torch.Tensor, stats: BlockStats, selector, param: float,
+                       n_sink: int, n_local: int, n_recent: int, box: BoxStats | None = None, counts=None,
+                       indices=None, stream=None):
+    """A supporting selector ("centroid", "full_l2", "box" or its RBS_SELECTOR_* code)."""
+    sel = SELECTORS[selector] if isinstance(selector, str) else int(selector)
+    if counts is None or indices is None:
+        counts, indices = allocate_lists(shape, Q.device)
+    c = stats.as_c()
+    b = box.as_c() if box is not None else None
+    _check("rbs_select_variant", load().rbs_select_variant(
+        ctypes.byref(shape), _ptr(Q), ctypes.byref(c), ctypes.byref(b) if b is not None else None, sel,
+        float(param), int(n_sink), int(n_local), int(n_recent), _ptr(counts), _ptr(indices), _stream(stream)))
+    return counts, indices
 
 
 def allocate_lists(shape: rbs_shape, device="cuda"):

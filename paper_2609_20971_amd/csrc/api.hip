@@ -40,6 +40,11 @@ int check_stats_ptrs(const rbs_stats* st) {
 
 int from_hip(hipError_t e) { return e == hipSuccess ? RBS_OK : RBS_ERR_HIP; }
 
+// Byte offset of the half-widths in the box summary (centres first, 256-aligned).
+size_t box_half_offset(int n_kv_heads, int n_blocks) {
+  return ((size_t)n_kv_heads * n_blocks * 128 * sizeof(_Float16) + 255) & ~(size_t)255;
+}
+
 }  // namespace
 
 extern "C" {
@@ -187,6 +192,85 @@ int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, cons
   aa.O = static_cast<uint16_t*>(O);
   aa.lse = lse;
   return from_hip(rbs::launch_select_attend(sa, aa, static_cast<hipStream_t>(stream)));
+}
+
+size_t rbs_box_summary_bytes(const rbs_shape* shape) {
+  if (check_shape(shape) != RBS_OK) return 0;
+  return 2 * box_half_offset(shape->n_kv_heads, blocks_of(shape));
+}
+
+int rbs_block_box(const rbs_shape* shape, const void* K, const rbs_box* box, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (K == nullptr || box == nullptr || box->center == nullptr || box->half == nullptr || box->summary == nullptr)
+    return RBS_ERR_NULL;
+  if (!aligned16(K) || !aligned16(box->center) || !aligned16(box->half) || !aligned16(box->summary))
+    return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  rbs::BoxArgs a;
+  a.K = static_cast<const uint16_t*>(K);
+  a.n_tokens = shape->n_tokens;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = M;
+  a.center = box->center;
+  a.half = box->half;
+  a.center16 = static_cast<_Float16*>(box->summary);
+  a.half16 = reinterpret_cast<_Float16*>(static_cast<unsigned char*>(box->summary) +
+                                         box_half_offset(shape->n_kv_heads, M));
+  return from_hip(rbs::launch_box(a, static_cast<hipStream_t>(stream)));
+}
+
+int rbs_select_variant(const rbs_shape* shape, const void* Q, const rbs_stats* stats, const rbs_box* box,
+                       int32_t selector, float param, int32_t n_sink, int32_t n_local, int32_t n_recent,
+                       int32_t* counts, int32_t* indices, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (Q == nullptr || counts == nullptr || indices == nullptr || stats == nullptr || stats->summary == nullptr)
+    return RBS_ERR_NULL;
+  if (selector != RBS_SELECTOR_CENTROID && selector != RBS_SELECTOR_FULL_L2 && selector != RBS_SELECTOR_BOX)
+    return RBS_ERR_ARG;
+  if (selector == RBS_SELECTOR_BOX) {
+    if (!(param > 0.f && param <= 1.f)) return RBS_ERR_ARG;
+    if (box == nullptr || box->summary == nullptr) return RBS_ERR_NULL;
+    if (!aligned16(box->summary)) return RBS_ERR_ALIGN;
+  } else if (!(param >= 0.f && param <= 1.f)) {
+    return RBS_ERR_ARG;
+  }
+  if (selector == RBS_SELECTOR_FULL_L2) {
+    if (stats->radii == nullptr) return RBS_ERR_NULL;
+    if (!aligned16(stats->radii)) return RBS_ERR_ALIGN;
+  }
+  if (n_sink < 0 || n_local < 1 || n_recent < 0) return RBS_ERR_ARG;
+  if (!aligned16(Q) || !aligned16(counts) || !aligned16(indices) || !aligned16(stats->summary)) return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  rbs::SelectArgs a;
+  a.Q = static_cast<const uint16_t*>(Q);
+  a.n_tokens = shape->n_tokens;
+  a.n_q_heads = shape->n_q_heads;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = M;
+  a.mode = selector;  // RBS_SELECTOR_* equals the kernel's SelectMode
+  if (selector == RBS_SELECTOR_BOX) {
+    a.cent16 = static_cast<const _Float16*>(box->summary);
+    a.half16 = reinterpret_cast<const _Float16*>(static_cast<const unsigned char*>(box->summary) +
+                                                 box_half_offset(shape->n_kv_heads, M));
+    a.budget = param;
+    a.tau_base = a.tau_rescue = 1.f;  // unused
+  } else {
+    a.cent16 = static_cast<const _Float16*>(stats->summary);
+    a.tau_base = a.tau_rescue = param;
+  }
+  a.uplift = nullptr;
+  a.radii = stats->radii;
+  a.n_sink = n_sink;
+  a.n_local = n_local;
+  a.n_recent = n_recent;
+  a.counts = counts;
+  a.indices = indices;
+  a.capacity = rbs_index_capacity(M);
+  return from_hip(rbs::launch_select(a, static_cast<hipStream_t>(stream)));
 }
 
 int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream) {

@@ -18,11 +18,24 @@ struct StatsArgs {
   float* uplift;     // select-ready rescue uplift [H_kv][M]
 };
 
+struct BoxArgs {
+  const uint16_t* K;
+  int n_tokens, n_kv_heads, block_size, n_blocks;
+  float* center;
+  float* half;
+  _Float16* center16;  // select-ready copies [H_kv][M][d]
+  _Float16* half16;
+};
+
 struct SelectArgs {
   const uint16_t* Q;
   int n_tokens, n_q_heads, n_kv_heads, block_size, n_blocks;
-  const _Float16* cent16;
+  int mode = 0;                       // SelectMode (select_block.hpp)
+  const _Float16* cent16;             // box: scaled box centres
+  const _Float16* half16 = nullptr;   // box: scaled box half-widths
   const float* uplift;
+  const float* radii = nullptr;       // full-L2
+  float budget = 0.f;                 // box: budget fraction
   float tau_base, tau_rescue;
   int n_sink, n_local, n_recent;
   int32_t* counts;
@@ -54,6 +67,7 @@ inline size_t summary_bytes(int n_kv_heads, int n_blocks) {
 }
 
 hipError_t launch_stats(const StatsArgs& a, hipStream_t s);
+hipError_t launch_box(const BoxArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStream_t s);

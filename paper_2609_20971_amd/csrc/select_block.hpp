@@ -31,40 +31,56 @@ constexpr int kTile = 32;  // centroids per tile
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
 
+// Selection policies: the method's dual-branch selector and the three
+// supporting selectors of the paper's selector comparison (Table
+// selector_ablation), each a single branch united with the forced blocks.
+enum SelectMode {
+  kSelectDual = 0,      // base + rescue branches (Sec. 3.2)
+  kSelectCentroid = 1,  // base branch alone, relative threshold
+  kSelectFullL2 = 2,    // rescue branch with beta = 1 (Eq. full_l2_bound), relative threshold
+  kSelectBox = 3,       // Quest-style box bound (Eq. quest_box), fixed budget
+};
+
 // Arguments of one selection, shared by the stand-alone and the fused kernel.
 struct SelectCore {
   const uint16_t* Q;
   int N, M, group;
-  const _Float16* cent16;
-  const float* uplift;
-  float log2_tau_base, log2_tau_rescue;
+  const _Float16* cent16;     // dual, centroid, full-L2: scaled centroids; box: scaled box centres
+  const _Float16* half16;     // box: scaled box half-widths
+  const float* uplift;        // dual: r beta log2(e)/sqrt(d)
+  const float* radii;         // full-L2: r (scaled here)
+  float log2_tau_base, log2_tau_rescue;  // centroid / full-L2: the one threshold in both
+  float budget;               // box: budget fraction rho
   int base_all, rescue_all, n_sink, n_local, n_recent;
   int32_t* counts;
   int32_t* indices;
   int64_t capacity;
 };
 
-template <int BS>
+template <int BS, int MODE = kSelectDual>
 constexpr size_t select_smem_bytes(int M) {
-  return 2 * kTile * 256 + 2 * (BS / 32) * kTile * 16 + BS * 4 + 2 * (size_t)M * 4 + 3 * (BS / 32) * 4;
+  return (MODE == kSelectBox ? 4 : 2) * kTile * 256 + 2 * (BS / 32) * kTile * 16 + BS * 4 + 2 * (size_t)M * 4 +
+         3 * (BS / 32) * 4 + (MODE == kSelectBox ? 2 * (BS / 32) * 4 : 0);
 }
 
 // Selection of query block i of query head h by the B/32 waves of the calling
 // workgroup.  smem: select_smem_bytes<BS>(M) bytes of LDS; list_lds (may be
 // null): receives a copy of the ascending list.  Writes counts and the list to
 // global memory and returns the count (to every thread).
-template <int BS>
+template <int BS, int MODE = kSelectDual>
 __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, unsigned char* smem_raw,
                                             __attribute__((address_space(3))) int32_t* list_lds) {
   constexpr int NW = BS / 32;
   constexpr int NT = NW * kWave;
   const uint16_t* __restrict__ Q = c.Q;
   const int N = c.N, M = c.M;
-  // Layout: cbuf[2][32 rows][16 chunks of 8 f16] | stage[2][NW][32][4] | nq[BS] | L_base[M] | L_res[M] |
-  // red_f[2 NW] | red_i[NW]
+  // Layout: cbuf[2][32 rows][16 chunks of 8 f16] (| hbuf[2][32][16], box) | stage[2][NW][32][4] | nq[BS] |
+  // L_base[M] | L_res[M] | red_f[2 NW] | red_i[NW] (| cnt[2][NW], box)
+  constexpr int kTileBufs = MODE == kSelectBox ? 4 : 2;
   uint4* cbuf = reinterpret_cast<uint4*>(smem_raw);
-  float4* stage = reinterpret_cast<float4*>(smem_raw + 2 * kTile * 256);
-  float* nq_s = reinterpret_cast<float*>(smem_raw + 2 * kTile * 256 + 2 * NW * kTile * 16);
+  uint4* hbuf = cbuf + 2 * kTile * 16;
+  float4* stage = reinterpret_cast<float4*>(smem_raw + kTileBufs * kTile * 256);
+  float* nq_s = reinterpret_cast<float*>(smem_raw + kTileBufs * kTile * 256 + 2 * NW * kTile * 16);
   float* L_base = nq_s + BS;
   float* L_res = L_base + M;
   float* red_f = L_res + M;
@@ -78,12 +94,15 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   const int n_cand = i + 1;
   const int n_tiles = (n_cand + kTile - 1) / kTile;
   const _Float16* cg = c.cent16 + (size_t)g * M * kHeadDim;
-  const float* ug = c.uplift + (size_t)g * M;
+  const _Float16* hg = MODE == kSelectBox ? c.half16 + (size_t)g * M * kHeadDim : nullptr;
+  const float* ug = MODE == kSelectFullL2 ? c.radii + (size_t)g * M : c.uplift + (size_t)g * M;
+  const float u_scale = MODE == kSelectFullL2 ? kLog2e / sqrtf((float)kHeadDim) : 1.0f;
 
   // ---- Q rows of this wave as MFMA A operands (row = 32*wave + l32).
   const int t_local = 32 * wave + l32;
   const bool row_ok = t_local < nb;
   f16x8 qa[8];
+  f16x8 qabs[MODE == kSelectBox ? 8 : 1];  // |q| for the box half-widths
   float sq = 0.f;
   {
     const uint16_t* qrow = Q + ((size_t)h * N + row0 + t_local) * kHeadDim + 8 * half;
@@ -95,6 +114,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         qa[ks][e] = (_Float16)f[e];
+        if constexpr (MODE == kSelectBox) qabs[ks][e] = (_Float16)fabsf(f[e]);
         sq = fmaf(f[e], f[e], sq);
       }
     }
@@ -113,20 +133,28 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   constexpr int kLdRowsPerPass = NT / 16;
   constexpr int kLdPasses = (kTile + kLdRowsPerPass - 1) / kLdRowsPerPass;
   uint4 pre[kLdPasses];
+  uint4 preh[MODE == kSelectBox ? kLdPasses : 1];
   auto fetch = [&](int tile) {
 #pragma unroll
     for (int p = 0; p < kLdPasses; ++p) {
       const int r = ld_row + p * kLdRowsPerPass;
       const int bb = tile * kTile + r;
-      pre[p] = (r < kTile && bb < M) ? *reinterpret_cast<const uint4*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk)
-                                     : make_uint4(0u, 0u, 0u, 0u);
+      const bool ok = r < kTile && bb < M;
+      pre[p] = ok ? *reinterpret_cast<const uint4*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk)
+                  : make_uint4(0u, 0u, 0u, 0u);
+      if constexpr (MODE == kSelectBox)
+        preh[p] = ok ? *reinterpret_cast<const uint4*>(hg + (size_t)bb * kHeadDim + 8 * ld_chunk)
+                     : make_uint4(0u, 0u, 0u, 0u);
     }
   };
   auto store = [&](int buf) {
 #pragma unroll
     for (int p = 0; p < kLdPasses; ++p) {
       const int r = ld_row + p * kLdRowsPerPass;
-      if (r < kTile) cbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = pre[p];
+      if (r < kTile) {
+        cbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = pre[p];
+        if constexpr (MODE == kSelectBox) hbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = preh[p];
+      }
     }
   };
   fetch(0);
@@ -155,6 +183,17 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         __builtin_memcpy(&bfrag, &raw, 16);
         acc = mfma_f16(qa[ks], bfrag, acc);
       }
+      if constexpr (MODE == kSelectBox) {
+        // + |q| . h_b: Eq. quest_box written as q . v_b + |q|^T h_b.
+        const uint4* hb = hbuf + buf * kTile * 16 + l32 * 16;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+          const uint4 raw = hb[swz(l32, 2 * ks + half)];
+          f16x8 bfrag;
+          __builtin_memcpy(&bfrag, &raw, 16);
+          acc = mfma_f16(qabs[ks], bfrag, acc);
+        }
+      }
       if (wave_partial) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -167,9 +206,13 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       float sb = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
-      const float u = (b < M) ? ug[b] : 0.f;
       float mr = mx, sr = sb;
-      if (__any(u != 0.f)) {
+      if constexpr (MODE == kSelectCentroid || MODE == kSelectBox) {
+        mr = -INFINITY;  // single branch: no rescue scores
+        sr = 0.f;
+      }
+      const float u = (MODE == kSelectDual || MODE == kSelectFullL2) && b < M ? ug[b] * u_scale : 0.f;
+      if ((MODE == kSelectDual || MODE == kSelectFullL2) && __any(u != 0.f)) {
         mr = mx + nq_max * u;
         sr = 0.f;
 #pragma unroll
@@ -230,6 +273,34 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   const float thr_res = mres + c.log2_tau_rescue;
   const bool recent_row = i >= M - c.n_recent;
 
+  // ---- Box: fixed budget, the k = max(1, ceil(rho |C_i|)) highest scores
+  // (ties with the k-th kept).  The k-th largest is found by a bitwise
+  // bisection on order-preserving integer keys of the scores: it is the
+  // largest key v with #{key >= v} >= k.
+  uint32_t kth_key = 0u;
+  if constexpr (MODE == kSelectBox) {
+    auto okey = [](float f) __attribute__((always_inline)) {
+      const uint32_t u = __float_as_uint(f);
+      return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    };
+    const int k = max(1, min(n_cand, (int)ceil((double)c.budget * (double)n_cand - 1e-12)));
+    int* cnt = red_i + NW;  // [2][NW]
+    for (int bit = 31, it = 0; bit >= 0; --bit, ++it) {
+      const uint32_t cand = kth_key | (1u << bit);
+      int mine = 0;
+      for (int b = tid; b < n_cand; b += NT) mine += okey(L_base[b]) >= cand ? 1 : 0;
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) mine += __shfl_xor(mine, m, kWave);
+      int* cb = cnt + (it & 1) * NW;
+      if (lane == 0) cb[wave] = mine;
+      __syncthreads();
+      int total = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) total += cb[w];
+      if (total >= k) kth_key = cand;
+    }
+  }
+
   // ---- Union with forced blocks and compaction to an ascending list.
   int32_t* out = c.indices + (int64_t)h * c.capacity + (int64_t)i * (i + 1) / 2;
   int total = 0;
@@ -237,8 +308,17 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     const int b = base + tid;
     bool sel = false;
     if (b < n_cand) {
-      sel = recent_row || b < c.n_sink || b > i - c.n_local || c.base_all || c.rescue_all ||
-            L_base[b] >= thr_base || L_res[b] >= thr_res;
+      const bool forced = recent_row || b < c.n_sink || b > i - c.n_local;
+      if constexpr (MODE == kSelectDual)
+        sel = forced || c.base_all || c.rescue_all || L_base[b] >= thr_base || L_res[b] >= thr_res;
+      else if constexpr (MODE == kSelectCentroid)
+        sel = forced || c.base_all || L_base[b] >= thr_base;
+      else if constexpr (MODE == kSelectFullL2)
+        sel = forced || c.rescue_all || L_res[b] >= thr_res;
+      else {
+        const uint32_t u = __float_as_uint(L_base[b]);
+        sel = forced || ((u & 0x80000000u) ? ~u : (u | 0x80000000u)) >= kth_key;
+      }
     }
     const uint64_t ballot = __ballot(sel);
     const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(ballot >> 32),
@@ -270,7 +350,10 @@ inline SelectCore make_select_core(const SelectArgs& a) {
   c.M = a.n_blocks;
   c.group = a.n_q_heads / a.n_kv_heads;
   c.cent16 = a.cent16;
+  c.half16 = a.half16;
   c.uplift = a.uplift;
+  c.radii = a.radii;
+  c.budget = a.budget;
   c.log2_tau_base = a.tau_base > 0.f ? log2f(a.tau_base) : -INFINITY;
   c.log2_tau_rescue = a.tau_rescue > 0.f ? log2f(a.tau_rescue) : -INFINITY;
   c.base_all = a.tau_base <= 0.f;

@@ -159,6 +159,79 @@ __global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __
   if (tid == 0) radii[blk] = sqrtf(fmaxf(fmaxf(red_r[0], red_r[1]), fmaxf(red_r[2], red_r[3])));
 }
 
+// Coordinate-wise box of every key block for the Quest-style supporting
+// selector (App. geometry, Eq. quest_box): per dimension the minimum a and
+// maximum u over the block's keys, written as centre (u + a)/2 and half-width
+// (u - a)/2 (both exact in fp32 for bf16 inputs), plus f16 copies scaled by
+// log2(e)/sqrt(d) for the selector's MFMA.  Same layout and row mapping as
+// stats_kernel: one workgroup per (KV head, key block), 16 lanes per row.
+template <int BS>
+__global__ __launch_bounds__(kStatsThreads) void box_kernel(const uint16_t* __restrict__ K, int N, int M,
+                                                           float* __restrict__ center, float* __restrict__ half,
+                                                           _Float16* __restrict__ center16,
+                                                           _Float16* __restrict__ half16, float sel_scale) {
+  constexpr int kRowsPerThread = BS / 16;
+  __shared__ float red_lo[4][kHeadDim];
+  __shared__ float red_hi[4][kHeadDim];
+  const int b = blockIdx.x, g = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int chunk = tid & 15, rg = tid >> 4;
+  const int row0 = b * BS;
+  const int nb = min(BS, N - row0);
+  const uint16_t* kb = K + ((size_t)g * N + row0) * kHeadDim + chunk * 8;
+  float lo[8], hi[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    lo[e] = INFINITY;
+    hi[e] = -INFINITY;
+  }
+#pragma unroll
+  for (int k = 0; k < kRowsPerThread; ++k) {
+    const int r = rg + 16 * k;
+    if (r < nb) {
+      float f[8];
+      unpack8(*reinterpret_cast<const uint4*>(kb + (size_t)r * kHeadDim), f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        lo[e] = fminf(lo[e], f[e]);
+        hi[e] = fmaxf(hi[e], f[e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    lo[e] = fminf(lo[e], wave_xor_f(lo[e], 16));
+    lo[e] = fminf(lo[e], wave_xor_f(lo[e], 32));
+    hi[e] = fmaxf(hi[e], wave_xor_f(hi[e], 16));
+    hi[e] = fmaxf(hi[e], wave_xor_f(hi[e], 32));
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      red_lo[wave][chunk * 8 + e] = lo[e];
+      red_hi[wave][chunk * 8 + e] = hi[e];
+    }
+  }
+  __syncthreads();
+  if (tid < 16) {
+    const size_t base = ((size_t)g * M + b) * kHeadDim + chunk * 8;
+    f16x8 c16, h16;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int x = chunk * 8 + e;
+      const float a = fminf(fminf(red_lo[0][x], red_lo[1][x]), fminf(red_lo[2][x], red_lo[3][x]));
+      const float u = fmaxf(fmaxf(red_hi[0][x], red_hi[1][x]), fmaxf(red_hi[2][x], red_hi[3][x]));
+      const float c = (u + a) * 0.5f, hw = (u - a) * 0.5f;
+      center[base + e] = c;
+      half[base + e] = hw;
+      c16[e] = (_Float16)(c * sel_scale);
+      h16[e] = (_Float16)(hw * sel_scale);
+    }
+    *reinterpret_cast<f16x8*>(center16 + base) = c16;
+    *reinterpret_cast<f16x8*>(half16 + base) = h16;
+  }
+}
+
 __global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __restrict__ radii, int M,
                                                                 float* __restrict__ beta,
                                                                 float* __restrict__ quantiles,
@@ -220,6 +293,24 @@ hipError_t launch_stats(const StatsArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(quantile_kernel, dim3(a.n_kv_heads), dim3(kStatsThreads), 0, s, a.radii, a.n_blocks, a.beta,
                      a.quantiles, a.uplift, sel_scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_box(const BoxArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_blocks, a.n_kv_heads);
+  const float sel_scale = kLog2e / sqrtf((float)kHeadDim);
+#define RBS_BOX_CASE(BSZ)                                                                                   \
+  case BSZ:                                                                                                 \
+    hipLaunchKernelGGL(box_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, a.n_tokens, a.n_blocks,       \
+                       a.center, a.half, a.center16, a.half16, sel_scale);                                  \
+    break;
+  switch (a.block_size) {
+    RBS_BOX_CASE(64)
+    RBS_BOX_CASE(128)
+    RBS_BOX_CASE(256)
+    default: return hipErrorInvalidValue;
+  }
+#undef RBS_BOX_CASE
   return hipGetLastError();
 }
 

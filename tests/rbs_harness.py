@@ -97,7 +97,10 @@ def compare_masks(gpu_lists, oracle_rows):
         diff = np.nonzero(g != ref["final"])[0]
         for b in diff:
             assert not ref["forced"][b], f"forced block {b} differs in row {key}"
-            mb, mr = ref["margin_base"][b], ref["margin_rescue"][b]
+            if "margin" in ref:  # single-branch supporting selector
+                mb = mr = ref["margin"][b]
+            else:
+                mb, mr = ref["margin_base"][b], ref["margin_rescue"][b]
             ok = abs(mb) <= MARGIN_BAND or abs(mr) <= MARGIN_BAND
             assert ok, (f"row {key} block {b}: gpu={bool(g[b])} oracle={bool(ref['final'][b])} "
                         f"margins base={mb:.3g} rescue={mr:.3g}")

@@ -148,3 +148,51 @@ def test_binding_raises_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         L.load()
+
+
+def _box(rbs, ptr=FAKE, **override):
+    vals = dict(center=ptr, half=ptr, summary=ptr)
+    vals.update(override)
+    return rbs.rbs_box(**vals)
+
+
+def _variant(lib, s, st, bx, sel=1, param=0.5, sink=1, local=1, recent=0, Q=FAKE, counts=FAKE, indices=FAKE):
+    return lib.rbs_select_variant(ctypes.byref(s), Q, ctypes.byref(st) if st is not None else None,
+                                  ctypes.byref(bx) if bx is not None else None, sel, param, sink, local, recent,
+                                  counts, indices, None)
+
+
+def test_box_summary_size_and_validation():
+    rbs, lib = _lib()
+    s = rbs.make_shape(1000, 4, 2, 64)
+    M = 16
+    assert lib.rbs_box_summary_bytes(ctypes.byref(s)) >= 2 * 2 * M * 128 * 2
+    bad = rbs.make_shape(1000, 4, 2, 96)
+    assert lib.rbs_box_summary_bytes(ctypes.byref(bad)) == 0
+    assert lib.rbs_block_box(ctypes.byref(bad), FAKE, ctypes.byref(_box(rbs)), None) == 3
+    assert lib.rbs_block_box(ctypes.byref(s), None, ctypes.byref(_box(rbs)), None) == 1
+    assert lib.rbs_block_box(ctypes.byref(s), FAKE, None, None) == 1
+    for field in ("center", "half", "summary"):
+        assert lib.rbs_block_box(ctypes.byref(s), FAKE, ctypes.byref(_box(rbs, **{field: None})), None) == 1
+        assert lib.rbs_block_box(ctypes.byref(s), FAKE, ctypes.byref(_box(rbs, **{field: MIS})), None) == 5
+
+
+def test_select_variant_validation():
+    rbs, lib = _lib()
+    s = rbs.make_shape(1024, 4, 2, 64)
+    st, bx = _stats(rbs), _box(rbs)
+    for sel in (0, 4, -1):
+        assert _variant(lib, s, st, bx, sel=sel) == 4
+    for sel, param in ((1, -0.1), (1, 1.5), (2, float("nan")), (3, 0.0), (3, 1.01), (3, -0.5)):
+        assert _variant(lib, s, st, bx, sel=sel, param=param) == 4
+    assert _variant(lib, s, st, None, sel=3, param=0.1) == 1
+    assert _variant(lib, s, st, _box(rbs, summary=None), sel=3, param=0.1) == 1
+    assert _variant(lib, s, st, _box(rbs, summary=MIS), sel=3, param=0.1) == 5
+    assert _variant(lib, s, _stats(rbs, radii=None), bx, sel=2) == 1
+    assert _variant(lib, s, _stats(rbs, radii=MIS), bx, sel=2) == 5
+    assert _variant(lib, s, None, bx) == 1
+    assert _variant(lib, s, st, bx, Q=None) == 1
+    assert _variant(lib, s, st, bx, counts=MIS) == 5
+    assert _variant(lib, s, st, bx, local=0) == 4
+    bad = rbs.make_shape(1024, 3, 2, 64)
+    assert _variant(lib, bad, st, bx) == 2

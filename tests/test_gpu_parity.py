@@ -252,3 +252,75 @@ def test_fused_select_attend_forced_and_dense_rows():
 def test_fused_select_attend_128k_matches_two_calls():
     """The headline layer through the fused entry point: identical to the two calls."""
     _fused_matches_two_calls(WORKLOADS["qwen3-30b-a3b-128k"])
+
+
+# ------------------------------------------------ supporting selectors (Table selector_ablation)
+
+def _variant_check(w: Workload, variant: str, param: float, rows=None, inputs=None):
+    """A supporting selector through the C ABI against the oracle's: box
+    statistics to fp32 rounding, lists bit for bit outside the near-threshold
+    band, the same structural invariants as the method's lists."""
+    import torch
+    import paper_2609_20971_amd as rbs
+    if inputs is None:
+        inputs = make_inputs(w)
+    shape = rbs.make_shape(w.seq_len, w.n_q_heads, w.n_kv_heads, w.block_size)
+    Qd, Kd = H.to_device(inputs["q"]), H.to_device(inputs["k"])
+    st = rbs.rbs_block_stats(shape, Kd)
+    box = rbs.rbs_block_box(shape, Kd) if variant == "box" else None
+    counts, indices = rbs.rbs_select_variant(shape, Qd, st, variant, param, w.n_sink, w.n_local, w.n_recent,
+                                             box=box)
+    torch.cuda.synchronize()
+    Kf = f64_from_bf16_bits(inputs["k"])
+    C, R = oracle.block_stats(Kf, w.block_size)
+    Vc = Hw = None
+    if variant == "box":
+        Vc, Hw = oracle.block_box(Kf, w.block_size)
+        for got, ref in ((box.center, Vc), (box.half, Hw)):
+            g = got.double().cpu().numpy()
+            assert np.abs(g - ref).max() <= 1e-6 * max(1.0, np.abs(ref).max())
+    M = w.n_blocks
+    rows = rows or [(h, i) for h in range(w.n_q_heads) for i in range(M)]
+    Qf = f64_from_bf16_bits(inputs["q"])
+    # The ABI takes the parameter as float32: the oracle gets that same value
+    # (a budget of 0.3 is 0.30000001, whose ceil(rho n) can differ from 0.3's).
+    param32 = float(np.float32(param))
+    ref = oracle.select_variant(Qf, C, R, Vc, Hw, w.block_size, variant, param32, w.n_sink, w.n_local,
+                                w.n_recent, rows=rows)
+    lists = H.gpu_rows(counts, indices, rows)
+    H.check_lists(lists, M, w.n_sink, w.n_local, w.n_recent)
+    n_rows, compared, near = H.compare_masks(lists, ref)
+    dens = sum(len(v) for v in lists.values()) / compared
+    _say(f"[parity] selector {variant}({param}) {w.name} N={w.seq_len} B={w.block_size}: rows {n_rows} "
+         f"blocks {compared} near-threshold flips {near}; density {dens:.4f}")
+    return lists
+
+
+@pytest.mark.parametrize("variant,param", [
+    ("centroid", 0.9), ("centroid", 0.194), ("full_l2", 0.9), ("full_l2", 0.022), ("box", 0.0405), ("box", 0.3),
+])
+@pytest.mark.parametrize("shape", [
+    dict(),
+    dict(seq_len=1000, block_size=64, n_q_heads=4, n_kv_heads=2, seed=1),
+    dict(seq_len=777, block_size=128, n_q_heads=2, n_kv_heads=2, seed=2),
+    dict(seq_len=1300, block_size=256, n_q_heads=4, n_kv_heads=1, seed=3),
+])
+def test_supporting_selectors_match_oracle(variant, param, shape):
+    w = WORKLOADS["tiny-2k"].with_(name="selectors", **shape)
+    _variant_check(w, variant, param)
+
+
+def test_supporting_selector_extremes():
+    """Threshold 0 keeps every causal block; a budget of 1 keeps every block."""
+    w = WORKLOADS["tiny-2k"].with_(seq_len=1536, seed=7)
+    for variant, param in (("centroid", 0.0), ("full_l2", 0.0), ("box", 1.0)):
+        lists = _variant_check(w, variant, param)
+        assert all(len(ids) == i + 1 for (h, i), ids in lists.items())
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("variant,param", [("centroid", 0.194), ("full_l2", 0.022), ("box", 0.0405)])
+def test_supporting_selectors_32k_sampled(variant, param):
+    w = WORKLOADS["qwen3-30b-a3b-32k"]
+    rows = H.sample_rows(w.n_q_heads, w.n_blocks, 24, seed=8, include=[(3, w.n_blocks - 1)])
+    _variant_check(w, variant, param, rows=rows)
