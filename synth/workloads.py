@@ -44,6 +44,7 @@ class Workload:
     rope: bool = False
     rope_base: float = 1.0e6
     needles_per_kv_head: int = 0
+    needle_norm: float = 3.0   # |k_p| of a planted needle (the selector study also uses stronger ones)
     # (mu, sigma) of the lognormal per-block key-noise scale: one pair for all
     # KV heads, or one pair per KV head.
     key_noise: tuple = ((0.0, 0.5),)
@@ -194,7 +195,7 @@ def make_inputs(w: Workload, threads: int | None = None) -> dict:
         for (gg, p, h, j) in plan:
             if gg == g:
                 t = needle_rows[(h, j)]
-                x[p] = 3.0 * t / np.linalg.norm(t)
+                x[p] = w.needle_norm * t / np.linalg.norm(t)
         k[g] = bf16_bits_from_f32(x)
 
     def gen_v(g):
