@@ -14,6 +14,11 @@
  *   rbs_block_box,      the supporting selectors of the paper's selector
  *   rbs_select_variant  comparison (centroid-only, full-L2 bound, Quest-style
  *                       box; Table selector_ablation, App. geometry)
+ *   rbs_*_varlen        the three stages over a batch of independent
+ *                       sequences in one launch each (appendix on A100
+ *                       system measurements, prompt throughput: batched
+ *                       prompts are separate causal sequences, never one
+ *                       concatenated sequence)
  *
  * Conventions shared by every call
  *   - Tensors are dense, row-major, in device memory:
@@ -197,6 +202,56 @@ int rbs_select_variant(const rbs_shape* shape, const void* Q, const rbs_stats* s
 
 /* Full causal lists (every block 0..i for every row): the dense path. */
 int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Batches of independent sequences (varlen).  The paper runs batched prompts
+ * as separate causal sequences, none concatenated into another (appendix on
+ * A100 system measurements, prompt throughput, Table a100_throughput at batch
+ * four); each sequence is processed exactly as the
+ * single-sequence calls process it, with its own blocks, radius quantiles
+ * and beta (its own prompt's radius distribution, Sec. 3.1), candidates and
+ * causal attention.  All sequences of a batch share one launch per stage.
+ *
+ * Layout: the sequences are packed along the token axis,
+ *   Q, O  bf16 [H_q][T][d]    K, V  bf16 [H_kv][T][d]    lse  fp32 [H_q][T]
+ * with T = shape->n_tokens = sum of seq_tokens; sequence s holds tokens
+ * t_s .. t_s + n_s - 1, t_s = n_0 + ... + n_(s-1).  Blocks restart at every
+ * sequence: sequence s has M_s = ceil(n_s / B) blocks, and the block arrays
+ * hold the sequences' blocks one after another (M_tot = sum of M_s, sequence s
+ * from m_s = M_0 + ... + M_(s-1)):
+ *   centroids fp32 [H_kv][M_tot][d]; radii, beta fp32 [H_kv][M_tot];
+ *   quantiles fp32 [n_seqs][H_kv][2]; summary rbs_varlen_summary_bytes();
+ *   counts int32 [H_q][M_tot] (row i of sequence s at m_s + i);
+ *   indices int32 [H_q][C_tot], C_tot = sum of M_s (M_s + 1) / 2: row i of
+ *   sequence s of head h at h C_tot + c_s + i (i + 1) / 2, c_s the sum of the
+ *   earlier sequences' M (M + 1) / 2.  List entries are block numbers local to
+ *   the sequence (0 .. i).
+ * Limits: 1 <= n_seqs <= RBS_MAX_SEQS; every n_s within the single-sequence
+ * limits; T = sum n_s (else RBS_ERR_SHAPE).  seq_tokens is a host array read
+ * during the call only.  Everything else as in the single-sequence calls.
+ */
+#define RBS_MAX_SEQS 64
+
+typedef struct {
+  int32_t n_seqs;             /* number of sequences, 1 .. RBS_MAX_SEQS       */
+  const int32_t* seq_tokens;  /* host array [n_seqs]: tokens of each sequence */
+} rbs_batch;
+
+/* M_tot, C_tot and the summary size of a batch (0 if shape or batch is invalid). */
+int32_t rbs_varlen_blocks(const rbs_shape* shape, const rbs_batch* batch);
+int64_t rbs_varlen_index_capacity(const rbs_shape* shape, const rbs_batch* batch);
+size_t rbs_varlen_summary_bytes(const rbs_shape* shape, const rbs_batch* batch);
+
+int rbs_block_stats_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* K,
+                           const rbs_stats* stats, void* stream);
+int rbs_select_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* Q, const rbs_stats* stats,
+                      float tau_base, float tau_rescue, int32_t n_sink, int32_t n_local, int32_t n_recent,
+                      int32_t* counts, int32_t* indices, void* stream);
+int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* Q, const void* K,
+                              const void* V, const int32_t* counts, const int32_t* indices,
+                              float softmax_scale, void* O, float* lse, void* stream);
+int rbs_dense_indices_varlen(const rbs_shape* shape, const rbs_batch* batch, int32_t* counts,
+                             int32_t* indices, void* stream);
 
 /* Static description of a status code. */
 const char* rbs_status_str(int status);

@@ -26,6 +26,12 @@ Parity status per function (what pins it, in tests/test_oracle_pins.py):
                        invariance of centroid / full-L2 and its failure for the box
   select_variant       pinned: budget fractions 1 and ~0, monotone budgets, forced
                        blocks, relative thresholds 0 and 1
+  batch_*              pinned: a batch of one is the single sequence; sequences
+                       are independent (changing one leaves the others' results
+                       unchanged); at full selection every sequence's output is
+                       its own brute-force causal attention, unlike the
+                       concatenated sequence; block-aligned sequences share the
+                       concatenation's centroids and radii but not its beta
 """
 
 from .rbs import (
@@ -52,6 +58,11 @@ from .rbs import (
     density,
     masks_from_lists,
     lists_from_masks,
+    batch_offsets,
+    batch_sequences,
+    batch_block_stats,
+    batch_select,
+    batch_attention_on_mask,
 )
 
 __all__ = [
@@ -71,4 +82,9 @@ __all__ = [
     "density",
     "masks_from_lists",
     "lists_from_masks",
+    "batch_offsets",
+    "batch_sequences",
+    "batch_block_stats",
+    "batch_select",
+    "batch_attention_on_mask",
 ]

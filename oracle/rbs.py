@@ -402,3 +402,68 @@ def masks_from_lists(counts, indices, rows):
         row[np.asarray(indices[h, base:base + counts[h, i]], dtype=np.int64)] = True
         out[(h, i)] = row
     return out
+
+
+# ---------------------------------------------------------------- batches
+#
+# App. "Additional A100 System Measurements", prompt throughput: a batch of
+# prompts is a set of independent causal sequences; none is concatenated into
+# another.  Every per-prompt quantity -- the block partition, the radius
+# quantiles and beta (the prompt's own radius distribution, Sec. 3.1), the
+# candidates, the causal attention -- is that of the sequence alone.  Layout of
+# a batch: the sequences packed along the token axis, and the block arrays
+# holding the sequences' blocks one after another.
+
+def batch_offsets(seq_tokens) -> list:
+    """Token offsets of the sequences: 0, n_0, n_0 + n_1, ..., T."""
+    out = [0]
+    for n in seq_tokens:
+        out.append(out[-1] + int(n))
+    return out
+
+
+def batch_sequences(X, seq_tokens) -> list:
+    """[X[:, t_s : t_s + n_s]] for every sequence s of a packed [H][T][d] batch."""
+    off = batch_offsets(seq_tokens)
+    assert off[-1] == X.shape[1], "sequence lengths must add up to the packed length"
+    return [X[:, off[s]:off[s + 1]] for s in range(len(seq_tokens))]
+
+
+def batch_block_stats(K, seq_tokens, block_size: int):
+    """block_stats and rescue_coefficients of every sequence alone, laid out
+    as the batch's block arrays: C [H_kv][M_tot][d], R and beta [H_kv][M_tot],
+    quantiles [n_seqs][H_kv][2]."""
+    parts = [block_stats(Ks, block_size) for Ks in batch_sequences(K, seq_tokens)]
+    coeffs = [rescue_coefficients(R) for (_, R) in parts]
+    C = np.concatenate([c for (c, _) in parts], axis=1)
+    R = np.concatenate([r for (_, r) in parts], axis=1)
+    beta = np.concatenate([b for (b, _) in coeffs], axis=1)
+    rq = np.stack([q for (_, q) in coeffs])
+    return C, R, beta, rq
+
+
+def batch_select(Q, K, seq_tokens, block_size: int, tau_base: float, tau_rescue: float,
+                 n_sink: int, n_local: int, n_recent: int, rows=None) -> dict:
+    """select on every sequence alone.  rows: {s: [(h, i)]} (default: every
+    row of every sequence).  Returns {s: {(h, i): row dict}}, i local to s."""
+    Qs, Ks = batch_sequences(Q, seq_tokens), batch_sequences(K, seq_tokens)
+    out = {}
+    for s in range(len(seq_tokens)):
+        if rows is not None and s not in rows:
+            continue
+        C, R = block_stats(Ks[s], block_size)
+        beta, _ = rescue_coefficients(R)
+        out[s] = select(Qs[s], C, R, beta, block_size, tau_base, tau_rescue, n_sink, n_local, n_recent,
+                        rows=None if rows is None else rows[s])
+    return out
+
+
+def batch_attention_on_mask(Q, K, V, seq_tokens, block_size: int, row_blocks: dict,
+                            scale: float | None = None) -> dict:
+    """attention_on_mask on every sequence alone.  row_blocks: {s: {h: {i:
+    retained blocks}}}, i and the blocks local to s.  Returns {s: {h: {i: O}}}."""
+    Qs, Ks, Vs = (batch_sequences(X, seq_tokens) for X in (Q, K, V))
+    group = Q.shape[0] // K.shape[0]
+    return {s: {h: attention_on_mask(Qs[s][h], Ks[s][h // group], Vs[s][h // group], block_size, rows, scale)
+                for h, rows in heads.items()}
+            for s, heads in row_blocks.items()}

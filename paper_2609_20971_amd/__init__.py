@@ -5,9 +5,24 @@
     O = rbs_sparse_prefill(shape, Q, K, V, counts, indices)            # Sec. 3.3
     counts, indices, O = rbs_select_attend(shape, Q, K, V, stats, ...)   # Sec. 3.2-3.3 in one pass
     box = rbs_block_box(shape, K); rbs_select_variant(shape, Q, stats, "box", rho, ..., box=box)  # supporting selectors
+    batch = Batch([n0, n1, ...]); shape = varlen_shape(batch, H_q, H_kv, B)   # independent sequences, packed
+    stats = rbs_block_stats_varlen(shape, batch, K); ...; rbs_sparse_prefill_varlen(shape, batch, Q, K, V, ...)
 """
 
 from ._lib import (  # noqa: F401
+    Batch,
+    RBS_MAX_SEQS,
+    allocate_lists_varlen,
+    allocate_stats_varlen,
+    rbs_batch,
+    rbs_block_stats_varlen,
+    rbs_dense_indices_varlen,
+    rbs_select_varlen,
+    rbs_sparse_prefill_varlen,
+    rbs_varlen_blocks,
+    rbs_varlen_index_capacity,
+    rbs_varlen_summary_bytes,
+    varlen_shape,
     BlockStats,
     BoxStats,
     SELECTORS,

@@ -55,6 +55,14 @@ class rbs_box(ctypes.Structure):
     ]
 
 
+class rbs_batch(ctypes.Structure):
+    _fields_ = [
+        ("n_seqs", ctypes.c_int32),
+        ("seq_tokens", ctypes.POINTER(ctypes.c_int32)),
+    ]
+
+
+RBS_MAX_SEQS = 64
 RBS_SELECTOR_CENTROID, RBS_SELECTOR_FULL_L2, RBS_SELECTOR_BOX = 1, 2, 3
 SELECTORS = {"centroid": RBS_SELECTOR_CENTROID, "full_l2": RBS_SELECTOR_FULL_L2, "box": RBS_SELECTOR_BOX}
 
@@ -93,6 +101,21 @@ def load() -> ctypes.CDLL:
     lib.rbs_select_variant.restype = ctypes.c_int
     lib.rbs_dense_indices.argtypes = [SP, P, P, P]
     lib.rbs_dense_indices.restype = ctypes.c_int
+    BP = ctypes.POINTER(rbs_batch)
+    lib.rbs_varlen_blocks.argtypes = [SP, BP]
+    lib.rbs_varlen_blocks.restype = I32
+    lib.rbs_varlen_index_capacity.argtypes = [SP, BP]
+    lib.rbs_varlen_index_capacity.restype = I64
+    lib.rbs_varlen_summary_bytes.argtypes = [SP, BP]
+    lib.rbs_varlen_summary_bytes.restype = SZ
+    lib.rbs_block_stats_varlen.argtypes = [SP, BP, P, ctypes.POINTER(rbs_stats), P]
+    lib.rbs_block_stats_varlen.restype = ctypes.c_int
+    lib.rbs_select_varlen.argtypes = [SP, BP, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, P, P, P]
+    lib.rbs_select_varlen.restype = ctypes.c_int
+    lib.rbs_sparse_prefill_varlen.argtypes = [SP, BP, P, P, P, P, P, F32, P, P, P]
+    lib.rbs_sparse_prefill_varlen.restype = ctypes.c_int
+    lib.rbs_dense_indices_varlen.argtypes = [SP, BP, P, P, P]
+    lib.rbs_dense_indices_varlen.restype = ctypes.c_int
     lib.rbs_status_str.argtypes = [ctypes.c_int]
     lib.rbs_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -267,4 +290,116 @@ def rbs_dense_indices(shape: rbs_shape, counts=None, indices=None, stream=None, 
         counts, indices = allocate_lists(shape, device)
     _check("rbs_dense_indices", load().rbs_dense_indices(ctypes.byref(shape), _ptr(counts), _ptr(indices),
                                                          _stream(stream)))
+    return counts, indices
+
+
+# ------------------------------------------------------------------ varlen
+
+class Batch:
+    """A batch of independent sequences packed along the token axis (the
+    rbs_*_varlen calls).  Holds the host array that rbs_batch points at."""
+
+    def __init__(self, seq_tokens):
+        self.seq_tokens = [int(x) for x in seq_tokens]
+        self._arr = (ctypes.c_int32 * max(1, len(self.seq_tokens)))(*self.seq_tokens)
+        self.c = rbs_batch(len(self.seq_tokens), self._arr)
+
+    @property
+    def n_seqs(self) -> int:
+        return len(self.seq_tokens)
+
+    @property
+    def n_tokens(self) -> int:
+        return sum(self.seq_tokens)
+
+    def token_offsets(self) -> list:
+        out = [0]
+        for n in self.seq_tokens:
+            out.append(out[-1] + n)
+        return out
+
+    def block_counts(self, block_size: int) -> list:
+        return [-(-n // block_size) for n in self.seq_tokens]
+
+
+def varlen_shape(batch: Batch, n_q_heads: int, n_kv_heads: int, block_size: int, head_dim: int = 128) -> rbs_shape:
+    return make_shape(batch.n_tokens, n_q_heads, n_kv_heads, block_size, head_dim)
+
+
+def rbs_varlen_blocks(shape: rbs_shape, batch: Batch) -> int:
+    return int(load().rbs_varlen_blocks(ctypes.byref(shape), ctypes.byref(batch.c)))
+
+
+def rbs_varlen_index_capacity(shape: rbs_shape, batch: Batch) -> int:
+    return int(load().rbs_varlen_index_capacity(ctypes.byref(shape), ctypes.byref(batch.c)))
+
+
+def rbs_varlen_summary_bytes(shape: rbs_shape, batch: Batch) -> int:
+    return int(load().rbs_varlen_summary_bytes(ctypes.byref(shape), ctypes.byref(batch.c)))
+
+
+def allocate_stats_varlen(shape: rbs_shape, batch: Batch, device="cuda") -> BlockStats:
+    """rbs_stats buffers of a batch: block arrays over all sequences' blocks,
+    quantiles [n_seqs][H_kv][2]."""
+    m, hk, d = rbs_varlen_blocks(shape, batch), shape.n_kv_heads, shape.head_dim
+    nbytes = rbs_varlen_summary_bytes(shape, batch)
+    if m == 0 or nbytes == 0:
+        raise RbsError("rbs_varlen_summary_bytes", RBS_ERR_SHAPE, "invalid shape or batch")
+    f32 = dict(dtype=torch.float32, device=device)
+    return BlockStats(shape, torch.empty((hk, m, d), **f32), torch.empty((hk, m), **f32),
+                      torch.empty((hk, m), **f32), torch.empty((batch.n_seqs, hk, 2), **f32),
+                      torch.empty(nbytes, dtype=torch.uint8, device=device))
+
+
+def allocate_lists_varlen(shape: rbs_shape, batch: Batch, device="cuda"):
+    m, cap = rbs_varlen_blocks(shape, batch), rbs_varlen_index_capacity(shape, batch)
+    if m == 0:
+        raise RbsError("rbs_varlen_blocks", RBS_ERR_SHAPE, "invalid shape or batch")
+    counts = torch.empty((shape.n_q_heads, m), dtype=torch.int32, device=device)
+    indices = torch.empty((shape.n_q_heads, cap), dtype=torch.int32, device=device)
+    return counts, indices
+
+
+def rbs_block_stats_varlen(shape: rbs_shape, batch: Batch, K: torch.Tensor, stats: BlockStats | None = None,
+                           stream=None) -> BlockStats:
+    """Stage 1 for every sequence of a batch (one launch)."""
+    if stats is None:
+        stats = allocate_stats_varlen(shape, batch, K.device)
+    c = stats.as_c()
+    _check("rbs_block_stats_varlen", load().rbs_block_stats_varlen(
+        ctypes.byref(shape), ctypes.byref(batch.c), _ptr(K), ctypes.byref(c), _stream(stream)))
+    return stats
+
+
+def rbs_select_varlen(shape: rbs_shape, batch: Batch, Q: torch.Tensor, stats: BlockStats, tau_base: float,
+                      tau_rescue: float, n_sink: int, n_local: int, n_recent: int, counts=None, indices=None,
+                      stream=None):
+    """Stage 2 for every sequence of a batch (one launch)."""
+    if counts is None or indices is None:
+        counts, indices = allocate_lists_varlen(shape, batch, Q.device)
+    c = stats.as_c()
+    _check("rbs_select_varlen", load().rbs_select_varlen(
+        ctypes.byref(shape), ctypes.byref(batch.c), _ptr(Q), ctypes.byref(c), float(tau_base), float(tau_rescue),
+        int(n_sink), int(n_local), int(n_recent), _ptr(counts), _ptr(indices), _stream(stream)))
+    return counts, indices
+
+
+def rbs_sparse_prefill_varlen(shape: rbs_shape, batch: Batch, Q, K, V, counts, indices, softmax_scale: float = 0.0,
+                              O=None, lse=None, stream=None):
+    """Stage 3 for every sequence of a batch (one launch); returns O."""
+    if O is None:
+        O = torch.empty_like(Q)
+    _check("rbs_sparse_prefill_varlen", load().rbs_sparse_prefill_varlen(
+        ctypes.byref(shape), ctypes.byref(batch.c), _ptr(Q), _ptr(K), _ptr(V), _ptr(counts), _ptr(indices),
+        float(softmax_scale), _ptr(O), _ptr(lse), _stream(stream)))
+    return O
+
+
+def rbs_dense_indices_varlen(shape: rbs_shape, batch: Batch, counts=None, indices=None, stream=None,
+                             device="cuda"):
+    """Full causal lists of every sequence of a batch."""
+    if counts is None or indices is None:
+        counts, indices = allocate_lists_varlen(shape, batch, device)
+    _check("rbs_dense_indices_varlen", load().rbs_dense_indices_varlen(
+        ctypes.byref(shape), ctypes.byref(batch.c), _ptr(counts), _ptr(indices), _stream(stream)))
     return counts, indices

@@ -40,6 +40,35 @@ int check_stats_ptrs(const rbs_stats* st) {
 
 int from_hip(hipError_t e) { return e == hipSuccess ? RBS_OK : RBS_ERR_HIP; }
 
+// Shape rules of a batch (the per-sequence limits are the single-sequence
+// ones), and its sequence table.  T = shape->n_tokens must equal the sum.
+int check_batch(const rbs_shape* s, const rbs_batch* b, rbs::SeqTable* t) {
+  if (s == nullptr || b == nullptr || b->seq_tokens == nullptr) return RBS_ERR_NULL;
+  if (s->head_dim != 128) return RBS_ERR_UNSUPPORTED;
+  if (s->block_size != 64 && s->block_size != 128 && s->block_size != 256) return RBS_ERR_UNSUPPORTED;
+  if (s->n_q_heads < 1 || s->n_kv_heads < 1 || s->n_q_heads % s->n_kv_heads != 0) return RBS_ERR_SHAPE;
+  if (b->n_seqs < 1 || b->n_seqs > RBS_MAX_SEQS) return RBS_ERR_SHAPE;
+  static_assert(RBS_MAX_SEQS == rbs::kMaxSeqs, "sequence table size");
+  *t = rbs::SeqTable{};
+  t->n = b->n_seqs;
+  int64_t tok = 0, blk = 0, cap = 0;
+  for (int q = 0; q < b->n_seqs; ++q) {
+    const int64_t n = b->seq_tokens[q];
+    if (n < 1 || n > kMaxTokens) return RBS_ERR_SHAPE;
+    const int64_t m = (n + s->block_size - 1) / s->block_size;
+    if (m > kMaxBlocks) return RBS_ERR_SHAPE;
+    tok += n;
+    blk += m;
+    cap += m * (m + 1) / 2;
+    t->tok[q + 1] = (int)tok;
+    t->blk[q + 1] = (int)blk;
+    t->cap[q + 1] = cap;
+  }
+  if (tok != s->n_tokens) return RBS_ERR_SHAPE;
+  if ((int64_t)s->n_q_heads * blk > INT32_MAX / 2) return RBS_ERR_SHAPE;
+  return RBS_OK;
+}
+
 // Byte offset of the half-widths in the box summary (centres first, 256-aligned).
 size_t box_half_offset(int n_kv_heads, int n_blocks) {
   return ((size_t)n_kv_heads * n_blocks * 128 * sizeof(_Float16) + 255) & ~(size_t)255;
@@ -281,6 +310,121 @@ int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices,
   const int M = blocks_of(shape);
   return from_hip(rbs::launch_dense_indices(shape->n_q_heads, M, rbs_index_capacity(M), counts, indices,
                                             static_cast<hipStream_t>(stream)));
+}
+
+int32_t rbs_varlen_blocks(const rbs_shape* shape, const rbs_batch* batch) {
+  rbs::SeqTable t;
+  return check_batch(shape, batch, &t) == RBS_OK ? t.blk[t.n] : 0;
+}
+
+int64_t rbs_varlen_index_capacity(const rbs_shape* shape, const rbs_batch* batch) {
+  rbs::SeqTable t;
+  return check_batch(shape, batch, &t) == RBS_OK ? t.cap[t.n] : 0;
+}
+
+size_t rbs_varlen_summary_bytes(const rbs_shape* shape, const rbs_batch* batch) {
+  rbs::SeqTable t;
+  if (check_batch(shape, batch, &t) != RBS_OK) return 0;
+  return rbs::summary_bytes(shape->n_kv_heads, t.blk[t.n]);
+}
+
+int rbs_block_stats_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* K, const rbs_stats* stats,
+                           void* stream) {
+  rbs::SeqTable t;
+  int rc = check_batch(shape, batch, &t);
+  if (rc != RBS_OK) return rc;
+  if (K == nullptr) return RBS_ERR_NULL;
+  if ((rc = check_stats_ptrs(stats)) != RBS_OK) return rc;
+  if (!aligned16(K)) return RBS_ERR_ALIGN;
+  const int M = t.blk[t.n];
+  rbs::StatsArgs a;
+  a.K = static_cast<const uint16_t*>(K);
+  a.n_tokens = shape->n_tokens;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = M;
+  a.centroids = stats->centroids;
+  a.radii = stats->radii;
+  a.beta = stats->beta;
+  a.quantiles = stats->quantiles;
+  a.cent16 = static_cast<_Float16*>(stats->summary);
+  a.uplift = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
+                                      rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  return from_hip(rbs::launch_stats_varlen(a, t, static_cast<hipStream_t>(stream)));
+}
+
+int rbs_select_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* Q, const rbs_stats* stats,
+                      float tau_base, float tau_rescue, int32_t n_sink, int32_t n_local, int32_t n_recent,
+                      int32_t* counts, int32_t* indices, void* stream) {
+  rbs::SeqTable t;
+  int rc = check_batch(shape, batch, &t);
+  if (rc != RBS_OK) return rc;
+  if (Q == nullptr || counts == nullptr || indices == nullptr || stats == nullptr || stats->summary == nullptr)
+    return RBS_ERR_NULL;
+  if (!(tau_base >= 0.f && tau_base <= 1.f) || !(tau_rescue >= 0.f && tau_rescue <= 1.f)) return RBS_ERR_ARG;
+  if (n_sink < 0 || n_local < 1 || n_recent < 0) return RBS_ERR_ARG;
+  if (!aligned16(Q) || !aligned16(counts) || !aligned16(indices) || !aligned16(stats->summary)) return RBS_ERR_ALIGN;
+  const int M = t.blk[t.n];
+  rbs::SelectArgs a;
+  a.Q = static_cast<const uint16_t*>(Q);
+  a.n_tokens = shape->n_tokens;
+  a.n_q_heads = shape->n_q_heads;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = M;
+  a.cent16 = static_cast<const _Float16*>(stats->summary);
+  a.uplift = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
+                                            rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  a.tau_base = tau_base;
+  a.tau_rescue = tau_rescue;
+  a.n_sink = n_sink;
+  a.n_local = n_local;
+  a.n_recent = n_recent;
+  a.counts = counts;
+  a.indices = indices;
+  a.capacity = t.cap[t.n];
+  return from_hip(rbs::launch_select_varlen(a, t, static_cast<hipStream_t>(stream)));
+}
+
+int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* Q, const void* K,
+                              const void* V, const int32_t* counts, const int32_t* indices, float softmax_scale,
+                              void* O, float* lse, void* stream) {
+  rbs::SeqTable t;
+  int rc = check_batch(shape, batch, &t);
+  if (rc != RBS_OK) return rc;
+  if (Q == nullptr || K == nullptr || V == nullptr || counts == nullptr || indices == nullptr || O == nullptr)
+    return RBS_ERR_NULL;
+  if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(counts) || !aligned16(indices) ||
+      !aligned16(O) || (lse != nullptr && !aligned16(lse)))
+    return RBS_ERR_ALIGN;
+  rbs::AttnArgs a;
+  a.Q = static_cast<const uint16_t*>(Q);
+  a.K = static_cast<const uint16_t*>(K);
+  a.V = static_cast<const uint16_t*>(V);
+  a.n_tokens = shape->n_tokens;
+  a.n_q_heads = shape->n_q_heads;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = t.blk[t.n];
+  a.counts = counts;
+  a.indices = indices;
+  a.capacity = t.cap[t.n];
+  a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
+  a.O = static_cast<uint16_t*>(O);
+  a.lse = lse;
+  return from_hip(rbs::launch_attention_varlen(a, t, static_cast<hipStream_t>(stream)));
+}
+
+int rbs_dense_indices_varlen(const rbs_shape* shape, const rbs_batch* batch, int32_t* counts, int32_t* indices,
+                             void* stream) {
+  rbs::SeqTable t;
+  int rc = check_batch(shape, batch, &t);
+  if (rc != RBS_OK) return rc;
+  if (counts == nullptr || indices == nullptr) return RBS_ERR_NULL;
+  if (!aligned16(counts) || !aligned16(indices)) return RBS_ERR_ALIGN;
+  return from_hip(
+      rbs::launch_dense_indices_varlen(shape->n_q_heads, t, counts, indices, static_cast<hipStream_t>(stream)));
 }
 
 const char* rbs_status_str(int status) {

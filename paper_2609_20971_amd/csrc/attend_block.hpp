@@ -90,6 +90,7 @@ struct AttnCore {
   const uint16_t* K;
   const uint16_t* V;
   int N, M, group;
+  int ld;  // tokens between consecutive heads of Q, K, V, O, lse (N, or the batch's total)
   float scale_log2;
   uint16_t* O;
   float* lse;
@@ -98,14 +99,16 @@ struct AttnCore {
 // Attention of query block i of query head h over the count key blocks that
 // list_at(0 .. count - 1) returns (wave-uniform, ascending, each <= i), by the
 // B/32 waves of the calling workgroup.  k_lds and v_lds: B * 256 bytes of LDS
-// each, 256-byte aligned.
-template <int BS, typename ListAt>
+// each, 256-byte aligned.  VARLEN: the head stride c.ld differs from N (a
+// sequence of a batch); otherwise it is N and c.ld is not read.
+template <int BS, bool VARLEN = false, typename ListAt>
 __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, int count, ListAt list_at,
                                              unsigned char* k_lds, unsigned char* v_lds) {
   constexpr int SUB = BS < 128 ? BS : 128;  // keys per softmax step
   constexpr int KT = SUB / 32;              // 32-key MFMA tiles per step
   const uint16_t* __restrict__ Q = c.Q;
   const int N = c.N;
+  const size_t ld = VARLEN ? (size_t)c.ld : (size_t)N;
   const float scale_log2 = c.scale_log2;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
@@ -116,7 +119,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
 
   bf16x8 qreg[8];
   {
-    const uint16_t* qrow = Q + ((size_t)h * N + qpos) * kHeadDim + 8 * half;
+    const uint16_t* qrow = Q + ((size_t)h * ld + qpos) * kHeadDim + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       const uint4 v = q_ok ? *reinterpret_cast<const uint4*>(qrow + 16 * ks) : make_uint4(0u, 0u, 0u, 0u);
@@ -128,8 +131,8 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   // would also wait for them.
   RBS_WAIT_VMCNT(0);
 
-  const uint16_t* kg = c.K + (size_t)g * N * kHeadDim;
-  const uint16_t* vg = c.V + (size_t)g * N * kHeadDim;
+  const uint16_t* kg = c.K + g * ld * kHeadDim;
+  const uint16_t* vg = c.V + g * ld * kHeadDim;
 
   float ms_run = -INFINITY;  // running reference maximum, log2 units
   float l_run = 0.f;         // this lane's share of the softmax denominator
@@ -264,7 +267,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   const float l_tot = l_run + wave_xor_f(l_run, 32);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   if (q_ok) {
-    uint16_t* orow = c.O + ((size_t)h * N + qpos) * kHeadDim;
+    uint16_t* orow = c.O + ((size_t)h * ld + qpos) * kHeadDim;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -278,7 +281,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
         *reinterpret_cast<uint2*>(orow + d0) = packed;
       }
     if (c.lse != nullptr && half == 0)
-      c.lse[(size_t)h * N + qpos] = l_tot > 0.f ? (ms_run + log2f(l_tot)) / kLog2e : -INFINITY;
+      c.lse[(size_t)h * ld + qpos] = l_tot > 0.f ? (ms_run + log2f(l_tot)) / kLog2e : -INFINITY;
   }
 }
 
@@ -302,6 +305,7 @@ inline AttnCore make_attn_core(const AttnArgs& a) {
   c.N = a.n_tokens;
   c.M = a.n_blocks;
   c.group = a.n_q_heads / a.n_kv_heads;
+  c.ld = a.n_tokens;
   c.scale_log2 = a.scale * kLog2e;
   c.O = a.O;
   c.lse = a.lse;

@@ -18,6 +18,36 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   attend_block<BS>(c, h, i, count, [&](int n) __attribute__((always_inline)) { return list[n]; }, k_lds, v_lds);
 }
 
+// Every sequence of a batch in one launch: work items are sequence-major and,
+// inside a sequence, ordered as work_item orders them.
+template <int BS>
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_varlen_kernel(
+    AttnCore c, const int32_t* __restrict__ counts, const int32_t* __restrict__ indices, const SeqTable t) {
+  __shared__ __align__(1024) unsigned char k_lds[BS * 256];
+  __shared__ __align__(1024) unsigned char v_lds[BS * 256];
+  const int hq = gridDim.x / t.blk[t.n];  // query heads
+  const int work = xcd_remap(blockIdx.x, gridDim.x);
+  const int sq = seq_of(t.blk, t.n, work / hq);
+  const int local = work - hq * t.blk[sq];
+  c.N = t.tok[sq + 1] - t.tok[sq];
+  c.M = t.blk[sq + 1] - t.blk[sq];
+  const int per_group = c.M * c.group;
+  const int g = local / per_group;
+  const int rem = local - g * per_group;
+  const int i = c.M - 1 - rem / c.group;
+  const int h = g * c.group + rem % c.group;
+  const size_t tok0 = (size_t)t.tok[sq] * kHeadDim;
+  c.Q += tok0;
+  c.K += tok0;
+  c.V += tok0;
+  c.O += tok0;
+  if (c.lse != nullptr) c.lse += t.tok[sq];
+  const int count = min(max(counts[(size_t)h * t.blk[t.n] + t.blk[sq] + i], 0), i + 1);
+  const int32_t* list = indices + (int64_t)h * t.cap[t.n] + t.cap[sq] + (int64_t)i * (i + 1) / 2;
+  attend_block<BS, true>(c, h, i, count, [&](int n) __attribute__((always_inline)) { return list[n]; }, k_lds,
+                         v_lds);
+}
+
 __global__ void dense_indices_kernel(int M, int64_t capacity, int32_t* __restrict__ counts,
                                      int32_t* __restrict__ indices) {
   const int i = blockIdx.x, h = blockIdx.y;
@@ -40,6 +70,40 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
     default: return hipErrorInvalidValue;
   }
 #undef RBS_ATTN_CASE
+  return hipGetLastError();
+}
+
+__global__ void dense_indices_varlen_kernel(const SeqTable t, int32_t* __restrict__ counts,
+                                            int32_t* __restrict__ indices) {
+  const int bg = blockIdx.x, h = blockIdx.y;
+  const int sq = seq_of(t.blk, t.n, bg);
+  const int i = bg - t.blk[sq];
+  int32_t* out = indices + (int64_t)h * t.cap[t.n] + t.cap[sq] + (int64_t)i * (i + 1) / 2;
+  for (int b = threadIdx.x; b <= i; b += blockDim.x) out[b] = b;
+  if (threadIdx.x == 0) counts[(size_t)h * t.blk[t.n] + bg] = i + 1;
+}
+
+hipError_t launch_attention_varlen(const AttnArgs& a, const SeqTable& t, hipStream_t s) {
+  const dim3 grid(t.blk[t.n] * a.n_q_heads);
+  const AttnCore c = make_attn_core(a);
+#define RBS_ATTN_VARLEN_CASE(BSZ)                                                                              \
+  case BSZ:                                                                                                    \
+    hipLaunchKernelGGL(attn_varlen_kernel<BSZ>, grid, dim3(BSZ * 2), 0, s, c, a.counts, a.indices, t);         \
+    break;
+  switch (a.block_size) {
+    RBS_ATTN_VARLEN_CASE(64)
+    RBS_ATTN_VARLEN_CASE(128)
+    RBS_ATTN_VARLEN_CASE(256)
+    default: return hipErrorInvalidValue;
+  }
+#undef RBS_ATTN_VARLEN_CASE
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_indices_varlen(int n_q_heads, const SeqTable& t, int32_t* counts, int32_t* indices,
+                                       hipStream_t s) {
+  hipLaunchKernelGGL(dense_indices_varlen_kernel, dim3(t.blk[t.n], n_q_heads), dim3(256), 0, s, t, counts,
+                     indices);
   return hipGetLastError();
 }
 

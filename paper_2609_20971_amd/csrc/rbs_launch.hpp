@@ -66,6 +66,39 @@ inline size_t summary_bytes(int n_kv_heads, int n_blocks) {
   return summary_uplift_offset(n_kv_heads, n_blocks) + (size_t)n_kv_heads * n_blocks * sizeof(float);
 }
 
+// A batch of independent sequences packed along the token axis (the varlen
+// entry points).  Sequence s holds tokens tok[s] .. tok[s+1]-1 of every head,
+// blocks blk[s] .. blk[s+1]-1 of the block arrays and index-list slots
+// cap[s] .. cap[s+1]-1 of every query head; a single sequence is {n = 1}.
+constexpr int kMaxSeqs = 64;
+struct SeqTable {
+  int n;
+  int tok[kMaxSeqs + 1];
+  int blk[kMaxSeqs + 1];
+  int64_t cap[kMaxSeqs + 1];
+};
+
+// The sequence holding position x of an offset array off[0..n] (off[0] = 0,
+// ascending): the largest s < n with off[s] <= x.
+__host__ __device__ inline int seq_of(const int* off, int n, int x) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= x) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+inline SeqTable single_sequence(int n_tokens, int n_blocks) {
+  SeqTable t{};
+  t.n = 1;
+  t.tok[1] = n_tokens;
+  t.blk[1] = n_blocks;
+  t.cap[1] = (int64_t)n_blocks * (n_blocks + 1) / 2;
+  return t;
+}
+
 hipError_t launch_stats(const StatsArgs& a, hipStream_t s);
 hipError_t launch_box(const BoxArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
@@ -74,5 +107,13 @@ hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStr
 size_t fused_smem_bytes(int block_size, int n_blocks);
 hipError_t launch_dense_indices(int n_q_heads, int n_blocks, int64_t capacity, int32_t* counts,
                                 int32_t* indices, hipStream_t s);
+
+// Varlen launchers: the Args hold the batch totals (n_tokens = T, n_blocks and
+// capacity = the table's last offsets); every sequence runs in the same launch.
+hipError_t launch_stats_varlen(const StatsArgs& a, const SeqTable& t, hipStream_t s);
+hipError_t launch_select_varlen(const SelectArgs& a, const SeqTable& t, hipStream_t s);
+hipError_t launch_attention_varlen(const AttnArgs& a, const SeqTable& t, hipStream_t s);
+hipError_t launch_dense_indices_varlen(int n_q_heads, const SeqTable& t, int32_t* counts, int32_t* indices,
+                                       hipStream_t s);
 
 }  // namespace rbs

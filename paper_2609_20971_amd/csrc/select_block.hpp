@@ -45,6 +45,8 @@ enum SelectMode {
 struct SelectCore {
   const uint16_t* Q;
   int N, M, group;
+  int ldq;  // tokens between consecutive query heads of Q (N, or the batch's total)
+  int ldm;  // blocks between consecutive heads of the block arrays and counts (M, or the batch's total)
   const _Float16* cent16;     // dual, centroid, full-L2: scaled centroids; box: scaled box centres
   const _Float16* half16;     // box: scaled box half-widths
   const float* uplift;        // dual: r beta log2(e)/sqrt(d)
@@ -93,9 +95,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   const int nb = min(BS, N - row0);
   const int n_cand = i + 1;
   const int n_tiles = (n_cand + kTile - 1) / kTile;
-  const _Float16* cg = c.cent16 + (size_t)g * M * kHeadDim;
-  const _Float16* hg = MODE == kSelectBox ? c.half16 + (size_t)g * M * kHeadDim : nullptr;
-  const float* ug = MODE == kSelectFullL2 ? c.radii + (size_t)g * M : c.uplift + (size_t)g * M;
+  const _Float16* cg = c.cent16 + (size_t)g * c.ldm * kHeadDim;
+  const _Float16* hg = MODE == kSelectBox ? c.half16 + (size_t)g * c.ldm * kHeadDim : nullptr;
+  const float* ug = MODE == kSelectFullL2 ? c.radii + (size_t)g * c.ldm : c.uplift + (size_t)g * c.ldm;
   const float u_scale = MODE == kSelectFullL2 ? kLog2e / sqrtf((float)kHeadDim) : 1.0f;
 
   // ---- Q rows of this wave as MFMA A operands (row = 32*wave + l32).
@@ -105,7 +107,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   f16x8 qabs[MODE == kSelectBox ? 8 : 1];  // |q| for the box half-widths
   float sq = 0.f;
   {
-    const uint16_t* qrow = Q + ((size_t)h * N + row0 + t_local) * kHeadDim + 8 * half;
+    const uint16_t* qrow = Q + ((size_t)h * c.ldq + row0 + t_local) * kHeadDim + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       uint4 v = row_ok ? *reinterpret_cast<const uint4*>(qrow + 16 * ks) : make_uint4(0u, 0u, 0u, 0u);
@@ -339,7 +341,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     total += pass_total;
     __syncthreads();
   }
-  if (tid == 0) c.counts[(size_t)h * M + i] = total;
+  if (tid == 0) c.counts[(size_t)h * c.ldm + i] = total;
   return total;
 }
 
@@ -349,6 +351,8 @@ inline SelectCore make_select_core(const SelectArgs& a) {
   c.N = a.n_tokens;
   c.M = a.n_blocks;
   c.group = a.n_q_heads / a.n_kv_heads;
+  c.ldq = a.n_tokens;
+  c.ldm = a.n_blocks;
   c.cent16 = a.cent16;
   c.half16 = a.half16;
   c.uplift = a.uplift;

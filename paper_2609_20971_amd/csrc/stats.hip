@@ -72,8 +72,10 @@ __device__ void radix_select4(const uint32_t* keys, int n, int rank0, int rank1,
   __syncthreads();
 }
 
+// Block blockIdx.x of all the sequences' blocks (sequence s owns blocks
+// t.blk[s] .. t.blk[s+1]-1 and tokens t.tok[s] .. t.tok[s+1]-1), KV head blockIdx.y.
 template <int BS>
-__global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __restrict__ K, int N, int M,
+__global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __restrict__ K, const SeqTable t,
                                                              float* __restrict__ centroids,
                                                              float* __restrict__ radii,
                                                              _Float16* __restrict__ cent16, float sel_scale) {
@@ -81,13 +83,16 @@ __global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __
   __shared__ float red[4][kHeadDim];
   __shared__ float red_r[4];
 
-  const int b = blockIdx.x, g = blockIdx.y;
+  const int bg = blockIdx.x, g = blockIdx.y;
+  const int sq = seq_of(t.blk, t.n, bg);
+  const int b = bg - t.blk[sq];
+  const int T = t.tok[t.n], M = t.blk[t.n];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int chunk = tid & 15;  // 8 consecutive dims: 8*chunk .. 8*chunk+7
   const int rg = tid >> 4;     // row group: rows rg, rg+16, ...
   const int row0 = b * BS;
-  const int nb = min(BS, N - row0);
-  const uint16_t* kb = K + ((size_t)g * N + row0) * kHeadDim + chunk * 8;
+  const int nb = min(BS, t.tok[sq + 1] - t.tok[sq] - row0);
+  const uint16_t* kb = K + ((size_t)g * T + t.tok[sq] + row0) * kHeadDim + chunk * 8;
 
   uint4 raw[kRowsPerThread];
 #pragma unroll
@@ -146,7 +151,7 @@ __global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __
   if (lane == 0) red_r[wave] = best;
   __syncthreads();
 
-  const size_t blk = (size_t)g * M + b;
+  const size_t blk = (size_t)g * M + bg;
   if (tid < 16) {
     float4* dst = reinterpret_cast<float4*>(centroids + blk * kHeadDim + chunk * 8);
     dst[0] = make_float4(c[0], c[1], c[2], c[3]);
@@ -232,7 +237,9 @@ __global__ __launch_bounds__(kStatsThreads) void box_kernel(const uint16_t* __re
   }
 }
 
-__global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __restrict__ radii, int M,
+// KV head blockIdx.x of sequence blockIdx.y: the quantiles of that sequence's
+// radii (its own prompt's distribution).
+__global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __restrict__ radii, const SeqTable t,
                                                                 float* __restrict__ beta,
                                                                 float* __restrict__ quantiles,
                                                                 float* __restrict__ uplift, float sel_scale) {
@@ -241,8 +248,10 @@ __global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __
   __shared__ uint32_t sel_prefix[4];
   __shared__ int sel_remaining[4];
   __shared__ uint32_t sel_out[4];
-  const int g = blockIdx.x, tid = threadIdx.x;
-  const float* rg_radii = radii + (size_t)g * M;
+  const int g = blockIdx.x, sq = blockIdx.y, tid = threadIdx.x;
+  const int M = t.blk[sq + 1] - t.blk[sq];
+  const size_t base = (size_t)g * t.blk[t.n] + t.blk[sq];
+  const float* rg_radii = radii + base;
   for (int e = tid; e < M; e += kStatsThreads) keys[e] = __float_as_uint(rg_radii[e]);
   __syncthreads();
 
@@ -265,22 +274,23 @@ __global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __
     float bt;
     if (spread) bt = fminf(fmaxf((r - r_low) / span, 0.0f), 1.0f);
     else bt = r > r_low ? 1.0f : 0.0f;
-    beta[(size_t)g * M + e] = bt;
-    uplift[(size_t)g * M + e] = r * bt * sel_scale;
+    beta[base + e] = bt;
+    uplift[base + e] = r * bt * sel_scale;
   }
   if (tid == 0) {
-    quantiles[2 * g + 0] = r_low;
-    quantiles[2 * g + 1] = r_high;
+    const size_t q = (size_t)sq * gridDim.x + g;
+    quantiles[2 * q + 0] = r_low;
+    quantiles[2 * q + 1] = r_high;
   }
 }
 
-hipError_t launch_stats(const StatsArgs& a, hipStream_t s) {
-  const dim3 grid(a.n_blocks, a.n_kv_heads);
+hipError_t launch_stats_varlen(const StatsArgs& a, const SeqTable& t, hipStream_t s) {
+  const dim3 grid(t.blk[t.n], a.n_kv_heads);
   const float sel_scale = kLog2e / sqrtf((float)kHeadDim);
-#define RBS_STATS_CASE(BSZ)                                                                               \
-  case BSZ:                                                                                               \
-    hipLaunchKernelGGL(stats_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, a.n_tokens, a.n_blocks,   \
-                       a.centroids, a.radii, a.cent16, sel_scale);                                        \
+#define RBS_STATS_CASE(BSZ)                                                                                 \
+  case BSZ:                                                                                                 \
+    hipLaunchKernelGGL(stats_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, t, a.centroids, a.radii,    \
+                       a.cent16, sel_scale);                                                                \
     break;
   switch (a.block_size) {
     RBS_STATS_CASE(64)
@@ -291,9 +301,13 @@ hipError_t launch_stats(const StatsArgs& a, hipStream_t s) {
 #undef RBS_STATS_CASE
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(quantile_kernel, dim3(a.n_kv_heads), dim3(kStatsThreads), 0, s, a.radii, a.n_blocks, a.beta,
+  hipLaunchKernelGGL(quantile_kernel, dim3(a.n_kv_heads, t.n), dim3(kStatsThreads), 0, s, a.radii, t, a.beta,
                      a.quantiles, a.uplift, sel_scale);
   return hipGetLastError();
+}
+
+hipError_t launch_stats(const StatsArgs& a, hipStream_t s) {
+  return launch_stats_varlen(a, single_sequence(a.n_tokens, a.n_blocks), s);
 }
 
 hipError_t launch_box(const BoxArgs& a, hipStream_t s) {

@@ -12,6 +12,8 @@ from .workloads import (
     workload,
     make_inputs,
     layer_schedule,
+    batch_workloads,
+    make_batch_inputs,
 )
 
 __all__ = [
@@ -23,4 +25,6 @@ __all__ = [
     "workload",
     "make_inputs",
     "layer_schedule",
+    "batch_workloads",
+    "make_batch_inputs",
 ]

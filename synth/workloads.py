@@ -216,3 +216,25 @@ def make_inputs(w: Workload, threads: int | None = None) -> dict:
 
 def as_f32(bits: np.ndarray) -> np.ndarray:
     return f32_from_bf16_bits(bits)
+
+
+def batch_workloads(base: Workload, seq_tokens, needles_per_2k: float | None = None) -> list:
+    """One Workload per sequence of a batch: the base layer's heads and
+    generator, the sequence's own length and seed (base.seed + s), and a needle
+    count scaled to its length (needles_per_2k per 2048 tokens when given,
+    else the base count)."""
+    out = []
+    for s, n in enumerate(seq_tokens):
+        nd = base.needles_per_kv_head if needles_per_2k is None else int(round(needles_per_2k * n / 2048))
+        out.append(base.with_(name=f"{base.name}-seq{s}", seq_len=int(n), seed=base.seed + s,
+                              needles_per_kv_head=nd))
+    return out
+
+
+def make_batch_inputs(workloads: list, threads: int | None = None) -> dict:
+    """Inputs of every sequence (make_inputs), packed along the token axis:
+    {"q", "k", "v"} as [H][sum of N][d] bf16 bit arrays, plus "seq_tokens" and
+    each sequence's "needles"."""
+    parts = [make_inputs(w, threads) for w in workloads]
+    return {x: np.concatenate([p[x] for p in parts], axis=1) for x in ("q", "k", "v")} | {
+        "seq_tokens": [w.seq_len for w in workloads], "needles": [p["needles"] for p in parts]}

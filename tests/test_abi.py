@@ -196,3 +196,73 @@ def test_select_variant_validation():
     assert _variant(lib, s, st, bx, local=0) == 4
     bad = rbs.make_shape(1024, 3, 2, 64)
     assert _variant(lib, bad, st, bx) == 2
+
+
+def _varlen_calls(lib, s, b, st, ptr=FAKE):
+    """Status of every varlen call on (shape, batch) with the given pointers."""
+    bb = ctypes.byref(b.c) if b is not None else None
+    return [
+        lib.rbs_block_stats_varlen(ctypes.byref(s), bb, ptr, ctypes.byref(st), None),
+        lib.rbs_select_varlen(ctypes.byref(s), bb, ptr, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, ptr, ptr, None),
+        lib.rbs_sparse_prefill_varlen(ctypes.byref(s), bb, ptr, ptr, ptr, ptr, ptr, 0.0, ptr, None, None),
+        lib.rbs_dense_indices_varlen(ctypes.byref(s), bb, ptr, ptr, None),
+    ]
+
+
+def test_varlen_sizes():
+    rbs, _ = _lib()
+    b = rbs.Batch([700, 1536, 64, 2049, 1])
+    s = rbs.varlen_shape(b, 4, 2, 128)
+    m = [6, 12, 1, 17, 1]
+    assert rbs.rbs_varlen_blocks(s, b) == sum(m)
+    assert rbs.rbs_varlen_index_capacity(s, b) == sum(x * (x + 1) // 2 for x in m)
+    assert rbs.rbs_varlen_summary_bytes(s, b) == 2 * 37 * 256 + 2 * 37 * 4  # = rbs_summary_bytes at M = 37
+    one = rbs.Batch([4096])
+    s1 = rbs.varlen_shape(one, 4, 2, 128)
+    assert rbs.rbs_varlen_summary_bytes(s1, one) == rbs.rbs_summary_bytes(s1)
+    assert rbs.rbs_varlen_index_capacity(s1, one) == rbs.rbs_index_capacity(32)
+
+
+@pytest.mark.parametrize("seqs,total,code", [
+    ([], None, 2),                      # no sequence
+    ([10] * 65, None, 2),               # more than RBS_MAX_SEQS
+    ([10, 0, 5], None, 2),              # an empty sequence
+    ([10, 262145], None, 2),            # a sequence over the token limit
+    ([100, 200], 301, 2),               # lengths do not add up to n_tokens
+])
+def test_varlen_batch_validation(seqs, total, code):
+    rbs, lib = _lib()
+    b = rbs.Batch(seqs)
+    s = rbs.make_shape(total if total is not None else max(1, sum(seqs)), 4, 2, 64)
+    st = _stats(rbs)
+    assert _varlen_calls(lib, s, b, st) == [code] * 4
+    assert rbs.rbs_varlen_blocks(s, b) == 0 and rbs.rbs_varlen_summary_bytes(s, b) == 0
+
+
+def test_varlen_null_unsupported_and_alignment():
+    rbs, lib = _lib()
+    b = rbs.Batch([100, 200])
+    s = rbs.varlen_shape(b, 4, 2, 64)
+    st = _stats(rbs)
+    assert _varlen_calls(lib, s, None, st) == [1] * 4           # no batch
+    nb = rbs.Batch([100, 200])
+    nb.c.seq_tokens = ctypes.POINTER(ctypes.c_int32)()           # NULL host array
+    assert _varlen_calls(lib, s, nb, st) == [1] * 4
+    assert _varlen_calls(lib, s, b, st, ptr=None) == [1] * 4
+    assert _varlen_calls(lib, s, b, st, ptr=MIS) == [5] * 4
+    bad = rbs.varlen_shape(b, 4, 2, 96)
+    assert _varlen_calls(lib, bad, b, st) == [3] * 4
+    assert lib.rbs_select_varlen(ctypes.byref(s), ctypes.byref(b.c), FAKE, ctypes.byref(st), 1.5, 0.9, 1, 1, 0,
+                                 FAKE, FAKE, None) == 4
+    assert lib.rbs_sparse_prefill_varlen(ctypes.byref(s), ctypes.byref(b.c), FAKE, FAKE, FAKE, FAKE, FAKE,
+                                         float("nan"), FAKE, None, None) == 4
+
+
+def test_varlen_largest_batch_passes_validation():
+    rbs, lib = _lib()
+    b = rbs.Batch([262144] * 2 + [1] * 62)  # RBS_MAX_SEQS sequences, two at the token limit
+    s = rbs.varlen_shape(b, 1, 1, 64)
+    st = _stats(rbs)
+    # Passes the shape and batch checks, stops at the NULL key pointer.
+    assert lib.rbs_block_stats_varlen(ctypes.byref(s), ctypes.byref(b.c), None, ctypes.byref(st), None) == 1
+    assert rbs.rbs_varlen_blocks(s, b) == 2 * 4096 + 62

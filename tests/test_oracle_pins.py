@@ -471,3 +471,101 @@ def test_variant_rows_keep_forced_blocks_and_threshold_extremes():
     box_all = oracle.select_variant(Q, C, R, Vc, Hw, B, "box", 1.0, 0, 1, 0)
     assert all(r["final"].all() for r in box_all.values())
     assert len(box_all) == M
+
+
+# ---------------------------------------------------------------- batches
+# App. "Additional A100 System Measurements", prompt throughput: batched
+# prompts are independent causal sequences, none concatenated into another.
+
+def _batch(lengths, H_q=2, H_kv=1, d=8, seed=0, noise=None):
+    rng = np.random.default_rng(seed)
+    T = sum(lengths)
+    Q = rng.standard_normal((H_q, T, d))
+    K = rng.standard_normal((H_kv, T, d)) + 2.0
+    if noise is not None:  # per-sequence key spread, so radius distributions differ
+        off = oracle.batch_offsets(lengths)
+        for s, sc in enumerate(noise):
+            K[:, off[s]:off[s + 1]] = 2.0 + sc * rng.standard_normal((H_kv, lengths[s], d)) * \
+                rng.lognormal(0.0, 0.7, size=(H_kv, lengths[s], 1))
+    V = rng.standard_normal((H_kv, T, d))
+    return Q, K, V
+
+
+def _all_rows(result):
+    return {s: {h: {i: np.nonzero(r["final"])[0].tolist() for (hh, i), r in rows.items() if hh == h}
+                for h in sorted({hh for (hh, _) in rows})}
+            for s, rows in result.items()}
+
+
+def test_batch_of_one_is_the_single_sequence():
+    Q, K, V = _batch([75])
+    C, R = oracle.block_stats(K, 16)
+    beta, rq = oracle.rescue_coefficients(R)
+    Cb, Rb, betab, rqb = oracle.batch_block_stats(K, [75], 16)
+    assert np.array_equal(C, Cb) and np.array_equal(R, Rb) and np.array_equal(beta, betab)
+    assert np.array_equal(rq, rqb[0])
+    single = oracle.select(Q, C, R, beta, 16, 0.9, 0.95, 1, 1, 0)
+    batched = oracle.batch_select(Q, K, [75], 16, 0.9, 0.95, 1, 1, 0)[0]
+    assert single.keys() == batched.keys()
+    assert all(np.array_equal(single[k]["final"], batched[k]["final"]) for k in single)
+
+
+def test_batch_sequences_are_independent():
+    lengths = [50, 70, 33]
+    Q, K, V = _batch(lengths, seed=1)
+    Q2, K2, V2 = Q.copy(), K.copy(), V.copy()
+    off = oracle.batch_offsets(lengths)
+    rng = np.random.default_rng(9)
+    for X in (Q2, K2, V2):  # change sequence 1 only
+        X[:, off[1]:off[2]] += rng.standard_normal(X[:, off[1]:off[2]].shape)
+    a = oracle.batch_select(Q, K, lengths, 16, 0.9, 0.95, 1, 1, 0)
+    b = oracle.batch_select(Q2, K2, lengths, 16, 0.9, 0.95, 1, 1, 0)
+    oa = oracle.batch_attention_on_mask(Q, K, V, lengths, 16, _all_rows(a))
+    ob = oracle.batch_attention_on_mask(Q2, K2, V2, lengths, 16, _all_rows(a))
+    for s in (0, 2):
+        for k in a[s]:
+            assert np.array_equal(a[s][k]["log_s_base"], b[s][k]["log_s_base"])
+            assert np.array_equal(a[s][k]["final"], b[s][k]["final"])
+        for h in oa[s]:
+            for i in oa[s][h]:
+                assert np.array_equal(oa[s][h][i], ob[s][h][i])
+    assert any(not np.array_equal(a[1][k]["log_s_base"], b[1][k]["log_s_base"]) for k in a[1])
+    Ma = oracle.batch_block_stats(K, lengths, 16)
+    Mb = oracle.batch_block_stats(K2, lengths, 16)
+    m = [0] + list(np.cumsum([-(-n // 16) for n in lengths]))
+    for s in (0, 2):
+        assert np.array_equal(Ma[1][:, m[s]:m[s + 1]], Mb[1][:, m[s]:m[s + 1]])
+        assert np.array_equal(Ma[3][s], Mb[3][s])
+
+
+def test_batch_at_full_selection_is_each_sequence_dense_attention():
+    lengths = [40, 29, 57]
+    Q, K, V = _batch(lengths, H_q=2, H_kv=1, seed=2)
+    sel = oracle.batch_select(Q, K, lengths, 16, 0.0, 0.0, 0, 1, 0)
+    for s, rows in sel.items():
+        for (h, i), r in rows.items():
+            assert r["final"].all()  # alpha = 0 keeps every causal block
+    out = oracle.batch_attention_on_mask(Q, K, V, lengths, 16, _all_rows(sel))
+    Qs, Ks, Vs = (oracle.batch_sequences(X, lengths) for X in (Q, K, V))
+    off = oracle.batch_offsets(lengths)
+    for s in range(len(lengths)):
+        for h in range(2):
+            got = np.concatenate([out[s][h][i] for i in sorted(out[s][h])])
+            assert np.allclose(got, oracle.dense_causal_attention(Qs[s][h], Ks[s][0], Vs[s][0]), atol=1e-12)
+            if s > 0:  # the concatenated sequence would also attend to earlier prompts
+                cat = oracle.dense_causal_attention(Q[h, :off[s + 1]], K[0, :off[s + 1]], V[0, :off[s + 1]])
+                assert not np.allclose(got, cat[off[s]:])
+
+
+def test_block_aligned_batch_shares_centroids_but_not_beta_with_the_concatenation():
+    lengths = [64, 96, 48]
+    _, K, _ = _batch(lengths, H_q=1, H_kv=1, seed=3, noise=[0.3, 1.0, 3.0])
+    Cb, Rb, betab, rqb = oracle.batch_block_stats(K, lengths, 16)
+    Cc, Rc = oracle.block_stats(K, 16)
+    assert np.array_equal(Cb, Cc) and np.array_equal(Rb, Rc)   # same block partition
+    beta_cat, _ = oracle.rescue_coefficients(Rc)
+    assert not np.allclose(betab, beta_cat)                    # per-prompt quantiles differ
+    off = [0, 4, 10, 13]
+    for s in range(3):
+        beta_s, rq_s = oracle.rescue_coefficients(Rc[:, off[s]:off[s + 1]])
+        assert np.array_equal(betab[:, off[s]:off[s + 1]], beta_s) and np.array_equal(rqb[s], rq_s)
