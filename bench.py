@@ -57,6 +57,16 @@ def parse():
                    help="sampled (head, query block) rows for the attention-mass coverage")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a 1 GiB device copy (for scaling HBM counters)")
+    p.add_argument("--batch", type=int, default=0,
+                   help="instead of the benchmark line: a batch of this many independent sequences of the "
+                        "workload's length through the varlen calls, against the same sequences one call "
+                        "at a time and against the dense path at the same batch")
+    p.add_argument("--batch-lens", default=None,
+                   help="comma-separated sequence lengths for the batch mode (overrides --batch)")
+    p.add_argument("--layer-sweep", type=int, default=0,
+                   help="instead of the benchmark line: this many layers of the 128K layer schedule "
+                        "(per-layer key noise and needle counts), per-layer density and times, sparse vs "
+                        "dense, serial and with the next layer's stats and selection on a second stream")
     return p.parse_args()
 
 
@@ -143,6 +153,10 @@ def main():
 
     if args.selector_study:
         return selector_study(args)
+    if args.batch or args.batch_lens:
+        return batch_bench(args)
+    if args.layer_sweep:
+        return layer_sweep(args)
     w = workload(args.workload or "qwen3-30b-a3b-128k")
     _log(f"[bench] workload {w.name}: N={w.seq_len} Hq={w.n_q_heads} Hkv={w.n_kv_heads} B={w.block_size}")
     t0 = time.perf_counter()
@@ -436,6 +450,216 @@ def selector_study(args):
         points.append(evaluate(name, param, None))
     print(json.dumps({"study": "selector comparison", "workload": w.name, "needle_norm": w.needle_norm,
                       "rows": len(rows), "needles": len(inp["needles"]), "points": points}), flush=True)
+
+
+def _upload(torch, np, bits, dev):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+
+def _events(torch, n):
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+def batch_bench(args):
+    """A batch of independent sequences (the paper's batched prompt throughput:
+    separate causal sequences, normalized to dense at the same batch): the
+    varlen calls (one launch per stage for the whole batch) against the same
+    sequences run one single-sequence call at a time, and the dense path of
+    the varlen attention.  One JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_2609_20971_amd as rbs
+    from synth import workload, batch_workloads, make_batch_inputs
+
+    w = workload(args.workload or "qwen3-30b-a3b-128k")
+    lens = ([int(x) for x in args.batch_lens.split(",")] if args.batch_lens else [w.seq_len] * args.batch)
+    per_2k = w.needles_per_kv_head * 2048 / w.seq_len
+    t0 = time.perf_counter()
+    inp = make_batch_inputs(batch_workloads(w, lens, needles_per_2k=per_2k))
+    _log(f"[batch] {w.name} x {len(lens)}: lengths {lens}; inputs in {time.perf_counter() - t0:.1f}s")
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(0)
+    Q, K, V = (_upload(torch, np, inp[x], dev) for x in ("q", "k", "v"))
+    batch = rbs.Batch(lens)
+    shape = rbs.varlen_shape(batch, w.n_q_heads, w.n_kv_heads, w.block_size)
+    stats = rbs.allocate_stats_varlen(shape, batch, dev)
+    counts, indices = rbs.allocate_lists_varlen(shape, batch, dev)
+    O = torch.empty_like(Q)
+    stream = torch.cuda.current_stream()
+    tb, tr, sink, local, recent = w.tau_base, w.tau_rescue, w.n_sink, w.n_local, w.n_recent
+
+    def varlen_step():
+        rbs.rbs_block_stats_varlen(shape, batch, K, stats, stream=stream)
+        rbs.rbs_select_varlen(shape, batch, Q, stats, tb, tr, sink, local, recent, counts, indices, stream=stream)
+        rbs.rbs_sparse_prefill_varlen(shape, batch, Q, K, V, counts, indices, 0.0, O, stream=stream)
+
+    # The same sequences one at a time through the single-sequence calls, on
+    # views of the packed tensors copied out once (outside the timed region).
+    off = batch.token_offsets()
+    singles = []
+    for s_, n in enumerate(lens):
+        sh = rbs.make_shape(n, w.n_q_heads, w.n_kv_heads, w.block_size)
+        q, k, v = (X[:, off[s_]:off[s_ + 1]].contiguous() for X in (Q, K, V))
+        singles.append((sh, q, k, v, rbs.BlockStats.allocate(sh, dev), *rbs.allocate_lists(sh, dev),
+                        torch.empty_like(q)))
+
+    def single_step():
+        for (sh, q, k, v, st, c, ix, o) in singles:
+            rbs.rbs_block_stats(sh, k, st, stream=stream)
+            rbs.rbs_select(sh, q, st, tb, tr, sink, local, recent, c, ix, stream=stream)
+            rbs.rbs_sparse_prefill(sh, q, k, v, c, ix, 0.0, o, stream=stream)
+
+    dcounts, dindices = rbs.allocate_lists_varlen(shape, batch, dev)
+    rbs.rbs_dense_indices_varlen(shape, batch, dcounts, dindices, stream=stream)
+
+    def dense_step():
+        rbs.rbs_sparse_prefill_varlen(shape, batch, Q, K, V, dcounts, dindices, 0.0, O, stream=stream)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a, b = _events(torch, 2)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    reps = max(1, args.steps)
+    t_var = timed(varlen_step, reps)
+    _log(f"[batch] varlen: {t_var:.3f} ms per batch")
+    t_single = timed(single_step, reps)
+    _log(f"[batch] one sequence at a time: {t_single:.3f} ms per batch")
+    t_dense = timed(dense_step, max(1, args.dense_reps))
+    _log(f"[batch] dense attention (varlen): {t_dense:.3f} ms per batch")
+    csum = int(counts.sum().item())
+    pairs = w.n_q_heads * sum(m * (m + 1) // 2 for m in batch.block_counts(w.block_size))
+    tokens = batch.n_tokens
+    print(json.dumps({
+        "mode": "batch", "workload": w.name, "seq_tokens": lens, "n_seqs": len(lens), "dtype": "bf16",
+        "data": "synthetic", "steps": reps,
+        "varlen_ms_per_batch": round(t_var, 4), "single_calls_ms_per_batch": round(t_single, 4),
+        "dense_attn_ms_per_batch": round(t_dense, 4),
+        "prompt_tokens_per_s": round(tokens / (t_var * 1e-3), 1),
+        "throughput_vs_dense": round(t_dense / t_var, 3),
+        "varlen_vs_single_calls": round(t_single / t_var, 3),
+        "density": round(csum / pairs, 6),
+    }), flush=True)
+
+
+def layer_sweep(args):
+    """The 48-layer prefill sweep of the 128K layer (per-layer key noise and
+    needle counts from the seeded layer schedule, so density varies by layer):
+    per-layer density, sparse path and dense attention times, totals; then the
+    whole sweep again with layer l+1's statistics and selection issued on a
+    second stream while layer l's attention runs.  One JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_2609_20971_amd as rbs
+    from synth import layer_schedule, make_inputs
+
+    layers = layer_schedule(args.layer_sweep)
+    w0 = layers[0]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(0)
+    shape = rbs.make_shape(w0.seq_len, w0.n_q_heads, w0.n_kv_heads, w0.block_size)
+    t0 = time.perf_counter()
+    data = []
+    for lw in layers:  # every layer's Q, K, V resident in HBM (about 1.3 GB per layer)
+        inp = make_inputs(lw)
+        data.append(tuple(_upload(torch, np, inp[x], dev) for x in ("q", "k", "v")))
+        del inp
+        _log(f"[sweep] {lw.name}: key sigma {lw.key_noise[0][1]:.3f}, {lw.needles_per_kv_head} needles / KV head "
+             f"({time.perf_counter() - t0:.0f}s)")
+    main_s = torch.cuda.current_stream()
+    side_s = torch.cuda.Stream()
+    sets = [(rbs.BlockStats.allocate(shape, dev), *rbs.allocate_lists(shape, dev)) for _ in range(2)]
+    O = torch.empty_like(data[0][0])
+    tb, tr, sink, local, recent = w0.tau_base, w0.tau_rescue, w0.n_sink, w0.n_local, w0.n_recent
+
+    def select_layer(l, st, c, ix, stream):
+        Q, K, _ = data[l]
+        rbs.rbs_block_stats(shape, K, st, stream=stream)
+        rbs.rbs_select(shape, Q, st, tb, tr, sink, local, recent, c, ix, stream=stream)
+
+    # Serial pass, stage events per layer.
+    st, c, ix = sets[0]
+    select_layer(0, st, c, ix, main_s)
+    rbs.rbs_sparse_prefill(shape, *data[0], c, ix, 0.0, O, stream=main_s)
+    torch.cuda.synchronize()
+    ev = [_events(torch, 3) for _ in layers]
+    dens = []
+    t_start = time.perf_counter()
+    for l in range(len(layers)):
+        ev[l][0].record(main_s)
+        select_layer(l, st, c, ix, main_s)
+        ev[l][1].record(main_s)
+        rbs.rbs_sparse_prefill(shape, *data[l], c, ix, 0.0, O, stream=main_s)
+        ev[l][2].record(main_s)
+        dens.append(c.sum())
+    torch.cuda.synchronize()
+    serial_wall = (time.perf_counter() - t_start) * 1e3
+    sel_ms = [e[0].elapsed_time(e[1]) for e in ev]
+    att_ms = [e[1].elapsed_time(e[2]) for e in ev]
+    pairs = w0.n_q_heads * w0.n_blocks * (w0.n_blocks + 1) // 2
+    density = [float(d.item()) / pairs for d in dens]
+    _log(f"[sweep] serial: {sum(sel_ms) + sum(att_ms):.1f} ms ({serial_wall:.1f} ms wall)")
+
+    # Dense attention per layer.
+    dc, di = rbs.rbs_dense_indices(shape, device=dev)
+    dense_ms = []
+    for l in range(len(layers)):
+        a, b = _events(torch, 2)
+        a.record(main_s)
+        rbs.rbs_sparse_prefill(shape, *data[l], dc, di, 0.0, O, stream=main_s)
+        b.record(main_s)
+        b.synchronize()
+        dense_ms.append(a.elapsed_time(b))
+    _log(f"[sweep] dense attention: {sum(dense_ms):.1f} ms")
+    del dc, di
+
+    # Pipelined pass: layer l+1's stats and selection on the side stream while
+    # layer l's attention runs on the main stream (double-buffered summaries
+    # and lists; events order every hand-off).
+    ready = [torch.cuda.Event() for _ in layers]
+    done = [torch.cuda.Event() for _ in layers]
+    torch.cuda.synchronize()
+    a, b = _events(torch, 2)
+    a.record(main_s)
+    side_s.wait_event(a)
+    select_layer(0, *sets[0], side_s)
+    ready[0].record(side_s)
+    for l in range(len(layers)):
+        if l + 1 < len(layers):
+            if l >= 1:
+                side_s.wait_event(done[l - 1])  # layer l-1's attention has read set (l+1) % 2
+            select_layer(l + 1, *sets[(l + 1) % 2], side_s)
+            ready[l + 1].record(side_s)
+        st, c, ix = sets[l % 2]
+        main_s.wait_event(ready[l])
+        rbs.rbs_sparse_prefill(shape, *data[l], c, ix, 0.0, O, stream=main_s)
+        done[l].record(main_s)
+    b.record(main_s)
+    torch.cuda.synchronize()
+    piped_ms = a.elapsed_time(b)
+    _log(f"[sweep] pipelined: {piped_ms:.1f} ms")
+    total_sparse = sum(sel_ms) + sum(att_ms)
+    print(json.dumps({
+        "mode": "layer_sweep", "layers": len(layers), "workload": w0.name.rsplit("-layer", 1)[0],
+        "dtype": "bf16", "data": "synthetic",
+        "density": [round(x, 5) for x in density],
+        "select_ms": [round(x, 3) for x in sel_ms], "attn_ms": [round(x, 3) for x in att_ms],
+        "dense_attn_ms": [round(x, 3) for x in dense_ms],
+        "total_sparse_ms": round(total_sparse, 2), "total_dense_attn_ms": round(sum(dense_ms), 2),
+        "speedup_vs_dense": round(sum(dense_ms) / total_sparse, 3),
+        "pipelined_total_ms": round(piped_ms, 2),
+        "mean_density": round(float(np.mean(density)), 5),
+    }), flush=True)
 
 
 # Sources each kernel is built from (their joint hash identifies the kernel in

@@ -207,6 +207,18 @@ def test_qwen3_32b_64k_sampled():
     _full_check(w, select_rows=rows, attn_rows=attn)
 
 
+@pytest.mark.slow
+@pytest.mark.parametrize("layer", [0, 47])
+def test_layer_schedule_layers_sampled(layer):
+    """Layers of the 48-layer 128K sweep (per-layer key noise and needle
+    counts); sampled rows."""
+    from synth import layer_schedule
+    w = layer_schedule(48)[layer]
+    M = w.n_blocks
+    rows = H.sample_rows(w.n_q_heads, M, 16, seed=10 + layer, include=[(3, M - 1), (30, 512)])
+    _full_check(w, select_rows=rows, attn_rows=rows[:6])
+
+
 def _fused_matches_two_calls(w: Workload, tau=None, forced=None):
     """The fused entry point against rbs_select + rbs_sparse_prefill on the same
     inputs: lists, O and LSE bit for bit."""
