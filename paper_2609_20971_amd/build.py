@@ -32,6 +32,12 @@ FLAGS = [
 ]
 
 
+# Per-source additions.  The selector keeps its MFMA results in ordinary
+# VGPRs: with the accumulation registers (AGPRs) every tile copied its 16
+# results out twice, and the unified register count cost a wave per SIMD.
+EXTRA_FLAGS = {"select.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _run(cmd):
     proc = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     # The host pass does not know the packed-fp32 feature and says so; drop that line.
@@ -49,7 +55,7 @@ def build(verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD_DIR, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmds.append([HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([HIPCC, *FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
     with ThreadPoolExecutor(len(cmds)) as ex:
         for text in ex.map(_run, cmds):
             if verbose and text.strip():

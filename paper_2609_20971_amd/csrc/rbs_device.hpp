@@ -30,6 +30,18 @@ __device__ __forceinline__ void unpack8(const uint4& v, float* f) {
 
 __device__ __forceinline__ float wave_xor_f(float v, int mask) { return __shfl_xor(v, mask, kWave); }
 
+// x combined with x of lane l ^ 32 through gfx950's half-wave lane swap (a
+// VALU op, no LDS round trip).  The swap returns, in lane l < 32, x[l + 32]
+// and x[l]; in lane l >= 32, x[l] and x[l - 32]: both operands in every lane.
+__device__ __forceinline__ float half_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float half_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // 32x32x16 MFMA wrappers: D = A(32x16) B(16x32) + C.

@@ -79,8 +79,8 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   // Layout: cbuf[2][32 rows][16 chunks of 8 f16] (| hbuf[2][32][16], box) | stage[2][NW][32][4] | nq[BS] |
   // L_base[M] | L_res[M] | red_f[2 NW] | red_i[NW] (| cnt[2][NW], box)
   constexpr int kTileBufs = MODE == kSelectBox ? 4 : 2;
-  uint4* cbuf = reinterpret_cast<uint4*>(smem_raw);
-  uint4* hbuf = cbuf + 2 * kTile * 16;
+  f16x8* cbuf = reinterpret_cast<f16x8*>(smem_raw);
+  f16x8* hbuf = cbuf + 2 * kTile * 16;
   float4* stage = reinterpret_cast<float4*>(smem_raw + kTileBufs * kTile * 256);
   float* nq_s = reinterpret_cast<float*>(smem_raw + kTileBufs * kTile * 256 + 2 * NW * kTile * 16);
   float* L_base = nq_s + BS;
@@ -134,22 +134,26 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   const int ld_row = tid >> 4, ld_chunk = tid & 15;  // NT >= 128 threads: rows ld_row, ld_row + NT/16, ...
   constexpr int kLdRowsPerPass = NT / 16;
   constexpr int kLdPasses = (kTile + kLdRowsPerPass - 1) / kLdRowsPerPass;
-  uint4 pre[kLdPasses];
-  uint4 preh[MODE == kSelectBox ? kLdPasses : 1];
-  auto fetch = [&](int tile) {
+  // Every load is issued without a branch: rows past the last block read
+  // block M - 1 (their lanes' results are never used), so no loaded value is
+  // merged at a branch join, where the compiler would wait for all loads in
+  // flight.  Vector types, not uint4: a struct copied from memory stays a
+  // memcpy that keeps the array out of registers.
+  constexpr bool kRescue = MODE == kSelectDual || MODE == kSelectFullL2;
+  f16x8 pre[kLdPasses];
+  f16x8 preh[MODE == kSelectBox ? kLdPasses : 1];
+  float u_next = 0.f;  // uplift (or radius) of this lane's centroid in the next tile
+  auto fetch = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < kLdPasses; ++p) {
-      const int r = ld_row + p * kLdRowsPerPass;
-      const int bb = tile * kTile + r;
-      const bool ok = r < kTile && bb < M;
-      pre[p] = ok ? *reinterpret_cast<const uint4*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk)
-                  : make_uint4(0u, 0u, 0u, 0u);
+      const int bb = min(tile * kTile + ld_row + p * kLdRowsPerPass, M - 1);
+      pre[p] = *reinterpret_cast<const f16x8*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk);
       if constexpr (MODE == kSelectBox)
-        preh[p] = ok ? *reinterpret_cast<const uint4*>(hg + (size_t)bb * kHeadDim + 8 * ld_chunk)
-                     : make_uint4(0u, 0u, 0u, 0u);
+        preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)bb * kHeadDim + 8 * ld_chunk);
     }
+    if constexpr (kRescue) u_next = ug[min(tile * kTile + l32, M - 1)];
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < kLdPasses; ++p) {
       const int r = ld_row + p * kLdRowsPerPass;
@@ -161,6 +165,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   };
   fetch(0);
   store(0);
+  float u_cur = u_next;
   __syncthreads();
 
   // Per-element token norms minus the wave maximum (rescue exponent offsets).
@@ -177,24 +182,14 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     const int b = tile * kTile + l32;
     if (wave_active) {
       f32x16 acc = {};
-      const uint4* cb = cbuf + buf * kTile * 16 + l32 * 16;
+      const f16x8* cb = cbuf + buf * kTile * 16 + l32 * 16;
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const uint4 raw = cb[swz(l32, 2 * ks + half)];
-        f16x8 bfrag;
-        __builtin_memcpy(&bfrag, &raw, 16);
-        acc = mfma_f16(qa[ks], bfrag, acc);
-      }
+      for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qa[ks], cb[swz(l32, 2 * ks + half)], acc);
       if constexpr (MODE == kSelectBox) {
         // + |q| . h_b: Eq. quest_box written as q . v_b + |q|^T h_b.
-        const uint4* hb = hbuf + buf * kTile * 16 + l32 * 16;
+        const f16x8* hb = hbuf + buf * kTile * 16 + l32 * 16;
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-          const uint4 raw = hb[swz(l32, 2 * ks + half)];
-          f16x8 bfrag;
-          __builtin_memcpy(&bfrag, &raw, 16);
-          acc = mfma_f16(qabs[ks], bfrag, acc);
-        }
+        for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qabs[ks], hb[swz(l32, 2 * ks + half)], acc);
       }
       if (wave_partial) {
 #pragma unroll
@@ -204,7 +199,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       float mx = acc[0];
 #pragma unroll
       for (int r = 1; r < 16; ++r) mx = fmaxf(mx, acc[r]);
-      mx = fmaxf(mx, wave_xor_f(mx, 32));
+      mx = half_max(mx);
       float sb = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
@@ -213,20 +208,23 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         mr = -INFINITY;  // single branch: no rescue scores
         sr = 0.f;
       }
-      const float u = (MODE == kSelectDual || MODE == kSelectFullL2) && b < M ? ug[b] * u_scale : 0.f;
-      if ((MODE == kSelectDual || MODE == kSelectFullL2) && __any(u != 0.f)) {
+      // Lanes past the candidates take u = 0: the rescue pass runs only
+      // when a candidate of the tile needs it.
+      const float u = kRescue && b < n_cand ? u_cur * u_scale : 0.f;
+      if (kRescue && __any(u != 0.f)) {
         mr = mx + nq_max * u;
         sr = 0.f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) sr += fast_exp2(fmaf(nqd[r], u, acc[r] - mx));
       }
-      sb += wave_xor_f(sb, 32);
-      sr += wave_xor_f(sr, 32);
+      sb = half_sum(sb);
+      sr = half_sum(sr);
       if (half == 0) stage[(buf * NW + wave) * kTile + l32] = make_float4(mx, sb, mr, sr);
     } else if (half == 0) {
       stage[(buf * NW + wave) * kTile + l32] = make_float4(-INFINITY, 0.f, -INFINITY, 0.f);
     }
     if (tile + 1 < n_tiles) store(buf ^ 1);
+    u_cur = u_next;
     __syncthreads();
     // Merge the waves' partial sums of this tile (wave 0: lanes 0-31 base, 32-63 rescue).
     if (wave == 0 && b < n_cand) {
