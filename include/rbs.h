@@ -78,9 +78,10 @@ typedef struct {
  *                                  head's M radii (linear interpolation between
  *                                  order statistics)
  *   summary    rbs_summary_bytes() bytes: the select-ready copy of the summaries
- *              (centroids as f16 pre-scaled by log2(e)/sqrt(d), and the
- *              per-block rescue uplift r_b beta_b log2(e)/sqrt(d)).  Opaque;
- *              written by rbs_block_stats, read by rbs_select.
+ *              (centroids as f16 pre-scaled by log2(e)/sqrt(d), the per-block
+ *              rescue uplift r_b beta_b log2(e)/sqrt(d), and the norms of the
+ *              scaled centroids).  Opaque; written by rbs_block_stats, read by
+ *              rbs_select and rbs_select_attend.
  */
 typedef struct {
   float* centroids;

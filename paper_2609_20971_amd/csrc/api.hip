@@ -108,6 +108,8 @@ int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stat
   a.cent16 = static_cast<_Float16*>(stats->summary);
   a.uplift = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
                                       rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  a.cnorm = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
+                                     rbs::summary_cnorm_offset(shape->n_kv_heads, M));
   return from_hip(rbs::launch_stats(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -132,6 +134,8 @@ int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats, fl
   a.cent16 = static_cast<const _Float16*>(stats->summary);
   a.uplift = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
                                             rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  a.cnorm = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
+                                           rbs::summary_cnorm_offset(shape->n_kv_heads, M));
   a.tau_base = tau_base;
   a.tau_rescue = tau_rescue;
   a.n_sink = n_sink;
@@ -197,6 +201,8 @@ int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, cons
   sa.cent16 = static_cast<const _Float16*>(stats->summary);
   sa.uplift = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
                                              rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  sa.cnorm = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
+                                            rbs::summary_cnorm_offset(shape->n_kv_heads, M));
   sa.tau_base = tau_base;
   sa.tau_rescue = tau_rescue;
   sa.n_sink = n_sink;
@@ -350,6 +356,8 @@ int rbs_block_stats_varlen(const rbs_shape* shape, const rbs_batch* batch, const
   a.cent16 = static_cast<_Float16*>(stats->summary);
   a.uplift = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
                                       rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  a.cnorm = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
+                                     rbs::summary_cnorm_offset(shape->n_kv_heads, M));
   return from_hip(rbs::launch_stats_varlen(a, t, static_cast<hipStream_t>(stream)));
 }
 
@@ -375,6 +383,8 @@ int rbs_select_varlen(const rbs_shape* shape, const rbs_batch* batch, const void
   a.cent16 = static_cast<const _Float16*>(stats->summary);
   a.uplift = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
                                             rbs::summary_uplift_offset(shape->n_kv_heads, M));
+  a.cnorm = reinterpret_cast<const float*>(static_cast<const unsigned char*>(stats->summary) +
+                                           rbs::summary_cnorm_offset(shape->n_kv_heads, M));
   a.tau_base = tau_base;
   a.tau_rescue = tau_rescue;
   a.n_sink = n_sink;

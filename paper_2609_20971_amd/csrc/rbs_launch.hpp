@@ -16,6 +16,7 @@ struct StatsArgs {
   float* quantiles;
   _Float16* cent16;  // select-ready centroids [H_kv][M][d]
   float* uplift;     // select-ready rescue uplift [H_kv][M]
+  float* cnorm;      // norm of each select-ready centroid [H_kv][M]
 };
 
 struct BoxArgs {
@@ -34,6 +35,7 @@ struct SelectArgs {
   const _Float16* cent16;             // box: scaled box centres
   const _Float16* half16 = nullptr;   // box: scaled box half-widths
   const float* uplift;
+  const float* cnorm = nullptr;       // dual: select-ready centroid norms
   const float* radii = nullptr;       // full-L2
   float budget = 0.f;                 // box: budget fraction
   float tau_base, tau_rescue;
@@ -56,14 +58,18 @@ struct AttnArgs {
   float* lse;
 };
 
-// Byte offset of the uplift array inside the select-ready summary.
+// Select-ready summary, each part 256-byte aligned: f16 centroids scaled by
+// log2(e)/sqrt(d) [H_kv][M][d] | fp32 uplift [H_kv][M] | fp32 norms of the
+// scaled centroids [H_kv][M].
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline size_t summary_uplift_offset(int n_kv_heads, int n_blocks) {
-  size_t cent = (size_t)n_kv_heads * n_blocks * 128 * sizeof(_Float16);
-  return (cent + 255) & ~(size_t)255;
+  return align256((size_t)n_kv_heads * n_blocks * 128 * sizeof(_Float16));
 }
-
+inline size_t summary_cnorm_offset(int n_kv_heads, int n_blocks) {
+  return align256(summary_uplift_offset(n_kv_heads, n_blocks) + (size_t)n_kv_heads * n_blocks * sizeof(float));
+}
 inline size_t summary_bytes(int n_kv_heads, int n_blocks) {
-  return summary_uplift_offset(n_kv_heads, n_blocks) + (size_t)n_kv_heads * n_blocks * sizeof(float);
+  return summary_cnorm_offset(n_kv_heads, n_blocks) + (size_t)n_kv_heads * n_blocks * sizeof(float);
 }
 
 // A batch of independent sequences packed along the token axis (the varlen

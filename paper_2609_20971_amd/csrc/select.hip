@@ -30,6 +30,7 @@ __global__ __launch_bounds__(BS * 2) void select_varlen_kernel(SelectCore c, int
   c.Q += (size_t)t.tok[sq] * kHeadDim;
   c.cent16 += (size_t)t.blk[sq] * kHeadDim;
   c.uplift += t.blk[sq];
+  c.cnorm += t.blk[sq];
   c.counts += t.blk[sq];
   c.indices += t.cap[sq];
   const int i = c.M - 1 - local / Hq;

@@ -28,6 +28,7 @@
 namespace rbs {
 
 constexpr int kTile = 32;  // centroids per tile
+constexpr float kPlainBound = 120.0f;  // |exponent| bound for unshifted exp2 sums (fp32 normal range: 2^-126)
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
 
@@ -50,6 +51,7 @@ struct SelectCore {
   const _Float16* cent16;     // dual, centroid, full-L2: scaled centroids; box: scaled box centres
   const _Float16* half16;     // box: scaled box half-widths
   const float* uplift;        // dual: r beta log2(e)/sqrt(d)
+  const float* cnorm;         // dual: norms of the scaled centroids
   const float* radii;         // full-L2: r (scaled here)
   float log2_tau_base, log2_tau_rescue;  // centroid / full-L2: the one threshold in both
   float budget;               // box: budget fraction rho
@@ -99,6 +101,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   const _Float16* hg = MODE == kSelectBox ? c.half16 + (size_t)g * c.ldm * kHeadDim : nullptr;
   const float* ug = MODE == kSelectFullL2 ? c.radii + (size_t)g * c.ldm : c.uplift + (size_t)g * c.ldm;
   const float u_scale = MODE == kSelectFullL2 ? kLog2e / sqrtf((float)kHeadDim) : 1.0f;
+  const float* cng = MODE == kSelectDual ? c.cnorm + (size_t)g * c.ldm : nullptr;
 
   // ---- Q rows of this wave as MFMA A operands (row = 32*wave + l32).
   const int t_local = 32 * wave + l32;
@@ -142,7 +145,8 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   constexpr bool kRescue = MODE == kSelectDual || MODE == kSelectFullL2;
   f16x8 pre[kLdPasses];
   f16x8 preh[MODE == kSelectBox ? kLdPasses : 1];
-  float u_next = 0.f;  // uplift (or radius) of this lane's centroid in the next tile
+  float u_next = 0.f;   // uplift (or radius) of this lane's centroid in the next tile
+  float cn_next = 0.f;  // and the norm of its scaled centroid (dual)
   auto fetch = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < kLdPasses; ++p) {
@@ -152,6 +156,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)bb * kHeadDim + 8 * ld_chunk);
     }
     if constexpr (kRescue) u_next = ug[min(tile * kTile + l32, M - 1)];
+    if constexpr (MODE == kSelectDual) cn_next = cng[min(tile * kTile + l32, M - 1)];
   };
   auto store = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
@@ -165,21 +170,35 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   };
   fetch(0);
   store(0);
-  float u_cur = u_next;
+  float u_cur = u_next, cn_cur = cn_next;
+  if (lane == 0) red_f[wave] = nq_max;
   __syncthreads();
 
-  // Per-element token norms minus the wave maximum (rescue exponent offsets).
+  // Largest |q| of the query block, and per element the token's |q| minus it
+  // (the rescue exponent offsets, <= 0).
+  float nq_row = red_f[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) nq_row = fmaxf(nq_row, red_f[w]);
   float nqd[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int t = 32 * wave + mfma_row(r, lane);
-    nqd[r] = (t < nb) ? nq_s[t] - nq_max : 0.f;
+    nqd[r] = (t < nb) ? nq_s[t] - nq_row : 0.f;
   }
 
   for (int tile = 0; tile < n_tiles; ++tile) {
     const int buf = tile & 1;
     if (tile + 1 < n_tiles) fetch(tile + 1);
     const int b = tile * kTile + l32;
+    // The dual selector skips the per-block shift when every exponent of the
+    // tile is bounded: with |q_t . c'_b| <= |q_t| |c'_b| (Cauchy-Schwarz) and
+    // u_b >= 0, the logits and rescue logits lie in
+    // [-nq_row (|c'_b| + u_b), nq_row |c'_b|], and within +-kPlainBound exp2
+    // neither overflows nor leaves the normal range.  Every wave of the
+    // workgroup reads the same values, so all take the same path.
+    bool plain_tile = false;
+    if constexpr (MODE == kSelectDual)
+      plain_tile = __all(b >= n_cand || nq_row * (cn_cur + u_cur) <= kPlainBound);
     if (wave_active) {
       f32x16 acc = {};
       const f16x8* cb = cbuf + buf * kTile * 16 + l32 * 16;
@@ -196,26 +215,49 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         for (int r = 0; r < 16; ++r)
           if (32 * wave + mfma_row(r, lane) >= nb) acc[r] = -INFINITY;
       }
-      float mx = acc[0];
+      // Per lane (key block b) and branch, a (shift, sum of exp2) pair over
+      // this wave's tokens: S_b = exp2(shift) * sum.
+      const bool plain = plain_tile;
+      float mx = 0.f, sb = 0.f;
+      if (plain) {
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, acc[r]);
-      mx = half_max(mx);
-      float sb = 0.f;
+        for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r]);
+      } else {
+        mx = acc[0];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
+        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, acc[r]);
+        mx = half_max(mx);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
+      }
       float mr = mx, sr = sb;
       if constexpr (MODE == kSelectCentroid || MODE == kSelectBox) {
         mr = -INFINITY;  // single branch: no rescue scores
         sr = 0.f;
       }
       // Lanes past the candidates take u = 0: the rescue pass runs only
-      // when a candidate of the tile needs it.
+      // when a candidate of the tile needs it.  Rescue logit of token t:
+      // acc + |q_t| u = nq_row u + (acc + nqd u).
       const float u = kRescue && b < n_cand ? u_cur * u_scale : 0.f;
       if (kRescue && __any(u != 0.f)) {
-        mr = mx + nq_max * u;
         sr = 0.f;
+        if (plain) {
+          mr = nq_row * u;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sr += fast_exp2(fmaf(nqd[r], u, acc[r] - mx));
+          for (int r = 0; r < 16; ++r) sr += fast_exp2(fmaf(nqd[r], u, acc[r]));
+        } else {
+          float v[16];
+          float mv = -INFINITY;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            v[r] = fmaf(nqd[r], u, acc[r]);
+            mv = fmaxf(mv, v[r]);
+          }
+          mv = half_max(mv);
+          mr = mv + nq_row * u;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sr += fast_exp2(v[r] - mv);
+        }
       }
       sb = half_sum(sb);
       sr = half_sum(sr);
@@ -225,9 +267,22 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     }
     if (tile + 1 < n_tiles) store(buf ^ 1);
     u_cur = u_next;
+    cn_cur = cn_next;
     __syncthreads();
-    // Merge the waves' partial sums of this tile (wave 0: lanes 0-31 base, 32-63 rescue).
-    if (wave == 0 && b < n_cand) {
+    // Merge the waves' partial sums of this tile (lanes 0-31 base, 32-63
+    // rescue), by one wave in turn: the waves of a workgroup sit on different
+    // SIMDs, and a fixed merging wave would load one SIMD more than the rest.
+    if (wave == (tile & (NW - 1)) && b < n_cand && plain_tile) {
+      // Every wave used the same shift: S_b = exp2(shift) * (sum of the sums).
+      float sum = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const float4 p = stage[(buf * NW + w) * kTile + l32];
+        sum += half ? p.w : p.y;
+      }
+      const float4 p0 = stage[(buf * NW) * kTile + l32];  // wave 0 is always active
+      (half ? L_res : L_base)[b] = (half ? p0.z : p0.x) + log2f(sum);
+    } else if (wave == (tile & (NW - 1)) && b < n_cand) {
       float top = -INFINITY;
 #pragma unroll
       for (int w = 0; w < NW; ++w) {
@@ -354,6 +409,7 @@ inline SelectCore make_select_core(const SelectArgs& a) {
   c.cent16 = a.cent16;
   c.half16 = a.half16;
   c.uplift = a.uplift;
+  c.cnorm = a.cnorm;
   c.radii = a.radii;
   c.budget = a.budget;
   c.log2_tau_base = a.tau_base > 0.f ? log2f(a.tau_base) : -INFINITY;

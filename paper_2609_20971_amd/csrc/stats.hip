@@ -78,7 +78,8 @@ template <int BS>
 __global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __restrict__ K, const SeqTable t,
                                                              float* __restrict__ centroids,
                                                              float* __restrict__ radii,
-                                                             _Float16* __restrict__ cent16, float sel_scale) {
+                                                             _Float16* __restrict__ cent16,
+                                                             float* __restrict__ cnorm, float sel_scale) {
   constexpr int kRowsPerThread = BS / 16;
   __shared__ float red[4][kHeadDim];
   __shared__ float red_r[4];
@@ -152,6 +153,18 @@ __global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __
   __syncthreads();
 
   const size_t blk = (size_t)g * M + bg;
+  // Norm of the select-ready (scaled) centroid: the selector bounds its
+  // logits with it (Cauchy-Schwarz).  Lanes 0-15 of wave 0 hold the 16 chunks.
+  if (wave == 0) {
+    float n2 = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) n2 = fmaf(c[e] * sel_scale, c[e] * sel_scale, n2);
+    n2 += wave_xor_f(n2, 1);
+    n2 += wave_xor_f(n2, 2);
+    n2 += wave_xor_f(n2, 4);
+    n2 += wave_xor_f(n2, 8);
+    if (lane == 0) cnorm[blk] = sqrtf(n2);
+  }
   if (tid < 16) {
     float4* dst = reinterpret_cast<float4*>(centroids + blk * kHeadDim + chunk * 8);
     dst[0] = make_float4(c[0], c[1], c[2], c[3]);
@@ -290,7 +303,7 @@ hipError_t launch_stats_varlen(const StatsArgs& a, const SeqTable& t, hipStream_
 #define RBS_STATS_CASE(BSZ)                                                                                 \
   case BSZ:                                                                                                 \
     hipLaunchKernelGGL(stats_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, t, a.centroids, a.radii,    \
-                       a.cent16, sel_scale);                                                                \
+                       a.cent16, a.cnorm, sel_scale);                                                       \
     break;
   switch (a.block_size) {
     RBS_STATS_CASE(64)

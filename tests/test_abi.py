@@ -50,8 +50,8 @@ def test_capacity_and_summary_sizes():
     assert rbs.rbs_index_capacity(1024) == 1024 * 1025 // 2
     assert rbs.rbs_index_capacity(0) == 0
     s = rbs.make_shape(131072, 32, 4, 128)
-    # f16 select-ready centroids + fp32 uplift per block.
-    assert rbs.rbs_summary_bytes(s) == 4 * 1024 * 256 + 4 * 1024 * 4
+    # f16 select-ready centroids + fp32 uplift and centroid norm per block.
+    assert rbs.rbs_summary_bytes(s) == 4 * 1024 * 256 + 2 * 4 * 1024 * 4
     assert rbs.rbs_summary_bytes(rbs.make_shape(100, 2, 1, 96)) == 0
 
 
@@ -216,7 +216,8 @@ def test_varlen_sizes():
     m = [6, 12, 1, 17, 1]
     assert rbs.rbs_varlen_blocks(s, b) == sum(m)
     assert rbs.rbs_varlen_index_capacity(s, b) == sum(x * (x + 1) // 2 for x in m)
-    assert rbs.rbs_varlen_summary_bytes(s, b) == 2 * 37 * 256 + 2 * 37 * 4  # = rbs_summary_bytes at M = 37
+    # rbs_summary_bytes at M = 37: f16 centroids, then uplift and norms, each part 256-aligned
+    assert rbs.rbs_varlen_summary_bytes(s, b) == 2 * 37 * 256 + 512 + 2 * 37 * 4
     one = rbs.Batch([4096])
     s1 = rbs.varlen_shape(one, 4, 2, 128)
     assert rbs.rbs_varlen_summary_bytes(s1, one) == rbs.rbs_summary_bytes(s1)
