@@ -14,6 +14,8 @@
  *   rbs_block_box,      the supporting selectors of the paper's selector
  *   rbs_select_variant  comparison (centroid-only, full-L2 bound, Quest-style
  *                       box; Table selector_ablation, App. geometry)
+ *   rbs_*_fp8           attention on FP8 (E4M3) Q, K, V on the FP8 matrix
+ *                       core (the paper's models are FP8 checkpoints, Sec. 4.1)
  *   rbs_*_varlen        the three stages over a batch of independent
  *                       sequences in one launch each (appendix on A100
  *                       system measurements, prompt throughput: batched
@@ -203,6 +205,36 @@ int rbs_select_variant(const rbs_shape* shape, const void* Q, const rbs_stats* s
 
 /* Full causal lists (every block 0..i for every row): the dense path. */
 int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * FP8 attention inputs.  The paper's models are FP8 checkpoints (Sec. 4.1;
+ * the precision of their attention is not stated).  These calls run stage 3
+ * on FP8 E4M3 copies of Q, K and V (OCP E4M3: bias 7, 3 mantissa bits,
+ * largest finite 448) with the products on gfx950's FP8 matrix core; the
+ * selection is unchanged (bf16 inputs, rbs_select).  Block size 128 only
+ * (others return RBS_ERR_UNSUPPORTED).
+ *
+ * Scaling: each head h of Q (then K, then V) is scaled so that its largest
+ * magnitude amax_h maps to 448: code = E4M3(x * (448 / amax_h)), rounded to
+ * nearest (ties to even), the scale rounded to fp32 and x * scale rounded to
+ * fp32 first; dequantisation multiplies by amax_h / 448 (fp32).  An all-zero
+ * head uses scale 1.
+ *   amax   fp32 [H_q + 2 H_kv]: Q heads, K heads, V heads
+ *   Q8     E4M3 [H_q][N][d]      K8  E4M3 [H_kv][N][d]  (row-major copies)
+ *   V8t    rbs_fp8_vt_bytes() bytes: per KV head and key block, the d x B
+ *          tile of V transposed, keys in the order the attention kernel
+ *          consumes them (opaque to the caller; keys past N are zero)
+ * Attention: as rbs_sparse_prefill on the dequantised inputs; P is rounded to
+ * E4M3 for the PV product (values <= 256), and the denominator sums the same
+ * rounded values.  O is bf16, lse as in rbs_sparse_prefill.
+ */
+size_t rbs_fp8_vt_bytes(const rbs_shape* shape);
+int rbs_fp8_amax(const rbs_shape* shape, const void* Q, const void* K, const void* V, float* amax, void* stream);
+int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const void* V, const float* amax,
+                 void* Q8, void* K8, void* V8t, void* stream);
+int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K8, const void* V8t,
+                           const float* amax, const int32_t* counts, const int32_t* indices,
+                           float softmax_scale, void* O, float* lse, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Batches of independent sequences (varlen).  The paper runs batched prompts

@@ -63,6 +63,12 @@ from .rbs import (
     batch_block_stats,
     batch_select,
     batch_attention_on_mask,
+    E4M3_MAX,
+    e4m3_decode,
+    e4m3_encode,
+    fp8_amax,
+    fp8_quantize,
+    fp8_dequantize,
 )
 
 __all__ = [
@@ -87,4 +93,10 @@ __all__ = [
     "batch_block_stats",
     "batch_select",
     "batch_attention_on_mask",
+    "E4M3_MAX",
+    "e4m3_decode",
+    "e4m3_encode",
+    "fp8_amax",
+    "fp8_quantize",
+    "fp8_dequantize",
 ]

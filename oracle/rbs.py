@@ -467,3 +467,81 @@ def batch_attention_on_mask(Q, K, V, seq_tokens, block_size: int, row_blocks: di
     return {s: {h: attention_on_mask(Qs[s][h], Ks[s][h // group], Vs[s][h // group], block_size, rows, scale)
                 for h, rows in heads.items()}
             for s, heads in row_blocks.items()}
+
+
+# ---------------------------------------------------------------- FP8 inputs
+#
+# Attention on FP8 inputs (the paper's models are FP8 checkpoints, Sec. 4.1;
+# the precision of their attention is not stated).  The format is E4M3 as
+# the OCP 8-bit floating-point specification defines it: 1 sign bit, 4
+# exponent bits with bias 7, 3 mantissa bits; subnormals (m / 8) 2^-6; the
+# largest finite magnitude 448 (S.1111.110); no infinities.  READINGS: each
+# head is scaled so that its largest |x| maps to 448 (inv = 448 / amax and
+# dequantisation amax / 448, both rounded to float32, x * inv rounded to
+# float32 before the conversion), conversion rounds to nearest with ties to
+# even and saturates at 448.  Attention on FP8 inputs is attention_on_mask on
+# the dequantised values.
+
+E4M3_MAX = 448.0
+
+
+def e4m3_decode(codes) -> np.ndarray:
+    """Value of each E4M3 code (uint8 array), float64; the two NaN codes decode to nan."""
+    c = np.asarray(codes, dtype=np.int64)
+    sign = np.where(c & 0x80, -1.0, 1.0)
+    e = (c >> 3) & 15
+    m = c & 7
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * 2.0 ** (e - 7))
+    mag = np.where((c & 0x7f) == 0x7f, np.nan, mag)
+    return sign * mag
+
+
+def e4m3_encode(x) -> np.ndarray:
+    """Nearest E4M3 code of each finite value (ties to even mantissa),
+    magnitudes above 448 saturating to 448.  Returns uint8."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.minimum(np.abs(x), E4M3_MAX)
+    out = np.zeros(a.shape, dtype=np.int64)
+    sub = a < 2.0 ** -6
+    # Subnormal range: a multiple of 2^-9, rounded half to even (np.rint).
+    out[sub] = np.rint(a[sub] * 2.0 ** 9).astype(np.int64)
+    nrm = ~sub
+    if nrm.any():
+        an = a[nrm]
+        e = np.floor(np.log2(an)).astype(np.int64)
+        # Guard the floor of log2 at exact powers of two.
+        e = np.where(2.0 ** e > an, e - 1, e)
+        e = np.where(2.0 ** (e + 1) <= an, e + 1, e)
+        q = np.rint((an / 2.0 ** e - 1.0) * 8.0).astype(np.int64)  # mantissa in eighths, half to even
+        carry = q == 8
+        e = np.where(carry, e + 1, e)
+        q = np.where(carry, 0, q)
+        out[nrm] = ((e + 7) << 3) | q
+    out = np.where(np.signbit(x), out | 0x80, out)
+    return out.astype(np.uint8)
+
+
+def fp8_amax(X) -> np.ndarray:
+    """Largest |x| of every head of X [H][N][d]."""
+    X = np.asarray(X, dtype=np.float64)
+    return np.abs(X).reshape(X.shape[0], -1).max(axis=1)
+
+
+def fp8_quantize(X, amax):
+    """E4M3 codes of X [H][N][d] with the per-head scaling above, and the
+    float32 dequantisation scale of every head.  Returns (codes uint8, deq)."""
+    X = np.asarray(X, dtype=np.float64)
+    codes = np.empty(X.shape, dtype=np.uint8)
+    deq = np.empty(X.shape[0], dtype=np.float64)
+    for h in range(X.shape[0]):
+        am = np.float32(amax[h])
+        inv = np.float32(448.0) / am if am > 0 else np.float32(1.0)
+        deq[h] = float(am / np.float32(448.0)) if am > 0 else 1.0
+        y = (X[h].astype(np.float32) * inv).astype(np.float32)
+        codes[h] = e4m3_encode(y)
+    return codes, deq
+
+
+def fp8_dequantize(codes, deq) -> np.ndarray:
+    """Values of E4M3 codes [H][N][d] times each head's scale, float64."""
+    return e4m3_decode(codes) * np.asarray(deq, dtype=np.float64)[:, None, None]

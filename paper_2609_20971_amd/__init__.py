@@ -7,9 +7,17 @@
     box = rbs_block_box(shape, K); rbs_select_variant(shape, Q, stats, "box", rho, ..., box=box)  # supporting selectors
     batch = Batch([n0, n1, ...]); shape = varlen_shape(batch, H_q, H_kv, B)   # independent sequences, packed
     stats = rbs_block_stats_varlen(shape, batch, K); ...; rbs_sparse_prefill_varlen(shape, batch, Q, K, V, ...)
+    f8 = rbs_fp8_prepare(shape, Q, K, V); O = rbs_sparse_prefill_fp8(shape, f8, counts, indices)  # FP8 inputs
 """
 
 from ._lib import (  # noqa: F401
+    Fp8Inputs,
+    allocate_fp8,
+    rbs_fp8_amax,
+    rbs_fp8_pack,
+    rbs_fp8_prepare,
+    rbs_fp8_vt_bytes,
+    rbs_sparse_prefill_fp8,
     Batch,
     RBS_MAX_SEQS,
     allocate_lists_varlen,

@@ -101,6 +101,14 @@ def load() -> ctypes.CDLL:
     lib.rbs_select_variant.restype = ctypes.c_int
     lib.rbs_dense_indices.argtypes = [SP, P, P, P]
     lib.rbs_dense_indices.restype = ctypes.c_int
+    lib.rbs_fp8_vt_bytes.argtypes = [SP]
+    lib.rbs_fp8_vt_bytes.restype = SZ
+    lib.rbs_fp8_amax.argtypes = [SP, P, P, P, P, P]
+    lib.rbs_fp8_amax.restype = ctypes.c_int
+    lib.rbs_fp8_pack.argtypes = [SP, P, P, P, P, P, P, P, P]
+    lib.rbs_fp8_pack.restype = ctypes.c_int
+    lib.rbs_sparse_prefill_fp8.argtypes = [SP, P, P, P, P, P, P, F32, P, P, P]
+    lib.rbs_sparse_prefill_fp8.restype = ctypes.c_int
     BP = ctypes.POINTER(rbs_batch)
     lib.rbs_varlen_blocks.argtypes = [SP, BP]
     lib.rbs_varlen_blocks.restype = I32
@@ -403,3 +411,61 @@ def rbs_dense_indices_varlen(shape: rbs_shape, batch: Batch, counts=None, indice
     _check("rbs_dense_indices_varlen", load().rbs_dense_indices_varlen(
         ctypes.byref(shape), ctypes.byref(batch.c), _ptr(counts), _ptr(indices), _stream(stream)))
     return counts, indices
+
+
+# ------------------------------------------------------------------ FP8 inputs
+
+@dataclass
+class Fp8Inputs:
+    """E4M3 copies of Q, K, V and their per-head amax (device buffers)."""
+    amax: torch.Tensor   # fp32 [H_q + 2 H_kv]
+    Q8: torch.Tensor     # uint8 [H_q][N][d]
+    K8: torch.Tensor     # uint8 [H_kv][N][d]
+    V8t: torch.Tensor    # uint8 [rbs_fp8_vt_bytes]
+
+
+def rbs_fp8_vt_bytes(shape: rbs_shape) -> int:
+    return int(load().rbs_fp8_vt_bytes(ctypes.byref(shape)))
+
+
+def allocate_fp8(shape: rbs_shape, device="cuda") -> Fp8Inputs:
+    nvt = rbs_fp8_vt_bytes(shape)
+    if nvt == 0:
+        raise RbsError("rbs_fp8_vt_bytes", RBS_ERR_UNSUPPORTED, "FP8 attention needs block size 128")
+    u8 = dict(dtype=torch.uint8, device=device)
+    return Fp8Inputs(torch.empty(shape.n_q_heads + 2 * shape.n_kv_heads, dtype=torch.float32, device=device),
+                     torch.empty((shape.n_q_heads, shape.n_tokens, shape.head_dim), **u8),
+                     torch.empty((shape.n_kv_heads, shape.n_tokens, shape.head_dim), **u8),
+                     torch.empty(nvt, **u8))
+
+
+def rbs_fp8_amax(shape: rbs_shape, Q, K, V, amax, stream=None):
+    _check("rbs_fp8_amax", load().rbs_fp8_amax(ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V), _ptr(amax),
+                                               _stream(stream)))
+    return amax
+
+
+def rbs_fp8_pack(shape: rbs_shape, Q, K, V, f8: Fp8Inputs, stream=None) -> Fp8Inputs:
+    _check("rbs_fp8_pack", load().rbs_fp8_pack(ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V), _ptr(f8.amax),
+                                               _ptr(f8.Q8), _ptr(f8.K8), _ptr(f8.V8t), _stream(stream)))
+    return f8
+
+
+def rbs_fp8_prepare(shape: rbs_shape, Q, K, V, f8: Fp8Inputs | None = None, stream=None) -> Fp8Inputs:
+    """amax then pack: the E4M3 inputs of rbs_sparse_prefill_fp8."""
+    if f8 is None:
+        f8 = allocate_fp8(shape, Q.device)
+    rbs_fp8_amax(shape, Q, K, V, f8.amax, stream)
+    return rbs_fp8_pack(shape, Q, K, V, f8, stream)
+
+
+def rbs_sparse_prefill_fp8(shape: rbs_shape, f8: Fp8Inputs, counts, indices, softmax_scale: float = 0.0, O=None,
+                           lse=None, stream=None):
+    """Stage 3 on the E4M3 inputs; returns O (bf16 [H_q][N][d])."""
+    if O is None:
+        O = torch.empty((shape.n_q_heads, shape.n_tokens, shape.head_dim), dtype=torch.bfloat16,
+                        device=f8.Q8.device)
+    _check("rbs_sparse_prefill_fp8", load().rbs_sparse_prefill_fp8(
+        ctypes.byref(shape), _ptr(f8.Q8), _ptr(f8.K8), _ptr(f8.V8t), _ptr(f8.amax), _ptr(counts), _ptr(indices),
+        float(softmax_scale), _ptr(O), _ptr(lse), _stream(stream)))
+    return O

@@ -437,6 +437,60 @@ int rbs_dense_indices_varlen(const rbs_shape* shape, const rbs_batch* batch, int
       rbs::launch_dense_indices_varlen(shape->n_q_heads, t, counts, indices, static_cast<hipStream_t>(stream)));
 }
 
+size_t rbs_fp8_vt_bytes(const rbs_shape* shape) {
+  if (check_shape(shape) != RBS_OK || shape->block_size != 128) return 0;
+  return (size_t)shape->n_kv_heads * blocks_of(shape) * 128 * shape->block_size;
+}
+
+int rbs_fp8_amax(const rbs_shape* shape, const void* Q, const void* K, const void* V, float* amax, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (Q == nullptr || K == nullptr || V == nullptr || amax == nullptr) return RBS_ERR_NULL;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(amax)) return RBS_ERR_ALIGN;
+  return from_hip(rbs::launch_fp8_amax(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
+                                       static_cast<const uint16_t*>(V), shape->n_tokens, shape->n_q_heads,
+                                       shape->n_kv_heads, amax, static_cast<hipStream_t>(stream)));
+}
+
+int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const void* V, const float* amax, void* Q8,
+                 void* K8, void* V8t, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (shape->block_size != 128) return RBS_ERR_UNSUPPORTED;
+  if (Q == nullptr || K == nullptr || V == nullptr || amax == nullptr || Q8 == nullptr || K8 == nullptr ||
+      V8t == nullptr)
+    return RBS_ERR_NULL;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(amax) || !aligned16(Q8) || !aligned16(K8) ||
+      !aligned16(V8t))
+    return RBS_ERR_ALIGN;
+  return from_hip(rbs::launch_fp8_pack(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
+                                       static_cast<const uint16_t*>(V), shape->n_tokens, shape->n_q_heads,
+                                       shape->n_kv_heads, blocks_of(shape), amax, static_cast<uint8_t*>(Q8),
+                                       static_cast<uint8_t*>(K8), static_cast<uint8_t*>(V8t),
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K8, const void* V8t,
+                           const float* amax, const int32_t* counts, const int32_t* indices, float softmax_scale,
+                           void* O, float* lse, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (shape->block_size != 128) return RBS_ERR_UNSUPPORTED;
+  if (Q8 == nullptr || K8 == nullptr || V8t == nullptr || amax == nullptr || counts == nullptr ||
+      indices == nullptr || O == nullptr)
+    return RBS_ERR_NULL;
+  if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
+  if (!aligned16(Q8) || !aligned16(K8) || !aligned16(V8t) || !aligned16(amax) || !aligned16(counts) ||
+      !aligned16(indices) || !aligned16(O) || (lse != nullptr && !aligned16(lse)))
+    return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
+  return from_hip(rbs::launch_attention_fp8(
+      static_cast<const uint8_t*>(Q8), static_cast<const uint8_t*>(K8), static_cast<const uint8_t*>(V8t), amax,
+      shape->n_tokens, shape->n_q_heads, shape->n_kv_heads, M, counts, indices, rbs_index_capacity(M), scale,
+      static_cast<uint16_t*>(O), lse, static_cast<hipStream_t>(stream)));
+}
+
 const char* rbs_status_str(int status) {
   switch (status) {
     case RBS_OK: return "ok";

@@ -267,3 +267,24 @@ def test_varlen_largest_batch_passes_validation():
     # Passes the shape and batch checks, stops at the NULL key pointer.
     assert lib.rbs_block_stats_varlen(ctypes.byref(s), ctypes.byref(b.c), None, ctypes.byref(st), None) == 1
     assert rbs.rbs_varlen_blocks(s, b) == 2 * 4096 + 62
+
+
+def test_fp8_sizes_and_validation():
+    rbs, lib = _lib()
+    s = rbs.make_shape(1000, 4, 2, 128)
+    assert rbs.rbs_fp8_vt_bytes(s) == 2 * 8 * 128 * 128
+    assert rbs.rbs_fp8_vt_bytes(rbs.make_shape(1000, 4, 2, 64)) == 0
+    S = ctypes.byref(s)
+    assert lib.rbs_fp8_amax(S, None, FAKE, FAKE, FAKE, None) == 1
+    assert lib.rbs_fp8_amax(S, FAKE, FAKE, FAKE, MIS, None) == 5
+    assert lib.rbs_fp8_pack(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == 1
+    assert lib.rbs_fp8_pack(S, FAKE, FAKE, FAKE, FAKE, FAKE, MIS, FAKE, None) == 5
+    b64 = rbs.make_shape(1000, 4, 2, 64)
+    assert lib.rbs_fp8_pack(ctypes.byref(b64), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 3
+    assert lib.rbs_sparse_prefill_fp8(ctypes.byref(b64), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None,
+                                      None) == 3
+    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, None, FAKE, FAKE, FAKE, 0.0, FAKE, None, None) == 1
+    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, float("nan"), FAKE, None, None) == 4
+    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, MIS, None) == 5
+    bad = rbs.make_shape(1000, 3, 2, 128)
+    assert lib.rbs_fp8_amax(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, None) == 2

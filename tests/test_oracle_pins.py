@@ -569,3 +569,64 @@ def test_block_aligned_batch_shares_centroids_but_not_beta_with_the_concatenatio
     for s in range(3):
         beta_s, rq_s = oracle.rescue_coefficients(Rc[:, off[s]:off[s + 1]])
         assert np.array_equal(betab[:, off[s]:off[s + 1]], beta_s) and np.array_equal(rqb[s], rq_s)
+
+
+# ---------------------------------------------------------------- FP8 E4M3
+# Values fixed by the OCP 8-bit floating-point format definition of E4M3
+# (bias 7, 3 mantissa bits, subnormals m/8 * 2^-6, largest finite 448).
+
+@pytest.mark.parametrize("x,code", [
+    (0.0, 0x00), (-0.0, 0x80), (1.0, 0x38), (-1.0, 0xb8), (448.0, 0x7e), (-448.0, 0xfe),
+    (2.0 ** -6, 0x08), (2.0 ** -9, 0x01), (7 * 2.0 ** -9, 0x07), (1.75, 0x3e), (240.0, 0x77),
+    (1.0625, 0x38),            # tie between 1.0 (mantissa 0) and 1.125 (1): even
+    (1.1875, 0x3a),            # tie between 1.125 (1) and 1.25 (2): even
+    (2.0 ** -10, 0x00),        # tie between 0 and the smallest subnormal: even
+    (3 * 2.0 ** -10, 0x02),    # tie between 2^-9 (1) and 2^-8 (2): even
+    (464.0, 0x7e), (1e6, 0x7e), (-1e6, 0xfe),   # saturation
+    (1.06, 0x38), (1.07, 0x39),
+])
+def test_e4m3_format_values(x, code):
+    assert int(oracle.e4m3_encode(np.array([x]))[0]) == code
+    exact = {0.0, 1.0, 448.0, 2.0 ** -6, 2.0 ** -9, 7 * 2.0 ** -9, 1.75, 240.0}
+    if abs(x) in exact:  # representable values decode back to themselves, sign included
+        v = oracle.e4m3_decode(np.array([code]))[0]
+        assert v == x and np.signbit(v) == np.signbit(x)
+
+
+def test_e4m3_codes_round_trip_in_order():
+    codes = np.arange(256, dtype=np.uint8)
+    v = oracle.e4m3_decode(codes)
+    finite = ~np.isnan(v)
+    assert finite.sum() == 254 and np.isnan(v[0x7f]) and np.isnan(v[0xff])
+    assert np.array_equal(oracle.e4m3_encode(v[finite]), codes[finite])
+    pos = v[:0x7f]
+    assert np.all(np.diff(pos) > 0) and pos[-1] == 448.0
+
+
+def test_e4m3_rounds_to_nearest_with_ties_to_even():
+    grid = oracle.e4m3_decode(np.arange(0x7f, dtype=np.uint8))   # 0 .. 448, code = index
+    rng = np.random.default_rng(4)
+    x = np.concatenate([rng.uniform(0, 448, 4000), rng.uniform(0, 2.0 ** -5, 2000),
+                        (grid[:-1] + grid[1:]) / 2])            # every midpoint is a tie
+    got = oracle.e4m3_encode(x).astype(np.int64)
+    d = np.abs(grid[None, :] - x[:, None])
+    best = d.min(axis=1)
+    for k in range(len(x)):
+        cands = np.nonzero(d[k] == best[k])[0]
+        want = cands[0] if len(cands) == 1 else [c for c in cands if c % 2 == 0][0]
+        assert got[k] == want, (x[k], got[k], want)
+
+
+def test_fp8_quantize_maps_amax_to_448():
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((3, 50, 8)) * np.array([0.01, 1.0, 300.0])[:, None, None]
+    amax = oracle.fp8_amax(X)
+    assert np.allclose(amax, np.abs(X).reshape(3, -1).max(axis=1))
+    codes, deq = oracle.fp8_quantize(X, amax)
+    for h in range(3):
+        i = np.unravel_index(np.abs(X[h]).argmax(), X[h].shape)
+        assert codes[h][i] & 0x7f == 0x7e                      # the largest magnitude becomes 448
+    Y = oracle.fp8_dequantize(codes, deq)
+    # Relative error of a normal E4M3 value is at most 2^-4 (3 mantissa bits, nearest).
+    big = np.abs(X) >= 2.0 ** -6 * deq[:, None, None] * 1.01
+    assert np.all(np.abs(Y - X)[big] <= 2.0 ** -4 * np.abs(X)[big] * 1.0001)
