@@ -63,6 +63,9 @@ def parse():
                         "at a time and against the dense path at the same batch")
     p.add_argument("--batch-lens", default=None,
                    help="comma-separated sequence lengths for the batch mode (overrides --batch)")
+    p.add_argument("--fp8", action="store_true",
+                   help="instead of the benchmark line: the attention stage on FP8 (E4M3) inputs over the same "
+                        "lists, against the bf16 attention and the FP8 dense path, plus the packing time")
     p.add_argument("--layer-sweep", type=int, default=0,
                    help="instead of the benchmark line: this many layers of the 128K layer schedule "
                         "(per-layer key noise and needle counts), per-layer density and times, sparse vs "
@@ -157,6 +160,8 @@ def main():
         return batch_bench(args)
     if args.layer_sweep:
         return layer_sweep(args)
+    if args.fp8:
+        return fp8_bench(args)
     w = workload(args.workload or "qwen3-30b-a3b-128k")
     _log(f"[bench] workload {w.name}: N={w.seq_len} Hq={w.n_q_heads} Hkv={w.n_kv_heads} B={w.block_size}")
     t0 = time.perf_counter()
@@ -548,6 +553,71 @@ def batch_bench(args):
         "throughput_vs_dense": round(t_dense / t_var, 3),
         "varlen_vs_single_calls": round(t_single / t_var, 3),
         "density": round(csum / pairs, 6),
+    }), flush=True)
+
+
+PEAK_FP8_TFLOPS = 5000.0     # MI355X dense FP8 MFMA, vendor figure (no sparsity)
+
+
+def fp8_bench(args):
+    """Attention on FP8 (E4M3) copies of Q, K, V (rbs_sparse_prefill_fp8) over
+    the selector's lists of the 128K layer, timed against the bf16 attention on
+    the same lists and against the FP8 dense path; the packing (amax + E4M3
+    conversion) is timed on its own, since an FP8 model's K/V cache is already
+    FP8.  One JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_2609_20971_amd as rbs
+    from synth import workload, make_inputs
+
+    w = workload(args.workload or "qwen3-30b-a3b-128k")
+    inp = make_inputs(w)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(0)
+    Q, K, V = (_upload(torch, np, inp[x], dev) for x in ("q", "k", "v"))
+    shape = rbs.make_shape(w.seq_len, w.n_q_heads, w.n_kv_heads, w.block_size)
+    stream = torch.cuda.current_stream()
+    stats = rbs.rbs_block_stats(shape, K, stream=stream)
+    counts, indices = rbs.rbs_select(shape, Q, stats, w.tau_base, w.tau_rescue, w.n_sink, w.n_local, w.n_recent,
+                                     stream=stream)
+    f8 = rbs.allocate_fp8(shape, dev)
+    O = torch.empty_like(Q)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a, b = _events(torch, 2)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    reps = max(1, args.steps)
+    t_pack = timed(lambda: rbs.rbs_fp8_prepare(shape, Q, K, V, f8, stream=stream), reps)
+    t_f8 = timed(lambda: rbs.rbs_sparse_prefill_fp8(shape, f8, counts, indices, 0.0, O, stream=stream), reps)
+    t_bf = timed(lambda: rbs.rbs_sparse_prefill(shape, Q, K, V, counts, indices, 0.0, O, stream=stream), reps)
+    dc, di = rbs.rbs_dense_indices(shape, device=dev)
+    t_f8d = timed(lambda: rbs.rbs_sparse_prefill_fp8(shape, f8, dc, di, 0.0, O, stream=stream),
+                  max(1, args.dense_reps))
+    csum = int(counts.sum().item())
+    alg = algorithmic(w, csum)
+    tf_f8 = alg["attn_flops"] / (t_f8 * 1e-3) / 1e12
+    tf_f8d = alg["dense_flops"] / (t_f8d * 1e-3) / 1e12
+    _log(f"[fp8] pack {t_pack:.3f} ms; attention fp8 {t_f8:.3f} ms ({tf_f8:.0f} TFLOP/s) vs bf16 {t_bf:.3f} ms; "
+         f"fp8 dense {t_f8d:.3f} ms ({tf_f8d:.0f} TFLOP/s)")
+    print(json.dumps({
+        "mode": "fp8", "workload": w.name, "dtype": "fp8 e4m3 (Q, K, V, P); fp32 accumulate", "data": "synthetic",
+        "steps": reps, "density": round(csum / alg["pairs"], 6),
+        "pack_ms": round(t_pack, 4), "attn_fp8_ms": round(t_f8, 4), "attn_bf16_ms": round(t_bf, 4),
+        "attn_fp8_vs_bf16": round(t_bf / t_f8, 3),
+        "attn_fp8_tflops": round(tf_f8, 1), "attn_fp8_mfma_frac": round(tf_f8 / PEAK_FP8_TFLOPS, 4),
+        "dense_fp8_ms": round(t_f8d, 3), "dense_fp8_tflops": round(tf_f8d, 1),
+        "dense_fp8_mfma_frac": round(tf_f8d / PEAK_FP8_TFLOPS, 4),
     }), flush=True)
 
 
