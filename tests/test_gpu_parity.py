@@ -124,6 +124,33 @@ def test_degenerate_radii_and_zero_queries():
     _full_check(w, inputs=inp)
 
 
+def _scaled(bits, factor):
+    from synth import bf16_bits_from_f32, f32_from_bf16_bits
+    return bf16_bits_from_f32(f32_from_bf16_bits(bits) * np.float32(factor))
+
+
+def test_large_norm_queries_take_the_shifted_selector_path():
+    """Queries 40x larger: |q| |c'| exceeds the unshifted-sum bound in every
+    tile, so every block sum takes the maximum-shifted path."""
+    w = WORKLOADS["tiny-2k"].with_(seq_len=1536, seed=31)
+    inp = make_inputs(w)
+    inp["q"] = _scaled(inp["q"], 40.0)
+    _full_check(w, inputs=inp)
+
+
+def test_mixed_shifted_and_unshifted_tiles():
+    """A few key blocks of the second 32-block tile 60x larger: rows past
+    block 32 score that tile on the shifted path and the others unshifted."""
+    w = WORKLOADS["tiny-2k"].with_(name="mixed", seq_len=6000, block_size=64, n_q_heads=4, n_kv_heads=2,
+                                   needles_per_kv_head=4, seed=32)
+    inp = make_inputs(w)
+    for b in (40, 45):
+        inp["k"][:, b * 64:(b + 1) * 64] = _scaled(inp["k"][:, b * 64:(b + 1) * 64], 60.0)
+    M = w.n_blocks
+    attn = H.sample_rows(w.n_q_heads, M, 12, seed=5, include=[(0, M - 1), (3, 45), (1, 20)])
+    _full_check(w, inputs=inp, attn_rows=attn)
+
+
 def test_dense_path_matches_dense_oracle():
     import torch
     import paper_2609_20971_amd as rbs
