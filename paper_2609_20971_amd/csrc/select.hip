@@ -7,7 +7,8 @@
 namespace rbs {
 
 template <int BS, int MODE>
-__global__ __launch_bounds__(BS * 2) void select_kernel(SelectCore c, int Hq) {
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(MODE == kSelectBox ? 3 : 4))) void select_kernel(
+    SelectCore c, int Hq) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int work = blockIdx.x;
   const int i = c.M - 1 - work / Hq;  // late (long) rows first
@@ -20,7 +21,8 @@ __global__ __launch_bounds__(BS * 2) void select_kernel(SelectCore c, int Hq) {
 // its tokens, blocks, counts and list slots (the head strides stay the
 // batch's).
 template <int BS>
-__global__ __launch_bounds__(BS * 2) void select_varlen_kernel(SelectCore c, int Hq, const SeqTable t) {
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(4))) void select_varlen_kernel(
+    SelectCore c, int Hq, const SeqTable t) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int work = blockIdx.x;
   const int sq = seq_of(t.blk, t.n, work / Hq);

@@ -29,6 +29,14 @@ namespace rbs {
 
 constexpr int kTile = 32;  // centroids per tile
 constexpr float kPlainBound = 120.0f;  // |exponent| bound for unshifted exp2 sums (fp32 normal range: 2^-126)
+constexpr float kCandSlack = 1e-2f;    // log2 units: rounding allowance of the rescue-candidate test
+
+// Branches a tile pass scores.
+template <bool BASE, bool RES>
+struct TilePass {
+  static constexpr bool base = BASE;
+  static constexpr bool res = RES;
+};
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
 
@@ -64,7 +72,7 @@ struct SelectCore {
 template <int BS, int MODE = kSelectDual>
 constexpr size_t select_smem_bytes(int M) {
   return (MODE == kSelectBox ? 4 : 2) * kTile * 256 + 2 * (BS / 32) * kTile * 16 + BS * 4 + 2 * (size_t)M * 4 +
-         3 * (BS / 32) * 4 + (MODE == kSelectBox ? 2 * (BS / 32) * 4 : 0);
+         3 * (BS / 32) * 4 + (MODE == kSelectBox ? 2 * (BS / 32) * 4 : 0) + (MODE == kSelectDual ? (size_t)M * 4 : 0);
 }
 
 // Selection of query block i of query head h by the B/32 waves of the calling
@@ -79,7 +87,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   const uint16_t* __restrict__ Q = c.Q;
   const int N = c.N, M = c.M;
   // Layout: cbuf[2][32 rows][16 chunks of 8 f16] (| hbuf[2][32][16], box) | stage[2][NW][32][4] | nq[BS] |
-  // L_base[M] | L_res[M] | red_f[2 NW] | red_i[NW] (| cnt[2][NW], box)
+  // L_base[M] | L_res[M] | red_f[2 NW] | red_i[NW] (| cnt[2][NW], box) (| cand[M], dual)
   constexpr int kTileBufs = MODE == kSelectBox ? 4 : 2;
   f16x8* cbuf = reinterpret_cast<f16x8*>(smem_raw);
   f16x8* hbuf = cbuf + 2 * kTile * 16;
@@ -89,6 +97,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   float* L_res = L_base + M;
   float* red_f = L_res + M;
   int* red_i = reinterpret_cast<int*>(red_f + 2 * NW);
+  int* cand = red_i + NW;  // dual: blocks whose rescue score is computed
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
@@ -127,58 +136,28 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   sq += wave_xor_f(sq, 32);
   const float nq = sqrtf(sq);
   if (half == 0) nq_s[t_local] = nq;
-  float nq_max = row_ok ? nq : 0.f;
+  float nq_max = row_ok ? nq : 0.f, nq_mn = row_ok ? nq : INFINITY;
 #pragma unroll
-  for (int m = 1; m < 64; m <<= 1) nq_max = fmaxf(nq_max, wave_xor_f(nq_max, m));
+  for (int m = 1; m < 64; m <<= 1) {
+    nq_max = fmaxf(nq_max, wave_xor_f(nq_max, m));
+    nq_mn = fminf(nq_mn, wave_xor_f(nq_mn, m));
+  }
   const bool wave_active = 32 * wave < nb;
   const bool wave_partial = 32 * wave + 32 > nb;
 
-  // ---- Stage centroid tile 0.
-  const int ld_row = tid >> 4, ld_chunk = tid & 15;  // NT >= 128 threads: rows ld_row, ld_row + NT/16, ...
-  constexpr int kLdRowsPerPass = NT / 16;
-  constexpr int kLdPasses = (kTile + kLdRowsPerPass - 1) / kLdRowsPerPass;
-  // Every load is issued without a branch: rows past the last block read
-  // block M - 1 (their lanes' results are never used), so no loaded value is
-  // merged at a branch join, where the compiler would wait for all loads in
-  // flight.  Vector types, not uint4: a struct copied from memory stays a
-  // memcpy that keeps the array out of registers.
-  constexpr bool kRescue = MODE == kSelectDual || MODE == kSelectFullL2;
-  f16x8 pre[kLdPasses];
-  f16x8 preh[MODE == kSelectBox ? kLdPasses : 1];
-  float u_next = 0.f;   // uplift (or radius) of this lane's centroid in the next tile
-  float cn_next = 0.f;  // and the norm of its scaled centroid (dual)
-  auto fetch = [&](int tile) __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < kLdPasses; ++p) {
-      const int bb = min(tile * kTile + ld_row + p * kLdRowsPerPass, M - 1);
-      pre[p] = *reinterpret_cast<const f16x8*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk);
-      if constexpr (MODE == kSelectBox)
-        preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)bb * kHeadDim + 8 * ld_chunk);
-    }
-    if constexpr (kRescue) u_next = ug[min(tile * kTile + l32, M - 1)];
-    if constexpr (MODE == kSelectDual) cn_next = cng[min(tile * kTile + l32, M - 1)];
-  };
-  auto store = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < kLdPasses; ++p) {
-      const int r = ld_row + p * kLdRowsPerPass;
-      if (r < kTile) {
-        cbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = pre[p];
-        if constexpr (MODE == kSelectBox) hbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = preh[p];
-      }
-    }
-  };
-  fetch(0);
-  store(0);
-  float u_cur = u_next, cn_cur = cn_next;
-  if (lane == 0) red_f[wave] = nq_max;
+  // Largest and smallest |q| of the query block, and per element the token's
+  // |q| minus the largest (the rescue exponent offsets, <= 0).
+  if (lane == 0) {
+    red_f[wave] = nq_max;
+    red_f[NW + wave] = nq_mn;
+  }
   __syncthreads();
-
-  // Largest |q| of the query block, and per element the token's |q| minus it
-  // (the rescue exponent offsets, <= 0).
-  float nq_row = red_f[0];
+  float nq_row = red_f[0], nq_min = red_f[NW];
 #pragma unroll
-  for (int w = 1; w < NW; ++w) nq_row = fmaxf(nq_row, red_f[w]);
+  for (int w = 1; w < NW; ++w) {
+    nq_row = fmaxf(nq_row, red_f[w]);
+    nq_min = fminf(nq_min, red_f[NW + w]);
+  }
   float nqd[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
@@ -186,120 +165,230 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     nqd[r] = (t < nb) ? nq_s[t] - nq_row : 0.f;
   }
 
-  for (int tile = 0; tile < n_tiles; ++tile) {
-    const int buf = tile & 1;
-    if (tile + 1 < n_tiles) fetch(tile + 1);
-    const int b = tile * kTile + l32;
-    // The dual selector skips the per-block shift when every exponent of the
-    // tile is bounded: with |q_t . c'_b| <= |q_t| |c'_b| (Cauchy-Schwarz) and
-    // u_b >= 0, the logits and rescue logits lie in
-    // [-nq_row (|c'_b| + u_b), nq_row |c'_b|], and within +-kPlainBound exp2
-    // neither overflows nor leaves the normal range.  Every wave of the
-    // workgroup reads the same values, so all take the same path.
-    bool plain_tile = false;
-    if constexpr (MODE == kSelectDual)
-      plain_tile = __all(b >= n_cand || nq_row * (cn_cur + u_cur) <= kPlainBound);
-    if (wave_active) {
-      f32x16 acc = {};
-      const f16x8* cb = cbuf + buf * kTile * 16 + l32 * 16;
+  // ---- Tile passes.  A pass scores tiles of 32 key blocks staged through LDS
+  // (double buffered, one barrier per tile); id_at(t, r) is the block of row r
+  // of tile t, or -1.  The flags choose the branches whose scores it merges
+  // into L_base / L_res.  Every load is issued without a branch (a padding row
+  // reads block 0; its lane's results are never used), so no loaded value is
+  // merged at a branch join, where the compiler would wait for all loads in
+  // flight.  Vector types, not uint4: a struct copied from memory stays a
+  // memcpy that keeps the array out of registers.
+  const int ld_row = tid >> 4, ld_chunk = tid & 15;  // NT >= 128 threads: rows ld_row, ld_row + NT/16, ...
+  constexpr int kLdRowsPerPass = NT / 16;
+  constexpr int kLdPasses = (kTile + kLdRowsPerPass - 1) / kLdRowsPerPass;
+  constexpr bool kRescue = MODE == kSelectDual || MODE == kSelectFullL2;
+  f16x8 pre[kLdPasses];
+  f16x8 preh[MODE == kSelectBox ? kLdPasses : 1];
+  float u_next = 0.f;   // uplift (or radius) of this lane's centroid in the next tile
+  float cn_next = 0.f;  // and the norm of its scaled centroid (dual)
+
+  auto run_pass = [&](int n_tiles_p, auto id_at, auto flags) __attribute__((always_inline)) {
+    constexpr bool BASE = decltype(flags)::base;
+    constexpr bool RES = decltype(flags)::res;
+    auto fetch = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qa[ks], cb[swz(l32, 2 * ks + half)], acc);
-      if constexpr (MODE == kSelectBox) {
-        // + |q| . h_b: Eq. quest_box written as q . v_b + |q|^T h_b.
-        const f16x8* hb = hbuf + buf * kTile * 16 + l32 * 16;
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qabs[ks], hb[swz(l32, 2 * ks + half)], acc);
+      for (int p = 0; p < kLdPasses; ++p) {
+        const int bb = max(id_at(tile, ld_row + p * kLdRowsPerPass), 0);
+        pre[p] = *reinterpret_cast<const f16x8*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk);
+        if constexpr (MODE == kSelectBox)
+          preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)bb * kHeadDim + 8 * ld_chunk);
       }
-      if (wave_partial) {
+      const int lb = max(id_at(tile, l32), 0);
+      if constexpr (kRescue) u_next = ug[lb];
+      if constexpr (MODE == kSelectDual) cn_next = cng[lb];
+    };
+    auto store = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (32 * wave + mfma_row(r, lane) >= nb) acc[r] = -INFINITY;
-      }
-      // Per lane (key block b) and branch, a (shift, sum of exp2) pair over
-      // this wave's tokens: S_b = exp2(shift) * sum.
-      const bool plain = plain_tile;
-      float mx = 0.f, sb = 0.f;
-      if (plain) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r]);
-      } else {
-        mx = acc[0];
-#pragma unroll
-        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, acc[r]);
-        mx = half_max(mx);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
-      }
-      float mr = mx, sr = sb;
-      if constexpr (MODE == kSelectCentroid || MODE == kSelectBox) {
-        mr = -INFINITY;  // single branch: no rescue scores
-        sr = 0.f;
-      }
-      // Lanes past the candidates take u = 0: the rescue pass runs only
-      // when a candidate of the tile needs it.  Rescue logit of token t:
-      // acc + |q_t| u = nq_row u + (acc + nqd u).
-      const float u = kRescue && b < n_cand ? u_cur * u_scale : 0.f;
-      if (kRescue && __any(u != 0.f)) {
-        sr = 0.f;
-        if (plain) {
-          mr = nq_row * u;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sr += fast_exp2(fmaf(nqd[r], u, acc[r]));
-        } else {
-          float v[16];
-          float mv = -INFINITY;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            v[r] = fmaf(nqd[r], u, acc[r]);
-            mv = fmaxf(mv, v[r]);
-          }
-          mv = half_max(mv);
-          mr = mv + nq_row * u;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sr += fast_exp2(v[r] - mv);
+      for (int p = 0; p < kLdPasses; ++p) {
+        const int r = ld_row + p * kLdRowsPerPass;
+        if (r < kTile) {
+          cbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = pre[p];
+          if constexpr (MODE == kSelectBox) hbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = preh[p];
         }
       }
-      sb = half_sum(sb);
-      sr = half_sum(sr);
-      if (half == 0) stage[(buf * NW + wave) * kTile + l32] = make_float4(mx, sb, mr, sr);
-    } else if (half == 0) {
-      stage[(buf * NW + wave) * kTile + l32] = make_float4(-INFINITY, 0.f, -INFINITY, 0.f);
+    };
+    if (n_tiles_p == 0) {
+      __syncthreads();  // a pass always ends at a barrier: its callers read LDS written before it
+      return;
     }
-    if (tile + 1 < n_tiles) store(buf ^ 1);
-    u_cur = u_next;
-    cn_cur = cn_next;
+    fetch(0);
+    store(0);
+    float u_cur = u_next, cn_cur = cn_next;
     __syncthreads();
-    // Merge the waves' partial sums of this tile (lanes 0-31 base, 32-63
-    // rescue), by one wave in turn: the waves of a workgroup sit on different
-    // SIMDs, and a fixed merging wave would load one SIMD more than the rest.
-    if (wave == (tile & (NW - 1)) && b < n_cand && plain_tile) {
-      // Every wave used the same shift: S_b = exp2(shift) * (sum of the sums).
-      float sum = 0.f;
+    for (int tile = 0; tile < n_tiles_p; ++tile) {
+      const int buf = tile & 1;
+      if (tile + 1 < n_tiles_p) fetch(tile + 1);
+      const int b = id_at(tile, l32);
+      // The dual selector skips the per-block shift when every exponent of
+      // the tile is bounded: with |q_t . c'_b| <= |q_t| |c'_b| (Cauchy-Schwarz)
+      // and u_b >= 0, the logits and rescue logits lie in
+      // [-nq_row (|c'_b| + u_b), nq_row |c'_b|], and within +-kPlainBound exp2
+      // neither overflows nor leaves the normal range.  Every wave of the
+      // workgroup reads the same values, so all take the same path.
+      bool plain_tile = false;
+      if constexpr (MODE == kSelectDual) plain_tile = __all(b < 0 || nq_row * (cn_cur + u_cur) <= kPlainBound);
+      if (wave_active) {
+        f32x16 acc = {};
+        const f16x8* cb = cbuf + buf * kTile * 16 + l32 * 16;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        const float4 p = stage[(buf * NW + w) * kTile + l32];
-        sum += half ? p.w : p.y;
-      }
-      const float4 p0 = stage[(buf * NW) * kTile + l32];  // wave 0 is always active
-      (half ? L_res : L_base)[b] = (half ? p0.z : p0.x) + log2f(sum);
-    } else if (wave == (tile & (NW - 1)) && b < n_cand) {
-      float top = -INFINITY;
+        for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qa[ks], cb[swz(l32, 2 * ks + half)], acc);
+        if constexpr (MODE == kSelectBox) {
+          // + |q| . h_b: Eq. quest_box written as q . v_b + |q|^T h_b.
+          const f16x8* hb = hbuf + buf * kTile * 16 + l32 * 16;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        const float4 p = stage[(buf * NW + w) * kTile + l32];
-        top = fmaxf(top, half ? p.z : p.x);
-      }
-      float sum = 0.f;
+          for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qabs[ks], hb[swz(l32, 2 * ks + half)], acc);
+        }
+        if (wave_partial) {
 #pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        const float4 p = stage[(buf * NW + w) * kTile + l32];
-        const float m = half ? p.z : p.x, sv = half ? p.w : p.y;
-        if (sv > 0.f) sum += sv * fast_exp2(m - top);
+          for (int r = 0; r < 16; ++r)
+            if (32 * wave + mfma_row(r, lane) >= nb) acc[r] = -INFINITY;
+        }
+        // Per lane (key block b) and branch, a (shift, sum of exp2) pair over
+        // this wave's tokens: S_b = exp2(shift) * sum.
+        float mx = -INFINITY, sb = 0.f, mr = -INFINITY, sr = 0.f;
+        if constexpr (BASE) {
+          if (plain_tile) {
+            mx = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r]);
+          } else {
+            mx = acc[0];
+#pragma unroll
+            for (int r = 1; r < 16; ++r) mx = fmaxf(mx, acc[r]);
+            mx = half_max(mx);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
+          }
+          sb = half_sum(sb);
+        }
+        if constexpr (RES) {
+          // Rescue logit of token t: acc + |q_t| u = nq_row u + (acc + nqd u).
+          const float u = b >= 0 ? u_cur * u_scale : 0.f;
+          if (plain_tile) {
+            mr = nq_row * u;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sr += fast_exp2(fmaf(nqd[r], u, acc[r]));
+          } else {
+            float v[16];
+            float mv = -INFINITY;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              v[r] = fmaf(nqd[r], u, acc[r]);
+              mv = fmaxf(mv, v[r]);
+            }
+            mv = half_max(mv);
+            mr = mv + nq_row * u;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sr += fast_exp2(v[r] - mv);
+          }
+          sr = half_sum(sr);
+        }
+        if (half == 0) stage[(buf * NW + wave) * kTile + l32] = make_float4(mx, sb, mr, sr);
+      } else if (half == 0) {
+        stage[(buf * NW + wave) * kTile + l32] = make_float4(-INFINITY, 0.f, -INFINITY, 0.f);
       }
-      (half ? L_res : L_base)[b] = top + log2f(sum);
+      if (tile + 1 < n_tiles_p) store(buf ^ 1);
+      u_cur = u_next;
+      cn_cur = cn_next;
+      __syncthreads();
+      // Merge the waves' partial sums of this tile (lanes 0-31 base, 32-63
+      // rescue), by one wave in turn: the waves of a workgroup sit on
+      // different SIMDs, and a fixed merging wave would load one SIMD more.
+      const bool mine = wave == (tile & (NW - 1)) && b >= 0 && (half ? RES : BASE);
+      if (mine && plain_tile) {
+        // Every wave used the same shift: S_b = exp2(shift) * (sum of the sums).
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+          const float4 p = stage[(buf * NW + w) * kTile + l32];
+          sum += half ? p.w : p.y;
+        }
+        const float4 p0 = stage[(buf * NW) * kTile + l32];  // wave 0 is always active
+        (half ? L_res : L_base)[b] = (half ? p0.z : p0.x) + log2f(sum);
+      } else if (mine) {
+        float top = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+          const float4 p = stage[(buf * NW + w) * kTile + l32];
+          top = fmaxf(top, half ? p.z : p.x);
+        }
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+          const float4 p = stage[(buf * NW + w) * kTile + l32];
+          const float m = half ? p.z : p.x, sv = half ? p.w : p.y;
+          if (sv > 0.f) sum += sv * fast_exp2(m - top);
+        }
+        (half ? L_res : L_base)[b] = top + log2f(sum);
+      }
     }
+    __syncthreads();
+  };
+
+  auto all_blocks = [&](int t, int r) __attribute__((always_inline)) {
+    const int s = t * kTile + r;
+    return s < n_cand ? s : -1;
+  };
+  if constexpr (MODE == kSelectDual) {
+    // Base scores of every candidate first.  The rescue branch then scores only
+    // the blocks that can reach its threshold: every token's rescue logit lies
+    // between its base logit plus nq_min u_b and plus nq_row u_b, so
+    // L_res(b) <= U(b) = L_base(b) + nq_row u_b, and the row's largest rescue
+    // score is at least LB = max_b L_base(b) + nq_min u_b.  A block with
+    // U(b) < LB + log2 tau_rescue can be neither selected by the rescue branch
+    // nor its maximum; a block with u_b = 0 has L_res(b) = L_base(b).  The
+    // remaining blocks (a few percent) get their exact rescue scores.
+    run_pass(n_tiles, all_blocks, TilePass<true, false>{});
+    int n_c = 0;
+    if (c.rescue_all) {
+      for (int b = tid; b < n_cand; b += NT) L_res[b] = L_base[b];  // every block passes: scores unused
+    } else {
+      float lbv = -INFINITY;
+      for (int b = tid; b < n_cand; b += NT) lbv = fmaxf(lbv, L_base[b] + nq_min * ug[b]);
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) lbv = fmaxf(lbv, wave_xor_f(lbv, m));
+      if (lane == 0) red_f[wave] = lbv;
+      __syncthreads();
+      float LB = red_f[0];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) LB = fmaxf(LB, red_f[w]);
+      const float cut = LB + c.log2_tau_rescue - kCandSlack;
+      for (int base = 0; base < n_cand; base += NT) {
+        const int b = base + tid;
+        bool is_cand = false;
+        if (b < n_cand) {
+          const float u = ug[b], lbase = L_base[b];
+          is_cand = u > 0.f && lbase + nq_row * u >= cut;
+          L_res[b] = u > 0.f ? -INFINITY : lbase;  // candidates get their exact score below
+        }
+        const uint64_t ballot = __ballot(is_cand);
+        const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(ballot >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)ballot, 0u));
+        if (lane == 0) red_i[wave] = __popcll(ballot);
+        __syncthreads();
+        int off = n_c, pass_total = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+          const int cw = red_i[w];
+          if (w < wave) off += cw;
+          pass_total += cw;
+        }
+        if (is_cand) cand[off + before] = b;
+        n_c += pass_total;
+        __syncthreads();
+      }
+    }
+    run_pass((n_c + kTile - 1) / kTile,
+             [&](int t, int r) __attribute__((always_inline)) {
+               const int s = t * kTile + r;
+               return s < n_c ? cand[s] : -1;
+             },
+             TilePass<false, true>{});
+  } else if constexpr (MODE == kSelectFullL2) {
+    run_pass(n_tiles, all_blocks, TilePass<false, true>{});
+  } else {
+    run_pass(n_tiles, all_blocks, TilePass<true, false>{});
   }
-  __syncthreads();
 
   // ---- Row maxima of both branches.
   float mb = -INFINITY, mres = -INFINITY;
