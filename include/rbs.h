@@ -101,6 +101,23 @@ size_t rbs_summary_bytes(const rbs_shape* shape);
  * room for i + 1 entries. */
 int64_t rbs_index_capacity(int32_t n_blocks);
 
+/* Workspace of the attention calls (rbs_sparse_prefill, _varlen, _fp8):
+ * RBS_ATTN_WORKSPACE_BYTES of device memory, 16-byte aligned, or NULL.
+ *   NULL      one workgroup per (query head, query block);
+ *   non-NULL  a persistent grid (as many workgroups as the GPU holds at once)
+ *             takes the same (query head, query block) items from per-XCD work
+ *             queues held in the workspace.  Each XCD runs the same items in
+ *             the same order as with NULL, so results are bit-identical; the
+ *             launch avoids the idle workgroup slots that in-order dispatch of
+ *             rows of very different lengths leaves (a sparse selection's
+ *             rows differ by an order of magnitude).
+ * The call resets the queues itself (with a kernel on `stream`, no memset):
+ * contents on entry are ignored and undefined afterwards.  The workspace is
+ * written by the call like an output, so calls that share one must be
+ * ordered (the same stream, or events between streams). */
+#define RBS_ATTN_WORKSPACE_BYTES 256
+size_t rbs_attention_workspace_bytes(void);
+
 /*
  * Stage 1 (Sec. 3.1; Algorithm 1, statistics loops).
  * K: bf16 [H_kv][N][d].  Fills every field of *stats: one pass over K for the
@@ -139,10 +156,11 @@ int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats,
  * softmax_scale <= 0 selects 1/sqrt(d).  lse (optional, NULL to skip): fp32
  * [H_q][N] natural-log sum of exp(scaled logits) per query (-inf when a query
  * has no retained key, in which case its output row is zero).
+ * workspace: NULL or RBS_ATTN_WORKSPACE_BYTES (see rbs_attention_workspace_bytes).
  */
 int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, const void* V,
                        const int32_t* counts, const int32_t* indices, float softmax_scale,
-                       void* O, float* lse, void* stream);
+                       void* O, float* lse, void* workspace, void* stream);
 
 /* rbs_select then rbs_sparse_prefill in one pass (Algorithm 1, selection loop
  * and attention; Sec. 3.2-3.3): each (query head, query block) selects its key
@@ -234,7 +252,7 @@ int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const voi
                  void* Q8, void* K8, void* V8t, void* stream);
 int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K8, const void* V8t,
                            const float* amax, const int32_t* counts, const int32_t* indices,
-                           float softmax_scale, void* O, float* lse, void* stream);
+                           float softmax_scale, void* O, float* lse, void* workspace, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Batches of independent sequences (varlen).  The paper runs batched prompts
@@ -282,7 +300,7 @@ int rbs_select_varlen(const rbs_shape* shape, const rbs_batch* batch, const void
                       int32_t* counts, int32_t* indices, void* stream);
 int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* Q, const void* K,
                               const void* V, const int32_t* counts, const int32_t* indices,
-                              float softmax_scale, void* O, float* lse, void* stream);
+                              float softmax_scale, void* O, float* lse, void* workspace, void* stream);
 int rbs_dense_indices_varlen(const rbs_shape* shape, const rbs_batch* batch, int32_t* counts,
                              int32_t* indices, void* stream);
 

@@ -11,6 +11,8 @@
 """
 
 from ._lib import (  # noqa: F401
+    AUTO,
+    attention_workspace,
     Fp8Inputs,
     allocate_fp8,
     rbs_fp8_amax,

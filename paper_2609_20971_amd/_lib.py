@@ -87,7 +87,9 @@ def load() -> ctypes.CDLL:
     lib.rbs_block_stats.restype = ctypes.c_int
     lib.rbs_select.argtypes = [SP, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, P, P, P]
     lib.rbs_select.restype = ctypes.c_int
-    lib.rbs_sparse_prefill.argtypes = [SP, P, P, P, P, P, F32, P, P, P]
+    lib.rbs_attention_workspace_bytes.argtypes = []
+    lib.rbs_attention_workspace_bytes.restype = SZ
+    lib.rbs_sparse_prefill.argtypes = [SP, P, P, P, P, P, F32, P, P, P, P]
     lib.rbs_sparse_prefill.restype = ctypes.c_int
     lib.rbs_select_attend.argtypes = [SP, P, P, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, F32, P, P, P,
                                       P, P]
@@ -107,7 +109,7 @@ def load() -> ctypes.CDLL:
     lib.rbs_fp8_amax.restype = ctypes.c_int
     lib.rbs_fp8_pack.argtypes = [SP, P, P, P, P, P, P, P, P]
     lib.rbs_fp8_pack.restype = ctypes.c_int
-    lib.rbs_sparse_prefill_fp8.argtypes = [SP, P, P, P, P, P, P, F32, P, P, P]
+    lib.rbs_sparse_prefill_fp8.argtypes = [SP, P, P, P, P, P, P, F32, P, P, P, P]
     lib.rbs_sparse_prefill_fp8.restype = ctypes.c_int
     BP = ctypes.POINTER(rbs_batch)
     lib.rbs_varlen_blocks.argtypes = [SP, BP]
@@ -120,7 +122,7 @@ def load() -> ctypes.CDLL:
     lib.rbs_block_stats_varlen.restype = ctypes.c_int
     lib.rbs_select_varlen.argtypes = [SP, BP, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, P, P, P]
     lib.rbs_select_varlen.restype = ctypes.c_int
-    lib.rbs_sparse_prefill_varlen.argtypes = [SP, BP, P, P, P, P, P, F32, P, P, P]
+    lib.rbs_sparse_prefill_varlen.argtypes = [SP, BP, P, P, P, P, P, F32, P, P, P, P]
     lib.rbs_sparse_prefill_varlen.restype = ctypes.c_int
     lib.rbs_dense_indices_varlen.argtypes = [SP, BP, P, P, P]
     lib.rbs_dense_indices_varlen.restype = ctypes.c_int
@@ -147,6 +149,36 @@ def _stream(stream) -> int | None:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+# Attention workspace argument: AUTO takes one cached per (device, stream) --
+# calls on one stream are ordered, so they may share it --; None asks for the
+# one-workgroup-per-item launch; a tensor of at least
+# rbs_attention_workspace_bytes() bytes is used as given.
+AUTO = "auto"
+_workspaces: dict = {}
+
+
+def attention_workspace(device, stream=None) -> torch.Tensor:
+    device = torch.device(device)
+    index = device.index if device.index is not None else torch.cuda.current_device()
+    key = (index, _stream(stream))
+    ws = _workspaces.get(key)
+    if ws is None:
+        n = int(load().rbs_attention_workspace_bytes())
+        ws = torch.zeros(n // 4, dtype=torch.int32, device=torch.device("cuda", index))
+        _workspaces[key] = ws
+    return ws
+
+
+def _workspace(workspace, device, stream):
+    if isinstance(workspace, str):
+        if workspace != AUTO:
+            raise ValueError(f"workspace must be AUTO, None or a tensor, not {workspace!r}")
+        return attention_workspace(device, stream)
+    if workspace is not None and workspace.numel() * workspace.element_size() < load().rbs_attention_workspace_bytes():
+        raise ValueError("workspace is smaller than rbs_attention_workspace_bytes()")
+    return workspace
 
 
 def make_shape(n_tokens: int, n_q_heads: int, n_kv_heads: int, block_size: int, head_dim: int = 128) -> rbs_shape:
@@ -266,13 +298,14 @@ def rbs_select(shape: rbs_shape, Q: torch.Tensor, stats: BlockStats, tau_base: f
 
 
 def rbs_sparse_prefill(shape: rbs_shape, Q, K, V, counts, indices, softmax_scale: float = 0.0, O=None,
-                       lse=None, stream=None):
+                       lse=None, stream=None, workspace=AUTO):
     """Stage 3: causal GQA block-sparse attention; returns O (bf16 [H_q][N][d])."""
     if O is None:
         O = torch.empty_like(Q)
+    ws = _workspace(workspace, Q.device, stream)
     _check("rbs_sparse_prefill", load().rbs_sparse_prefill(ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V),
                                                            _ptr(counts), _ptr(indices), float(softmax_scale),
-                                                           _ptr(O), _ptr(lse), _stream(stream)))
+                                                           _ptr(O), _ptr(lse), _ptr(ws), _stream(stream)))
     return O
 
 
@@ -393,13 +426,14 @@ def rbs_select_varlen(shape: rbs_shape, batch: Batch, Q: torch.Tensor, stats: Bl
 
 
 def rbs_sparse_prefill_varlen(shape: rbs_shape, batch: Batch, Q, K, V, counts, indices, softmax_scale: float = 0.0,
-                              O=None, lse=None, stream=None):
+                              O=None, lse=None, stream=None, workspace=AUTO):
     """Stage 3 for every sequence of a batch (one launch); returns O."""
     if O is None:
         O = torch.empty_like(Q)
+    ws = _workspace(workspace, Q.device, stream)
     _check("rbs_sparse_prefill_varlen", load().rbs_sparse_prefill_varlen(
         ctypes.byref(shape), ctypes.byref(batch.c), _ptr(Q), _ptr(K), _ptr(V), _ptr(counts), _ptr(indices),
-        float(softmax_scale), _ptr(O), _ptr(lse), _stream(stream)))
+        float(softmax_scale), _ptr(O), _ptr(lse), _ptr(ws), _stream(stream)))
     return O
 
 
@@ -460,12 +494,13 @@ def rbs_fp8_prepare(shape: rbs_shape, Q, K, V, f8: Fp8Inputs | None = None, stre
 
 
 def rbs_sparse_prefill_fp8(shape: rbs_shape, f8: Fp8Inputs, counts, indices, softmax_scale: float = 0.0, O=None,
-                           lse=None, stream=None):
+                           lse=None, stream=None, workspace=AUTO):
     """Stage 3 on the E4M3 inputs; returns O (bf16 [H_q][N][d])."""
     if O is None:
         O = torch.empty((shape.n_q_heads, shape.n_tokens, shape.head_dim), dtype=torch.bfloat16,
                         device=f8.Q8.device)
+    ws = _workspace(workspace, f8.Q8.device, stream)
     _check("rbs_sparse_prefill_fp8", load().rbs_sparse_prefill_fp8(
         ctypes.byref(shape), _ptr(f8.Q8), _ptr(f8.K8), _ptr(f8.V8t), _ptr(f8.amax), _ptr(counts), _ptr(indices),
-        float(softmax_scale), _ptr(O), _ptr(lse), _stream(stream)))
+        float(softmax_scale), _ptr(O), _ptr(lse), _ptr(ws), _stream(stream)))
     return O

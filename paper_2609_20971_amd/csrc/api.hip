@@ -49,6 +49,7 @@ int check_batch(const rbs_shape* s, const rbs_batch* b, rbs::SeqTable* t) {
   if (s->n_q_heads < 1 || s->n_kv_heads < 1 || s->n_q_heads % s->n_kv_heads != 0) return RBS_ERR_SHAPE;
   if (b->n_seqs < 1 || b->n_seqs > RBS_MAX_SEQS) return RBS_ERR_SHAPE;
   static_assert(RBS_MAX_SEQS == rbs::kMaxSeqs, "sequence table size");
+  static_assert(RBS_ATTN_WORKSPACE_BYTES == rbs::kQueueInts * sizeof(int), "attention workspace size");
   *t = rbs::SeqTable{};
   t->n = b->n_seqs;
   int64_t tok = 0, blk = 0, cap = 0;
@@ -87,6 +88,8 @@ int64_t rbs_index_capacity(int32_t n_blocks) {
   if (n_blocks < 0) return 0;
   return (int64_t)n_blocks * (n_blocks + 1) / 2;
 }
+
+size_t rbs_attention_workspace_bytes(void) { return RBS_ATTN_WORKSPACE_BYTES; }
 
 int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stats, void* stream) {
   int rc = check_shape(shape);
@@ -148,14 +151,15 @@ int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats, fl
 }
 
 int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, const void* V, const int32_t* counts,
-                       const int32_t* indices, float softmax_scale, void* O, float* lse, void* stream) {
+                       const int32_t* indices, float softmax_scale, void* O, float* lse, void* workspace,
+                       void* stream) {
   int rc = check_shape(shape);
   if (rc != RBS_OK) return rc;
   if (Q == nullptr || K == nullptr || V == nullptr || counts == nullptr || indices == nullptr || O == nullptr)
     return RBS_ERR_NULL;
   if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(counts) || !aligned16(indices) ||
-      !aligned16(O) || (lse != nullptr && !aligned16(lse)))
+      !aligned16(O) || (lse != nullptr && !aligned16(lse)) || (workspace != nullptr && !aligned16(workspace)))
     return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
   rbs::AttnArgs a;
@@ -173,6 +177,7 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
   a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   a.O = static_cast<uint16_t*>(O);
   a.lse = lse;
+  a.queue = static_cast<int*>(workspace);
   return from_hip(rbs::launch_attention(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -398,7 +403,7 @@ int rbs_select_varlen(const rbs_shape* shape, const rbs_batch* batch, const void
 
 int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* Q, const void* K,
                               const void* V, const int32_t* counts, const int32_t* indices, float softmax_scale,
-                              void* O, float* lse, void* stream) {
+                              void* O, float* lse, void* workspace, void* stream) {
   rbs::SeqTable t;
   int rc = check_batch(shape, batch, &t);
   if (rc != RBS_OK) return rc;
@@ -406,7 +411,7 @@ int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, co
     return RBS_ERR_NULL;
   if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(counts) || !aligned16(indices) ||
-      !aligned16(O) || (lse != nullptr && !aligned16(lse)))
+      !aligned16(O) || (lse != nullptr && !aligned16(lse)) || (workspace != nullptr && !aligned16(workspace)))
     return RBS_ERR_ALIGN;
   rbs::AttnArgs a;
   a.Q = static_cast<const uint16_t*>(Q);
@@ -423,6 +428,7 @@ int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, co
   a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   a.O = static_cast<uint16_t*>(O);
   a.lse = lse;
+  a.queue = static_cast<int*>(workspace);
   return from_hip(rbs::launch_attention_varlen(a, t, static_cast<hipStream_t>(stream)));
 }
 
@@ -472,7 +478,7 @@ int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const voi
 
 int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K8, const void* V8t,
                            const float* amax, const int32_t* counts, const int32_t* indices, float softmax_scale,
-                           void* O, float* lse, void* stream) {
+                           void* O, float* lse, void* workspace, void* stream) {
   int rc = check_shape(shape);
   if (rc != RBS_OK) return rc;
   if (shape->block_size != 128) return RBS_ERR_UNSUPPORTED;
@@ -481,14 +487,15 @@ int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K
     return RBS_ERR_NULL;
   if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
   if (!aligned16(Q8) || !aligned16(K8) || !aligned16(V8t) || !aligned16(amax) || !aligned16(counts) ||
-      !aligned16(indices) || !aligned16(O) || (lse != nullptr && !aligned16(lse)))
+      !aligned16(indices) || !aligned16(O) || (lse != nullptr && !aligned16(lse)) ||
+      (workspace != nullptr && !aligned16(workspace)))
     return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   return from_hip(rbs::launch_attention_fp8(
       static_cast<const uint8_t*>(Q8), static_cast<const uint8_t*>(K8), static_cast<const uint8_t*>(V8t), amax,
       shape->n_tokens, shape->n_q_heads, shape->n_kv_heads, M, counts, indices, rbs_index_capacity(M), scale,
-      static_cast<uint16_t*>(O), lse, static_cast<hipStream_t>(stream)));
+      static_cast<uint16_t*>(O), lse, static_cast<int*>(workspace), static_cast<hipStream_t>(stream)));
 }
 
 const char* rbs_status_str(int status) {

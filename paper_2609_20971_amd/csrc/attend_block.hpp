@@ -286,15 +286,77 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
 }
 
 
-// Workgroup id -> (query head, query block): KV-group-major, late rows first
-// within a group, the group's query heads adjacent (and on one XCD).
-__device__ __forceinline__ void work_item(int M, int group, int& h, int& i) {
-  const int work = xcd_remap(blockIdx.x, gridDim.x);
+// Work slot id (of total) -> (query head, query block): KV-group-major, late
+// rows first within a group, the group's query heads adjacent (and, through
+// xcd_remap, on one XCD).
+__device__ __forceinline__ void work_of(int id, int total, int M, int group, int& h, int& i) {
+  const int work = xcd_remap(id, total);
   const int per_group = M * group;
   const int g = work / per_group;
   const int rem = work - g * per_group;
   i = M - 1 - rem / group;
   h = g * group + rem % group;
+}
+
+// One workgroup per work slot: the slot is the workgroup id.
+__device__ __forceinline__ void work_item(int M, int group, int& h, int& i) {
+  work_of(blockIdx.x, gridDim.x, M, group, h, i);
+}
+
+// Work queues of the persistent launches.  The hardware sends workgroup j to
+// XCD j % 8, and a one-workgroup-per-slot launch runs slot s on XCD s % 8.  A
+// persistent launch keeps that placement: workgroup j serves queue j % 8,
+// whose k-th ticket is slot 8 k + j % 8, so every XCD runs the slots (and
+// reads the K/V blocks) it would have run in the one-per-slot launch, in the
+// same order, but a workgroup takes its next slot as soon as it is free
+// instead of waiting for the in-order dispatcher, which holds back every XCD
+// while one of them has no free slot.  kQueueInts int32 counters, zeroed by
+// reset_queues before each launch.
+
+// The next work slot of this workgroup's queue, the same value in every
+// thread.  Wave 0 takes the ticket (one increment, made by its lane 0; the
+// other lanes add zero) and passes it through LDS; the barrier makes it
+// visible and is also the one every wave passes before the tiles of the
+// previous item may be overwritten.  Control flow stays uniform throughout:
+// no lane-divergent branch surrounds the barrier.
+__device__ __forceinline__ int take_slot(int* queue, int* lds_slot) {
+  const int x = blockIdx.x & (kQueues - 1);
+  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) == 0) {
+    const int t = atomicAdd(queue + x, (threadIdx.x & 63) == 0 ? 1 : 0);
+    *lds_slot = __builtin_amdgcn_readfirstlane(t);
+  }
+  __syncthreads();
+  return kQueues * __builtin_amdgcn_readfirstlane(*lds_slot) + x;
+}
+
+// Zero the kQueueInts counters of a persistent launch (a kernel, not a memset,
+// so that the call can be captured in a graph and replayed).
+hipError_t reset_queues(int* queue, hipStream_t s);
+
+// Workgroups of Kernel (threads each) that the device holds at once, rounded
+// down to a multiple of the queue count and cached per device (each kernel
+// has its own cache), but no more than the cap work slots need.
+template <auto Kernel>
+hipError_t resident_grid(int threads, int cap, int* grid) {
+  static int cached[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  int n = __atomic_load_n(&cached[dev], __ATOMIC_RELAXED);
+  if (n == 0) {
+    int cus = 0, per_cu = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, Kernel, threads, 0);
+    if (e != hipSuccess) return e;
+    n = cus * (per_cu > 1 ? per_cu : 1) / kQueues * kQueues;
+    if (n < kQueues) n = kQueues;
+    __atomic_store_n(&cached[dev], n, __ATOMIC_RELAXED);
+  }
+  const int need = (cap + kQueues - 1) / kQueues * kQueues;  // more would only take empty tickets
+  *grid = n < need ? n : (need > kQueues ? need : kQueues);
+  return hipSuccess;
 }
 
 inline AttnCore make_attn_core(const AttnArgs& a) {

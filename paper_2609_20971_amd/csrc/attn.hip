@@ -1,32 +1,58 @@
 // Stage 3: causal GQA block-sparse attention (Sec. 3.3; Algorithm 1, last
-// step).  One workgroup per (query head, query block); the work of a block
-// is attend_block (attend_block.hpp).
+// step).  The work of one (query head, query block) is attend_block
+// (attend_block.hpp).  Two launches of the same work: one workgroup per
+// (query head, query block), or a persistent grid that takes them from the
+// per-XCD queues of take_slot (same slots on the same XCDs, in the same
+// order, bit-identical results; fewer idle workgroup slots when the rows'
+// lengths differ a lot, as a sparse selection's do).
 #include "attend_block.hpp"
 #include "rbs_launch.hpp"
 
 namespace rbs {
 
 template <int BS>
-__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_kernel(
-    AttnCore c, const int32_t* __restrict__ counts, const int32_t* __restrict__ indices, int64_t capacity) {
-  __shared__ __align__(1024) unsigned char k_lds[BS * 256];
-  __shared__ __align__(1024) unsigned char v_lds[BS * 256];
+__device__ __forceinline__ void attend_slot(const AttnCore& c, const int32_t* __restrict__ counts,
+                                            const int32_t* __restrict__ indices, int64_t capacity, int slot,
+                                            int total, unsigned char* k_lds, unsigned char* v_lds) {
   int h, i;
-  work_item(c.M, c.group, h, i);
+  work_of(slot, total, c.M, c.group, h, i);
   const int count = min(max(counts[(size_t)h * c.M + i], 0), i + 1);
   const int32_t* list = indices + (int64_t)h * capacity + (int64_t)i * (i + 1) / 2;
   attend_block<BS>(c, h, i, count, [&](int n) __attribute__((always_inline)) { return list[n]; }, k_lds, v_lds);
 }
 
-// Every sequence of a batch in one launch: work items are sequence-major and,
-// inside a sequence, ordered as work_item orders them.
 template <int BS>
-__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_varlen_kernel(
-    AttnCore c, const int32_t* __restrict__ counts, const int32_t* __restrict__ indices, const SeqTable t) {
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_kernel(
+    AttnCore c, const int32_t* __restrict__ counts, const int32_t* __restrict__ indices, int64_t capacity) {
   __shared__ __align__(1024) unsigned char k_lds[BS * 256];
   __shared__ __align__(1024) unsigned char v_lds[BS * 256];
-  const int hq = gridDim.x / t.blk[t.n];  // query heads
-  const int work = xcd_remap(blockIdx.x, gridDim.x);
+  attend_slot<BS>(c, counts, indices, capacity, blockIdx.x, gridDim.x, k_lds, v_lds);
+}
+
+// Persistent form: total = M * H_q work slots, queue = kQueueInts zeroed ints.
+template <int BS>
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_queue_kernel(
+    AttnCore c, const int32_t* __restrict__ counts, const int32_t* __restrict__ indices, int64_t capacity,
+    int total, int* __restrict__ queue) {
+  __shared__ __align__(1024) unsigned char k_lds[BS * 256];
+  __shared__ __align__(1024) unsigned char v_lds[BS * 256];
+  __shared__ int lds_slot;
+  for (;;) {
+    const int slot = take_slot(queue, &lds_slot);
+    if (slot >= total) break;
+    attend_slot<BS>(c, counts, indices, capacity, slot, total, k_lds, v_lds);
+    __syncthreads();  // tiles and lds_slot free for the next item
+  }
+}
+
+// Every sequence of a batch in one launch: work items are sequence-major and,
+// inside a sequence, ordered as work_of orders them.
+template <int BS>
+__device__ __forceinline__ void attend_slot_varlen(AttnCore c, const int32_t* __restrict__ counts,
+                                                   const int32_t* __restrict__ indices, const SeqTable& t, int slot,
+                                                   int total, unsigned char* k_lds, unsigned char* v_lds) {
+  const int hq = total / t.blk[t.n];  // query heads
+  const int work = xcd_remap(slot, total);
   const int sq = seq_of(t.blk, t.n, work / hq);
   const int local = work - hq * t.blk[sq];
   c.N = t.tok[sq + 1] - t.tok[sq];
@@ -48,6 +74,39 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
                          v_lds);
 }
 
+template <int BS>
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_varlen_kernel(
+    AttnCore c, const int32_t* __restrict__ counts, const int32_t* __restrict__ indices, const SeqTable t) {
+  __shared__ __align__(1024) unsigned char k_lds[BS * 256];
+  __shared__ __align__(1024) unsigned char v_lds[BS * 256];
+  attend_slot_varlen<BS>(c, counts, indices, t, blockIdx.x, gridDim.x, k_lds, v_lds);
+}
+
+template <int BS>
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_varlen_queue_kernel(
+    AttnCore c, const int32_t* __restrict__ counts, const int32_t* __restrict__ indices, const SeqTable t,
+    int total, int* __restrict__ queue) {
+  __shared__ __align__(1024) unsigned char k_lds[BS * 256];
+  __shared__ __align__(1024) unsigned char v_lds[BS * 256];
+  __shared__ int lds_slot;
+  for (;;) {
+    const int slot = take_slot(queue, &lds_slot);
+    if (slot >= total) break;
+    attend_slot_varlen<BS>(c, counts, indices, t, slot, total, k_lds, v_lds);
+    __syncthreads();
+  }
+}
+
+__global__ void reset_queues_kernel(int* __restrict__ queue) {
+  if (threadIdx.x < kQueueInts) queue[threadIdx.x] = 0;
+}
+
+hipError_t reset_queues(int* queue, hipStream_t s) {
+  hipLaunchKernelGGL(reset_queues_kernel, dim3(1), dim3(kQueueInts), 0, s, queue);
+  return hipGetLastError();
+}
+
+
 __global__ void dense_indices_kernel(int M, int64_t capacity, int32_t* __restrict__ counts,
                                      int32_t* __restrict__ indices) {
   const int i = blockIdx.x, h = blockIdx.y;
@@ -57,11 +116,24 @@ __global__ void dense_indices_kernel(int M, int64_t capacity, int32_t* __restric
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid(a.n_blocks * a.n_q_heads);
+  const int total = a.n_blocks * a.n_q_heads;
   const AttnCore c = make_attn_core(a);
+  if (a.queue != nullptr) {
+    hipError_t e = reset_queues(a.queue, s);
+    if (e != hipSuccess) return e;
+  }
+  int grid = 0;
 #define RBS_ATTN_CASE(BSZ)                                                                                     \
   case BSZ:                                                                                                    \
-    hipLaunchKernelGGL(attn_kernel<BSZ>, grid, dim3(BSZ * 2), 0, s, c, a.counts, a.indices, a.capacity);       \
+    if (a.queue == nullptr) {                                                                                  \
+      hipLaunchKernelGGL(attn_kernel<BSZ>, dim3(total), dim3(BSZ * 2), 0, s, c, a.counts, a.indices,          \
+                         a.capacity);                                                                          \
+    } else {                                                                                                   \
+      const hipError_t e = resident_grid<attn_queue_kernel<BSZ>>(BSZ * 2, total, &grid);                       \
+      if (e != hipSuccess) return e;                                                                           \
+      hipLaunchKernelGGL(attn_queue_kernel<BSZ>, dim3(grid), dim3(BSZ * 2), 0, s, c, a.counts, a.indices,     \
+                         a.capacity, total, a.queue);                                                          \
+    }                                                                                                          \
     break;
   switch (a.block_size) {
     RBS_ATTN_CASE(64)
@@ -84,11 +156,23 @@ __global__ void dense_indices_varlen_kernel(const SeqTable t, int32_t* __restric
 }
 
 hipError_t launch_attention_varlen(const AttnArgs& a, const SeqTable& t, hipStream_t s) {
-  const dim3 grid(t.blk[t.n] * a.n_q_heads);
+  const int total = t.blk[t.n] * a.n_q_heads;
   const AttnCore c = make_attn_core(a);
+  if (a.queue != nullptr) {
+    hipError_t e = reset_queues(a.queue, s);
+    if (e != hipSuccess) return e;
+  }
+  int grid = 0;
 #define RBS_ATTN_VARLEN_CASE(BSZ)                                                                              \
   case BSZ:                                                                                                    \
-    hipLaunchKernelGGL(attn_varlen_kernel<BSZ>, grid, dim3(BSZ * 2), 0, s, c, a.counts, a.indices, t);         \
+    if (a.queue == nullptr) {                                                                                  \
+      hipLaunchKernelGGL(attn_varlen_kernel<BSZ>, dim3(total), dim3(BSZ * 2), 0, s, c, a.counts, a.indices, t); \
+    } else {                                                                                                   \
+      const hipError_t e = resident_grid<attn_varlen_queue_kernel<BSZ>>(BSZ * 2, total, &grid);                \
+      if (e != hipSuccess) return e;                                                                           \
+      hipLaunchKernelGGL(attn_varlen_queue_kernel<BSZ>, dim3(grid), dim3(BSZ * 2), 0, s, c, a.counts,         \
+                         a.indices, t, total, a.queue);                                                        \
+    }                                                                                                          \
     break;
   switch (a.block_size) {
     RBS_ATTN_VARLEN_CASE(64)

@@ -205,13 +205,11 @@ struct AttnF8Args {
   float* lse;
 };
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fp8_kernel(AttnF8Args c) {
+// Query block i of query head h; k_lds, v_lds: 16 KiB each.
+__device__ __forceinline__ void attend_block_fp8(const AttnF8Args& c, int h, int i, unsigned char* k_lds,
+                                                 unsigned char* v_lds) {
   constexpr int BS = 128;
-  __shared__ __align__(1024) unsigned char k_lds[BS * 128];
-  __shared__ __align__(1024) unsigned char v_lds[kHeadDim * BS];
   const int group = c.Hq / c.Hkv;
-  int h, i;
-  work_item(c.M, group, h, i);
   const int g = h / group;
   const int N = c.N;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -349,6 +347,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
 }
 
+// One workgroup per (query head, query block), ordered by work_item.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fp8_kernel(AttnF8Args c) {
+  __shared__ __align__(1024) unsigned char k_lds[128 * 128];
+  __shared__ __align__(1024) unsigned char v_lds[kHeadDim * 128];
+  int h, i;
+  work_item(c.M, c.Hq / c.Hkv, h, i);
+  attend_block_fp8(c, h, i, k_lds, v_lds);
+}
+
+// Persistent form (the queues of take_slot): the same work slots on the same
+// XCDs in the same order, bit-identical results.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fp8_queue_kernel(
+    AttnF8Args c, int* __restrict__ queue) {
+  __shared__ __align__(1024) unsigned char k_lds[128 * 128];
+  __shared__ __align__(1024) unsigned char v_lds[kHeadDim * 128];
+  __shared__ int lds_slot;
+  const int total = c.M * c.Hq;
+  for (;;) {
+    const int slot = take_slot(queue, &lds_slot);
+    if (slot >= total) break;
+    int h, i;
+    work_of(slot, total, c.M, c.Hq / c.Hkv, h, i);
+    attend_block_fp8(c, h, i, k_lds, v_lds);
+    __syncthreads();  // tiles and lds_slot free for the next item
+  }
+}
+
 // ------------------------------------------------------------------ launchers
 
 hipError_t launch_fp8_amax(const uint16_t* Q, const uint16_t* K, const uint16_t* V, int n_tokens, int n_q_heads,
@@ -380,7 +405,7 @@ hipError_t launch_fp8_pack(const uint16_t* Q, const uint16_t* K, const uint16_t*
 hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint8_t* V8t, const float* amax,
                                 int n_tokens, int n_q_heads, int n_kv_heads, int n_blocks, const int32_t* counts,
                                 const int32_t* indices, int64_t capacity, float scale, uint16_t* O, float* lse,
-                                hipStream_t s) {
+                                int* queue, hipStream_t s) {
   AttnF8Args a;
   a.Q8 = Q8;
   a.K8 = K8;
@@ -396,7 +421,17 @@ hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint
   a.capacity = capacity;
   a.O = O;
   a.lse = lse;
-  hipLaunchKernelGGL(attn_fp8_kernel, dim3(n_blocks * n_q_heads), dim3(256), 0, s, a);
+  const int total = n_blocks * n_q_heads;
+  if (queue == nullptr) {
+    hipLaunchKernelGGL(attn_fp8_kernel, dim3(total), dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
+  hipError_t e = reset_queues(queue, s);
+  if (e != hipSuccess) return e;
+  int grid = 0;
+  e = resident_grid<attn_fp8_queue_kernel>(256, total, &grid);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_fp8_queue_kernel, dim3(grid), dim3(256), 0, s, a, queue);
   return hipGetLastError();
 }
 

@@ -56,6 +56,7 @@ struct AttnArgs {
   float scale;
   uint16_t* O;
   float* lse;
+  int* queue = nullptr;  // persistent launch's work queues (kQueueInts ints), or one workgroup per item
 };
 
 // Select-ready summary, each part 256-byte aligned: f16 centroids scaled by
@@ -77,6 +78,9 @@ inline size_t summary_bytes(int n_kv_heads, int n_blocks) {
 // blocks blk[s] .. blk[s+1]-1 of the block arrays and index-list slots
 // cap[s] .. cap[s+1]-1 of every query head; a single sequence is {n = 1}.
 constexpr int kMaxSeqs = 64;
+constexpr int kMaxDevices = 64;  // devices whose resident-grid size the launchers cache
+constexpr int kQueues = 8;       // work queues of a persistent attention launch, one per XCD
+constexpr int kQueueInts = 64;   // its workspace: 256 bytes, the eight counters and room to spare
 struct SeqTable {
   int n;
   int tok[kMaxSeqs + 1];
@@ -123,7 +127,7 @@ hipError_t launch_fp8_pack(const uint16_t* Q, const uint16_t* K, const uint16_t*
 hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint8_t* V8t, const float* amax,
                                 int n_tokens, int n_q_heads, int n_kv_heads, int n_blocks, const int32_t* counts,
                                 const int32_t* indices, int64_t capacity, float scale, uint16_t* O, float* lse,
-                                hipStream_t s);
+                                int* queue, hipStream_t s);
 
 // Varlen launchers: the Args hold the batch totals (n_tokens = T, n_blocks and
 // capacity = the table's last offsets); every sequence runs in the same launch.

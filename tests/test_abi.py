@@ -76,7 +76,7 @@ def test_shape_validation(field, value, code):
     st = _stats(rbs)
     assert lib.rbs_block_stats(ctypes.byref(s), FAKE, ctypes.byref(st), None) == code
     assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, FAKE, FAKE, None) == code
-    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None) == code
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None) == code
     assert lib.rbs_dense_indices(ctypes.byref(s), FAKE, FAKE, None) == code
     assert _fused(lib, s, st) == code
 
@@ -109,9 +109,11 @@ def test_null_and_alignment_errors():
     assert lib.rbs_select(ctypes.byref(s), None, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, FAKE, FAKE, None) == 1
     assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, None, FAKE, None) == 1
     assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, FAKE, MIS, None) == 5
-    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, None, FAKE, FAKE, 0.0, FAKE, None, None) == 1
-    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, MIS, None, None) == 5
-    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, MIS, None) == 5
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, None, FAKE, FAKE, 0.0, FAKE, None, None, None) == 1
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, MIS, None, None, None) == 5
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, MIS, None, None) == 5
+    # A misaligned attention workspace is refused before anything is launched.
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, MIS, None) == 5
     assert lib.rbs_dense_indices(ctypes.byref(s), FAKE, None, None) == 1
     for arg in ("Q", "K", "V", "counts", "indices", "O"):
         assert _fused(lib, s, st, **{arg: None}) == 1
@@ -138,7 +140,7 @@ def test_bad_softmax_scale():
     rbs, lib = _lib()
     s = rbs.make_shape(1024, 4, 2, 64)
     for bad in (float("nan"), float("inf")):
-        assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, bad, FAKE, None, None) == 4
+        assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, FAKE, bad, FAKE, None, None, None) == 4
         assert _fused(lib, s, _stats(rbs), scale=bad) == 4
 
 
@@ -204,7 +206,7 @@ def _varlen_calls(lib, s, b, st, ptr=FAKE):
     return [
         lib.rbs_block_stats_varlen(ctypes.byref(s), bb, ptr, ctypes.byref(st), None),
         lib.rbs_select_varlen(ctypes.byref(s), bb, ptr, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, ptr, ptr, None),
-        lib.rbs_sparse_prefill_varlen(ctypes.byref(s), bb, ptr, ptr, ptr, ptr, ptr, 0.0, ptr, None, None),
+        lib.rbs_sparse_prefill_varlen(ctypes.byref(s), bb, ptr, ptr, ptr, ptr, ptr, 0.0, ptr, None, None, None),
         lib.rbs_dense_indices_varlen(ctypes.byref(s), bb, ptr, ptr, None),
     ]
 
@@ -251,12 +253,14 @@ def test_varlen_null_unsupported_and_alignment():
     assert _varlen_calls(lib, s, nb, st) == [1] * 4
     assert _varlen_calls(lib, s, b, st, ptr=None) == [1] * 4
     assert _varlen_calls(lib, s, b, st, ptr=MIS) == [5] * 4
+    assert lib.rbs_sparse_prefill_varlen(ctypes.byref(s), ctypes.byref(b.c), FAKE, FAKE, FAKE, FAKE, FAKE, 0.0,
+                                         FAKE, None, MIS, None) == 5
     bad = rbs.varlen_shape(b, 4, 2, 96)
     assert _varlen_calls(lib, bad, b, st) == [3] * 4
     assert lib.rbs_select_varlen(ctypes.byref(s), ctypes.byref(b.c), FAKE, ctypes.byref(st), 1.5, 0.9, 1, 1, 0,
                                  FAKE, FAKE, None) == 4
     assert lib.rbs_sparse_prefill_varlen(ctypes.byref(s), ctypes.byref(b.c), FAKE, FAKE, FAKE, FAKE, FAKE,
-                                         float("nan"), FAKE, None, None) == 4
+                                         float("nan"), FAKE, None, None, None) == 4
 
 
 def test_varlen_largest_batch_passes_validation():
@@ -282,9 +286,15 @@ def test_fp8_sizes_and_validation():
     b64 = rbs.make_shape(1000, 4, 2, 64)
     assert lib.rbs_fp8_pack(ctypes.byref(b64), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 3
     assert lib.rbs_sparse_prefill_fp8(ctypes.byref(b64), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None,
-                                      None) == 3
-    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, None, FAKE, FAKE, FAKE, 0.0, FAKE, None, None) == 1
-    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, float("nan"), FAKE, None, None) == 4
-    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, MIS, None) == 5
+                                      None, None) == 3
+    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, None, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None) == 1
+    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, float("nan"), FAKE, None, None, None) == 4
+    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, MIS, None, None) == 5
+    assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, MIS, None) == 5
     bad = rbs.make_shape(1000, 3, 2, 128)
     assert lib.rbs_fp8_amax(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, None) == 2
+
+
+def test_attention_workspace_size():
+    rbs, lib = _lib()
+    assert lib.rbs_attention_workspace_bytes() == 256
