@@ -101,7 +101,8 @@ size_t rbs_summary_bytes(const rbs_shape* shape);
  * room for i + 1 entries. */
 int64_t rbs_index_capacity(int32_t n_blocks);
 
-/* Workspace of the attention calls (rbs_sparse_prefill, _varlen, _fp8):
+/* Workspace of the attention calls (rbs_sparse_prefill, _varlen, _fp8 and
+ * rbs_select_attend):
  * RBS_ATTN_WORKSPACE_BYTES of device memory, 16-byte aligned, or NULL.
  *   NULL      one workgroup per (query head, query block);
  *   non-NULL  a persistent grid (as many workgroups as the GPU holds at once)
@@ -173,7 +174,7 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
 int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, const void* V,
                       const rbs_stats* stats, float tau_base, float tau_rescue, int32_t n_sink,
                       int32_t n_local, int32_t n_recent, float softmax_scale, int32_t* counts,
-                      int32_t* indices, void* O, float* lse, void* stream);
+                      int32_t* indices, void* O, float* lse, void* workspace, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Supporting selectors (the paper's selector comparison, Table

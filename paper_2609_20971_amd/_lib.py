@@ -92,7 +92,7 @@ def load() -> ctypes.CDLL:
     lib.rbs_sparse_prefill.argtypes = [SP, P, P, P, P, P, F32, P, P, P, P]
     lib.rbs_sparse_prefill.restype = ctypes.c_int
     lib.rbs_select_attend.argtypes = [SP, P, P, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, F32, P, P, P,
-                                      P, P]
+                                      P, P, P]
     lib.rbs_select_attend.restype = ctypes.c_int
     lib.rbs_box_summary_bytes.argtypes = [SP]
     lib.rbs_box_summary_bytes.restype = SZ
@@ -311,17 +311,18 @@ def rbs_sparse_prefill(shape: rbs_shape, Q, K, V, counts, indices, softmax_scale
 
 def rbs_select_attend(shape: rbs_shape, Q, K, V, stats: BlockStats, tau_base: float, tau_rescue: float,
                       n_sink: int, n_local: int, n_recent: int, softmax_scale: float = 0.0, counts=None,
-                      indices=None, O=None, lse=None, stream=None):
+                      indices=None, O=None, lse=None, stream=None, workspace=AUTO):
     """Stages 2 and 3 in one pass; returns (counts, indices, O) as the two calls would."""
     if counts is None or indices is None:
         counts, indices = allocate_lists(shape, Q.device)
     if O is None:
         O = torch.empty_like(Q)
     c = stats.as_c()
+    ws = _workspace(workspace, Q.device, stream)
     _check("rbs_select_attend", load().rbs_select_attend(
         ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V), ctypes.byref(c), float(tau_base), float(tau_rescue),
         int(n_sink), int(n_local), int(n_recent), float(softmax_scale), _ptr(counts), _ptr(indices), _ptr(O),
-        _ptr(lse), _stream(stream)))
+        _ptr(lse), _ptr(ws), _stream(stream)))
     return counts, indices, O
 
 

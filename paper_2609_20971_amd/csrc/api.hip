@@ -183,7 +183,8 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
 
 int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, const void* V, const rbs_stats* stats,
                       float tau_base, float tau_rescue, int32_t n_sink, int32_t n_local, int32_t n_recent,
-                      float softmax_scale, int32_t* counts, int32_t* indices, void* O, float* lse, void* stream) {
+                      float softmax_scale, int32_t* counts, int32_t* indices, void* O, float* lse, void* workspace,
+                      void* stream) {
   int rc = check_shape(shape);
   if (rc != RBS_OK) return rc;
   if (Q == nullptr || K == nullptr || V == nullptr || O == nullptr || counts == nullptr || indices == nullptr ||
@@ -193,7 +194,8 @@ int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, cons
   if (n_sink < 0 || n_local < 1 || n_recent < 0) return RBS_ERR_ARG;
   if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(counts) ||
-      !aligned16(indices) || !aligned16(stats->summary) || (lse != nullptr && !aligned16(lse)))
+      !aligned16(indices) || !aligned16(stats->summary) || (lse != nullptr && !aligned16(lse)) ||
+      (workspace != nullptr && !aligned16(workspace)))
     return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
   rbs::SelectArgs sa;
@@ -231,6 +233,7 @@ int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, cons
   aa.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   aa.O = static_cast<uint16_t*>(O);
   aa.lse = lse;
+  aa.queue = static_cast<int*>(workspace);
   return from_hip(rbs::launch_select_attend(sa, aa, static_cast<hipStream_t>(stream)));
 }
 

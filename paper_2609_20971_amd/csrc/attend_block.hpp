@@ -333,26 +333,27 @@ __device__ __forceinline__ int take_slot(int* queue, int* lds_slot) {
 // so that the call can be captured in a graph and replayed).
 hipError_t reset_queues(int* queue, hipStream_t s);
 
-// Workgroups of Kernel (threads each) that the device holds at once, rounded
-// down to a multiple of the queue count and cached per device (each kernel
-// has its own cache), but no more than the cap work slots need.
+// Workgroups of Kernel (threads each, smem bytes of dynamic LDS) that the
+// device holds at once, rounded down to a multiple of the queue count, but no
+// more than the cap work slots need.  Cached per device (each kernel has its
+// own cache) when the kernel has no dynamic LDS, whose size changes the count.
 template <auto Kernel>
-hipError_t resident_grid(int threads, int cap, int* grid) {
+hipError_t resident_grid(int threads, int cap, int* grid, size_t smem = 0) {
   static int cached[kMaxDevices] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  int n = __atomic_load_n(&cached[dev], __ATOMIC_RELAXED);
+  int n = smem == 0 ? __atomic_load_n(&cached[dev], __ATOMIC_RELAXED) : 0;
   if (n == 0) {
     int cus = 0, per_cu = 0;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, Kernel, threads, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, Kernel, threads, smem);
     if (e != hipSuccess) return e;
     n = cus * (per_cu > 1 ? per_cu : 1) / kQueues * kQueues;
     if (n < kQueues) n = kQueues;
-    __atomic_store_n(&cached[dev], n, __ATOMIC_RELAXED);
+    if (smem == 0) __atomic_store_n(&cached[dev], n, __ATOMIC_RELAXED);
   }
   const int need = (cap + kQueues - 1) / kQueues * kQueues;  // more would only take empty tickets
   *grid = n < need ? n : (need > kQueues ? need : kQueues);

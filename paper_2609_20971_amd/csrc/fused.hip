@@ -36,6 +36,30 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       smem + BS * 256);
 }
 
+// Persistent form (the queues of take_slot): the same work slots on the same
+// XCDs in the same order, bit-identical results.
+template <int BS>
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void select_attend_queue_kernel(
+    SelectCore sc, AttnCore ac, int total, int* __restrict__ queue) {
+  extern __shared__ __align__(1024) unsigned char smem[];
+  __shared__ int lds_slot;
+  typedef __attribute__((address_space(3))) int32_t lds_i32;
+  lds_i32* list_lds = (lds_i32*)(smem + fused_region_bytes<BS>(ac.M));
+  for (;;) {
+    const int slot = take_slot(queue, &lds_slot);
+    if (slot >= total) break;
+    int h, i;
+    work_of(slot, total, ac.M, ac.group, h, i);
+    const int count = select_block<BS>(sc, h, i, smem, list_lds);
+    __syncthreads();
+    attend_block<BS>(
+        ac, h, i, min(max(count, 0), i + 1),
+        [&](int n) __attribute__((always_inline)) { return __builtin_amdgcn_readfirstlane(list_lds[n]); }, smem,
+        smem + BS * 256);
+    __syncthreads();  // tiles, list and lds_slot free for the next item
+  }
+}
+
 size_t fused_smem_bytes(int block_size, int n_blocks) {
   switch (block_size) {
     case 64: return fused_region_bytes<64>(n_blocks) + (size_t)n_blocks * 4;
@@ -46,16 +70,31 @@ size_t fused_smem_bytes(int block_size, int n_blocks) {
 }
 
 hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStream_t s) {
-  const dim3 grid(sa.n_blocks * sa.n_q_heads);
+  const int total = sa.n_blocks * sa.n_q_heads;
   const SelectCore sc = make_select_core(sa);
   const AttnCore ac = make_attn_core(aa);
   const size_t smem = fused_smem_bytes(sa.block_size, sa.n_blocks);
+  if (aa.queue != nullptr) {
+    hipError_t e = reset_queues(aa.queue, s);
+    if (e != hipSuccess) return e;
+  }
+  int grid = 0;
 #define RBS_FUSED_CASE(BSZ)                                                                                   \
   case BSZ: {                                                                                                 \
-    hipError_t e = hipFuncSetAttribute((const void*)select_attend_kernel<BSZ>,                                \
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);                \
-    if (e != hipSuccess) return e;                                                                            \
-    hipLaunchKernelGGL(select_attend_kernel<BSZ>, grid, dim3(BSZ * 2), smem, s, sc, ac);                      \
+    if (aa.queue == nullptr) {                                                                                \
+      hipError_t e = hipFuncSetAttribute((const void*)select_attend_kernel<BSZ>,                              \
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);              \
+      if (e != hipSuccess) return e;                                                                          \
+      hipLaunchKernelGGL(select_attend_kernel<BSZ>, dim3(total), dim3(BSZ * 2), smem, s, sc, ac);             \
+    } else {                                                                                                  \
+      hipError_t e = hipFuncSetAttribute((const void*)select_attend_queue_kernel<BSZ>,                        \
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);              \
+      if (e != hipSuccess) return e;                                                                          \
+      e = resident_grid<select_attend_queue_kernel<BSZ>>(BSZ * 2, total, &grid, smem);                        \
+      if (e != hipSuccess) return e;                                                                          \
+      hipLaunchKernelGGL(select_attend_queue_kernel<BSZ>, dim3(grid), dim3(BSZ * 2), smem, s, sc, ac, total,  \
+                         aa.queue);                                                                           \
+    }                                                                                                         \
     break;                                                                                                    \
   }
   switch (sa.block_size) {

@@ -82,9 +82,9 @@ def test_shape_validation(field, value, code):
 
 
 def _fused(lib, s, st, Q=FAKE, K=FAKE, V=FAKE, tb=0.9, tr=0.9, sink=1, local=1, recent=0, scale=0.0, counts=FAKE,
-           indices=FAKE, O=FAKE, lse=None):
+           indices=FAKE, O=FAKE, lse=None, workspace=None):
     return lib.rbs_select_attend(ctypes.byref(s), Q, K, V, ctypes.byref(st) if st is not None else None, tb, tr,
-                                 sink, local, recent, scale, counts, indices, O, lse, None)
+                                 sink, local, recent, scale, counts, indices, O, lse, workspace, None)
 
 
 def test_largest_shape_passes_shape_validation():
@@ -122,6 +122,7 @@ def test_null_and_alignment_errors():
     assert _fused(lib, s, _stats(rbs, summary=None)) == 1
     assert _fused(lib, s, _stats(rbs, summary=MIS)) == 5
     assert _fused(lib, s, st, lse=MIS) == 5
+    assert _fused(lib, s, st, workspace=MIS) == 5
 
 
 @pytest.mark.parametrize("tb,tr,sink,local,recent", [

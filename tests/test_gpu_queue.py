@@ -142,3 +142,32 @@ def test_queue_fp8_equals_one_workgroup_per_item():
         out.append((O, lse))
     _assert_same(out[0], out[1], "fp8")
     assert np.isfinite(out[1][1].cpu().numpy()).all()
+
+
+@pytest.mark.parametrize("B", [64, 128])
+def test_queue_fused_equals_one_workgroup_per_item(B):
+    import torch
+    import paper_2609_20971_amd as rbs
+    w = WORKLOADS["tiny-2k"].with_(name="queue-fused", seq_len=3000, n_q_heads=8, n_kv_heads=2, block_size=B,
+                                   seed=45 + B)
+    _say(f"[queue] fused B={B}")
+    inp = make_inputs(w)
+    shape = rbs.make_shape(w.seq_len, w.n_q_heads, w.n_kv_heads, w.block_size)
+    Q, K, V = (H.to_device(inp[x]) for x in ("q", "k", "v"))
+    st = rbs.rbs_block_stats(shape, K)
+    out = []
+    for ws in (None, "auto"):
+        lse = torch.full((w.n_q_heads, w.seq_len), 7.0, dtype=torch.float32, device="cuda")
+        counts, indices, O = rbs.rbs_select_attend(shape, Q, K, V, st, w.tau_base, w.tau_rescue, w.n_sink,
+                                                   w.n_local, w.n_recent, lse=lse, workspace=ws)
+        out.append((counts, indices, O, lse))
+    torch.cuda.synchronize()
+    assert torch.equal(out[0][0], out[1][0]), "counts"
+    cnt = out[0][0].cpu().numpy()
+    a, b = out[0][1].cpu().numpy(), out[1][1].cpu().numpy()
+    for h in range(w.n_q_heads):
+        for i in range(w.n_blocks):
+            o = i * (i + 1) // 2
+            assert np.array_equal(a[h, o:o + cnt[h, i]], b[h, o:o + cnt[h, i]]), (h, i)
+    assert torch.equal(out[0][2], out[1][2]), "O"
+    assert torch.equal(out[0][3], out[1][3]), "lse"
