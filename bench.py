@@ -271,7 +271,7 @@ def main():
     select_gbps = alg["select_bytes"] / (stage_ms[1] * 1e-3) / 1e9
     select_tflops = alg["select_flops"] / (stage_ms[1] * 1e-3) / 1e12
 
-    traffic = _profiled_traffic("attn_kernel", w.name)
+    traffic = _profiled_traffic("attn_queue_kernel", w.name)
 
     result = {
         "metric": METRIC,
@@ -732,14 +732,16 @@ def layer_sweep(args):
     }), flush=True)
 
 
-# Sources each kernel is built from (their joint hash identifies the kernel in
-# the committed rocprofv3 summaries).
+# Sources each kernel is built from, with the build script (it holds per-source
+# compiler flags); their joint hash identifies the kernel in the committed
+# rocprofv3 summaries.  The attention calls run the persistent (queue) kernels.
 KERNEL_SOURCES = {
-    "stats_kernel": ["stats.hip", "rbs_device.hpp"],
-    "quantile_kernel": ["stats.hip", "rbs_device.hpp"],
-    "select_kernel": ["select.hip", "select_block.hpp", "rbs_device.hpp"],
-    "attn_kernel": ["attn.hip", "attend_block.hpp", "rbs_device.hpp"],
-    "select_attend_kernel": ["fused.hip", "select_block.hpp", "attend_block.hpp", "rbs_device.hpp"],
+    "stats_kernel": ["stats.hip", "rbs_device.hpp", "../build.py"],
+    "quantile_kernel": ["stats.hip", "rbs_device.hpp", "../build.py"],
+    "select_kernel": ["select.hip", "select_block.hpp", "rbs_device.hpp", "../build.py"],
+    "attn_queue_kernel": ["attn.hip", "attend_block.hpp", "rbs_device.hpp", "rbs_launch.hpp", "../build.py"],
+    "select_attend_queue_kernel": ["fused.hip", "select_block.hpp", "attend_block.hpp", "rbs_device.hpp",
+                                   "rbs_launch.hpp", "../build.py"],
 }
 
 
