@@ -299,3 +299,18 @@ def test_fp8_sizes_and_validation():
 def test_attention_workspace_size():
     rbs, lib = _lib()
     assert lib.rbs_attention_workspace_bytes() == 256
+
+
+def test_binding_workspace_argument():
+    """The binding's workspace argument: None passes NULL, a tensor must hold
+    rbs_attention_workspace_bytes(), anything else is refused (host checks only)."""
+    import torch
+    from paper_2609_20971_amd import _lib as L
+    _lib()
+    assert L._workspace(None, "cpu", 0) is None
+    t = torch.zeros(64, dtype=torch.int32)
+    assert L._workspace(t, "cpu", 0) is t
+    with pytest.raises(ValueError):
+        L._workspace(torch.zeros(63, dtype=torch.int32), "cpu", 0)
+    with pytest.raises(ValueError):
+        L._workspace("cached", "cpu", 0)
