@@ -152,9 +152,12 @@ def _stream(stream) -> int | None:
 
 
 # Attention workspace argument: AUTO takes one cached per (device, stream) --
-# calls on one stream are ordered, so they may share it --; None asks for the
-# one-workgroup-per-item launch; a tensor of at least
-# rbs_attention_workspace_bytes() bytes is used as given.
+# calls on one stream are ordered, so they may share it (a stream handle that
+# is destroyed and handed out again while work is pending would share it
+# with that work; torch's pooled streams are never destroyed) --; None asks
+# for the one-workgroup-per-item launch; a device tensor of at least
+# rbs_attention_workspace_bytes() bytes is used as given.  Its contents do not
+# matter: every call resets the queues on its own stream.
 AUTO = "auto"
 _workspaces: dict = {}
 
@@ -166,7 +169,7 @@ def attention_workspace(device, stream=None) -> torch.Tensor:
     ws = _workspaces.get(key)
     if ws is None:
         n = int(load().rbs_attention_workspace_bytes())
-        ws = torch.zeros(n // 4, dtype=torch.int32, device=torch.device("cuda", index))
+        ws = torch.empty(n // 4, dtype=torch.int32, device=torch.device("cuda", index))
         _workspaces[key] = ws
     return ws
 
@@ -176,8 +179,15 @@ def _workspace(workspace, device, stream):
         if workspace != AUTO:
             raise ValueError(f"workspace must be AUTO, None or a tensor, not {workspace!r}")
         return attention_workspace(device, stream)
-    if workspace is not None and workspace.numel() * workspace.element_size() < load().rbs_attention_workspace_bytes():
+    if workspace is None:
+        return None
+    if workspace.numel() * workspace.element_size() < load().rbs_attention_workspace_bytes():
         raise ValueError("workspace is smaller than rbs_attention_workspace_bytes()")
+    dev = torch.device(device)
+    if dev.type == "cuda":
+        index = dev.index if dev.index is not None else torch.cuda.current_device()
+        if workspace.device.type != "cuda" or workspace.device.index != index:
+            raise ValueError(f"workspace is on {workspace.device}, the inputs on cuda:{index}")
     return workspace
 
 
