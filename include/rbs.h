@@ -230,8 +230,8 @@ int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices,
  * the precision of their attention is not stated).  These calls run stage 3
  * on FP8 E4M3 copies of Q, K and V (OCP E4M3: bias 7, 3 mantissa bits,
  * largest finite 448) with the products on gfx950's FP8 matrix core; the
- * selection is unchanged (bf16 inputs, rbs_select).  Block size 128 only
- * (others return RBS_ERR_UNSUPPORTED).
+ * selection is unchanged (bf16 inputs, rbs_select).  Block sizes 64, 128
+ * and 256, as for the bf16 calls.
  *
  * Scaling: each head h of Q (then K, then V) is scaled so that its largest
  * magnitude amax_h maps to 448: code = E4M3(x * (448 / amax_h)), rounded to
@@ -242,7 +242,8 @@ int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices,
  *   Q8     E4M3 [H_q][N][d]      K8  E4M3 [H_kv][N][d]  (row-major copies)
  *   V8t    rbs_fp8_vt_bytes() bytes: per KV head and key block, the d x B
  *          tile of V transposed, keys in the order the attention kernel
- *          consumes them (opaque to the caller; keys past N are zero)
+ *          consumes them (B = 256: as two d x 128 halves; opaque to the
+ *          caller; keys past N are zero)
  * Attention: as rbs_sparse_prefill on the dequantised inputs; P is rounded to
  * E4M3 for the PV product (values <= 256), and the denominator sums the same
  * rounded values.  O is bf16, lse as in rbs_sparse_prefill.

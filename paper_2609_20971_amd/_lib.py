@@ -476,7 +476,7 @@ def rbs_fp8_vt_bytes(shape: rbs_shape) -> int:
 def allocate_fp8(shape: rbs_shape, device="cuda") -> Fp8Inputs:
     nvt = rbs_fp8_vt_bytes(shape)
     if nvt == 0:
-        raise RbsError("rbs_fp8_vt_bytes", RBS_ERR_UNSUPPORTED, "FP8 attention needs block size 128")
+        raise RbsError("rbs_fp8_vt_bytes", RBS_ERR_SHAPE, "invalid shape for the FP8 inputs")
     u8 = dict(dtype=torch.uint8, device=device)
     return Fp8Inputs(torch.empty(shape.n_q_heads + 2 * shape.n_kv_heads, dtype=torch.float32, device=device),
                      torch.empty((shape.n_q_heads, shape.n_tokens, shape.head_dim), **u8),

@@ -447,7 +447,7 @@ int rbs_dense_indices_varlen(const rbs_shape* shape, const rbs_batch* batch, int
 }
 
 size_t rbs_fp8_vt_bytes(const rbs_shape* shape) {
-  if (check_shape(shape) != RBS_OK || shape->block_size != 128) return 0;
+  if (check_shape(shape) != RBS_OK) return 0;
   return (size_t)shape->n_kv_heads * blocks_of(shape) * 128 * shape->block_size;
 }
 
@@ -465,7 +465,6 @@ int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const voi
                  void* K8, void* V8t, void* stream) {
   int rc = check_shape(shape);
   if (rc != RBS_OK) return rc;
-  if (shape->block_size != 128) return RBS_ERR_UNSUPPORTED;
   if (Q == nullptr || K == nullptr || V == nullptr || amax == nullptr || Q8 == nullptr || K8 == nullptr ||
       V8t == nullptr)
     return RBS_ERR_NULL;
@@ -474,7 +473,8 @@ int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const voi
     return RBS_ERR_ALIGN;
   return from_hip(rbs::launch_fp8_pack(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
                                        static_cast<const uint16_t*>(V), shape->n_tokens, shape->n_q_heads,
-                                       shape->n_kv_heads, blocks_of(shape), amax, static_cast<uint8_t*>(Q8),
+                                       shape->n_kv_heads, shape->block_size, blocks_of(shape), amax,
+                                       static_cast<uint8_t*>(Q8),
                                        static_cast<uint8_t*>(K8), static_cast<uint8_t*>(V8t),
                                        static_cast<hipStream_t>(stream)));
 }
@@ -484,7 +484,6 @@ int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K
                            void* O, float* lse, void* workspace, void* stream) {
   int rc = check_shape(shape);
   if (rc != RBS_OK) return rc;
-  if (shape->block_size != 128) return RBS_ERR_UNSUPPORTED;
   if (Q8 == nullptr || K8 == nullptr || V8t == nullptr || amax == nullptr || counts == nullptr ||
       indices == nullptr || O == nullptr)
     return RBS_ERR_NULL;
@@ -497,7 +496,8 @@ int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   return from_hip(rbs::launch_attention_fp8(
       static_cast<const uint8_t*>(Q8), static_cast<const uint8_t*>(K8), static_cast<const uint8_t*>(V8t), amax,
-      shape->n_tokens, shape->n_q_heads, shape->n_kv_heads, M, counts, indices, rbs_index_capacity(M), scale,
+      shape->n_tokens, shape->n_q_heads, shape->n_kv_heads, shape->block_size, M, counts, indices,
+      rbs_index_capacity(M), scale,
       static_cast<uint16_t*>(O), lse, static_cast<int*>(workspace), static_cast<hipStream_t>(stream)));
 }
 

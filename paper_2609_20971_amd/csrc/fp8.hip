@@ -9,11 +9,12 @@
 //                 tiles V^T [d][keys] whose key order matches the register
 //                 order of P in the attention kernel, so that the PV operand
 //                 is a plain 32-byte row read.
-//   attn_fp8      one workgroup per (query head, query block), B = 128, the
+//   attn_fp8      per (query head, query block), B = 64, 128 or 256, the
 //                 orientation and pipeline of the bf16 kernel: S^T = K Q^T and
 //                 O^T = V^T P^T, Q in registers, K and V^T tiles copied
-//                 global -> LDS (16 KiB each, 128-byte rows, 16-byte chunks
-//                 XOR-swizzled), online softmax in fp32, P rounded to E4M3.
+//                 global -> LDS (B x 128 bytes each, 128-byte rows, 16-byte
+//                 chunks XOR-swizzled), online softmax in fp32 in steps of up
+//                 to 128 keys, P rounded to E4M3.
 //                 The softmax denominator is accumulated by the matrix core
 //                 too (ones times P^T), from exactly the rounded P.
 //
@@ -55,13 +56,21 @@ __device__ __forceinline__ int pack4_fp8(float a, float b, float c, float d) {
 __device__ __forceinline__ float fp8_inv_scale(float amax) { return amax > 0.f ? kFp8Max / amax : 1.0f; }
 __device__ __forceinline__ float fp8_deq_scale(float amax) { return amax > 0.f ? amax / kFp8Max : 1.0f; }
 
-// Key of position p (0 .. 127) of a V^T tile row.  Position p = 64 s + 32 g + b
+// Key of position p (0 .. B - 1) of a V^T tile row.  Position p = 64 s + 32 g + b
 // is byte b of k-group g of PV step s; it holds the key whose probability sits
 // at that byte of the P operand: element r = b % 16 of S^T tile 2 s + b / 16 in
 // lane half g, i.e. key 64 s + 32 (b / 16) + 8 (r / 4) + 4 g + r % 4.
 __host__ __device__ inline int vt_key(int p) {
   const int s = p >> 6, g = (p >> 5) & 1, b = p & 31, r = b & 15;
   return 64 * s + 32 * (b >> 4) + 8 * (r >> 2) + 4 * g + (r & 3);
+}
+
+// Byte of (dimension d, position p) in a block's d x B V^T tile: row-major
+// [d][B] for B <= 128; for B = 256 two [d][128] halves, positions 0 .. 127
+// first, so that every softmax step of 128 keys reads 128-byte rows.
+template <int BS>
+__host__ __device__ inline int vt_offset(int d, int p) {
+  return BS <= 128 ? d * BS + p : (p >> 7) * (kHeadDim * 128) + d * 128 + (p & 127);
 }
 
 // ------------------------------------------------------------------ amax
@@ -122,7 +131,7 @@ __global__ __launch_bounds__(256) void fp8_pack_rows_kernel(const uint16_t* __re
 
 // V^T tiles: workgroup (key block kb, KV head g) reads the block's B x d bf16
 // values, rounds them to E4M3 into LDS [key][d], and writes the d x B tile with
-// the keys in vt_key order (keys past N are zero).
+// the keys in vt_key order, laid out by vt_offset (keys past N are zero).
 template <int BS>
 __global__ __launch_bounds__(256) void fp8_pack_vt_kernel(const uint16_t* __restrict__ V, int N, int M,
                                                           const float* __restrict__ amax_v,
@@ -157,7 +166,7 @@ __global__ __launch_bounds__(256) void fp8_pack_vt_kernel(const uint16_t* __rest
       for (int e = 0; e < 4; ++e) x |= (uint32_t)tile[vt_key(p0 + 4 * q + e) * kHeadDim + d] << (8 * e);
       w[q] = x;
     }
-    *reinterpret_cast<uint4*>(out + (size_t)d * BS + p0) = make_uint4(w[0], w[1], w[2], w[3]);
+    *reinterpret_cast<uint4*>(out + vt_offset<BS>(d, p0)) = make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
 
@@ -205,10 +214,23 @@ struct AttnF8Args {
   float* lse;
 };
 
-// Query block i of query head h; k_lds, v_lds: 16 KiB each.
+// 32 bytes of the V^T operand for dimension d, PV step st of the softmax step
+// starting at key kbase, lane half `half`: positions 64 st' + 32 half .. + 31
+// of the block (st' = kbase / 64 + st) in the tile layout of vt_offset.
+template <int BS>
+__device__ __forceinline__ i32x8 read_vt32(const unsigned char* v_lds, int kbase, int d, int st, int half) {
+  if (BS == 64) return read_row32(v_lds, d >> 1, 2 * (d & 1) + half);  // two 64-key rows per 128 bytes
+  return read_row32(v_lds, kbase + d, 2 * st + half);                   // 128-key sub-tile kbase / 128
+}
+
+// Query block i of query head h; k_lds, v_lds: BS * 128 bytes each.  The
+// block's keys are taken in softmax steps of up to 128 (two for B = 256).
+template <int BS>
 __device__ __forceinline__ void attend_block_fp8(const AttnF8Args& c, int h, int i, unsigned char* k_lds,
                                                  unsigned char* v_lds) {
-  constexpr int BS = 128;
+  constexpr int SUB = BS < 128 ? BS : 128;  // keys per softmax step
+  constexpr int KT = SUB / 32;              // 32-key S^T tiles per step
+  constexpr int NST = SUB / 64;             // 64-key PV steps per softmax step
   const int group = c.Hq / c.Hkv;
   const int g = h / group;
   const int N = c.N;
@@ -248,12 +270,14 @@ __device__ __forceinline__ void attend_block_fp8(const AttnF8Args& c, int h, int
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
   f32x16 lsum = {};  // every element: the running softmax denominator of this lane's query
 
+  // Each tile is BS rows of 128 bytes (V^T: see vt_offset); a wave copies 32
+  // rows with 4 copies per lane, so 4 copies per lane per tile.
   const uint32_t k_base = lds_offset(k_lds), v_base = lds_offset(v_lds);
   int kb = count > 0 ? min(max(list[0], 0), i) : 0;
   int kb_ahead = count > 1 ? list[1] : 0;
   if (count > 0) {
     issue_tile8(kg + (size_t)kb * BS * kHeadDim, min(BS, N - kb * BS), k_base, wave, lane);
-    issue_tile8(vg + (size_t)kb * kHeadDim * BS, kHeadDim, v_base, wave, lane);
+    issue_tile8(vg + (size_t)kb * kHeadDim * BS, BS, v_base, wave, lane);
   }
   for (int n = 0; n < count; ++n) {
     const bool has_next = n + 1 < count;
@@ -265,64 +289,78 @@ __device__ __forceinline__ void attend_block_fp8(const AttnF8Args& c, int h, int
     RBS_WAIT_VMCNT(4);  // this block's K has landed (its V may still be in flight)
     __syncthreads();
 
-    f32x16 s[4];
+    // (Steps not unrolled: two unrolled 128-key steps spill heavily.)
+#pragma unroll 1
+    for (int sub = 0; sub < BS / SUB; ++sub) {
+      const int kbase = sub * SUB;
+      f32x16 s[KT];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      s[mt] = f32x16{};
+      for (int mt = 0; mt < KT; ++mt) {
+        s[mt] = f32x16{};
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) s[mt] = mfma_f8(read_row32(k_lds, 32 * mt + l32, 2 * ks + half), qreg[ks], s[mt]);
-    }
-    __syncthreads();  // every wave is done with this K tile
-    if (has_next) issue_tile8(kg + (size_t)kb_next * BS * kHeadDim, min(BS, N - kb_next * BS), k_base, wave, lane);
-    if (diag || nk < BS) {
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = 32 * mt + mfma_row(r, lane);
-          if (key >= nk || (diag && key > q_local)) s[mt][r] = -INFINITY;
-        }
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
-    mx = half_max(mx);
-    const float mxs = mx * sl;
-    if (__any(mxs > ms_run + kP8Slack)) {
-      const float ms_new = fmaxf(ms_run, mxs);
-      const float alpha = ms_new == ms_run ? 1.f : fast_exp2(ms_run - ms_new);
-      ms_run = ms_new;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) lsum[r] *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-    }
-    const float shift = (ms_run == -INFINITY ? 0.f : ms_run) - kP8Bias;
-    // P in E4M3: byte b of k-group `half` of step st holds element b % 16 of
-    // tile 2 st + b / 16.
-    i32x8 pk[2];
-#pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int t = 2 * st + (j >> 2), r0 = 4 * (j & 3);
-        pk[st][j] = pack4_fp8(fast_exp2(fmaf(s[t][r0], sl, -shift)), fast_exp2(fmaf(s[t][r0 + 1], sl, -shift)),
-                              fast_exp2(fmaf(s[t][r0 + 2], sl, -shift)), fast_exp2(fmaf(s[t][r0 + 3], sl, -shift)));
+        for (int ks = 0; ks < 2; ++ks)
+          s[mt] = mfma_f8(read_row32(k_lds, kbase + 32 * mt + l32, 2 * ks + half), qreg[ks], s[mt]);
       }
-    if (has_next) RBS_WAIT_VMCNT(4); else RBS_WAIT_VMCNT(0);  // this block's V has landed
-    __syncthreads();
+      if (sub == BS / SUB - 1) {
+        __syncthreads();  // every wave is done with this K tile
+        if (has_next)
+          issue_tile8(kg + (size_t)kb_next * BS * kHeadDim, min(BS, N - kb_next * BS), k_base, wave, lane);
+      }
+      if (diag || nk < BS) {
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
+        for (int mt = 0; mt < KT; ++mt)
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) o[dt] = mfma_f8(read_row32(v_lds, 32 * dt + l32, 2 * st + half), pk[st], o[dt]);
-      lsum = mfma_f8(ones, pk[st], lsum);
+          for (int r = 0; r < 16; ++r) {
+            const int key = kbase + 32 * mt + mfma_row(r, lane);
+            if (key >= nk || (diag && key > q_local)) s[mt][r] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < KT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
+      mx = half_max(mx);
+      const float mxs = mx * sl;
+      if (__any(mxs > ms_run + kP8Slack)) {
+        const float ms_new = fmaxf(ms_run, mxs);
+        const float alpha = ms_new == ms_run ? 1.f : fast_exp2(ms_run - ms_new);
+        ms_run = ms_new;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) lsum[r] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+      }
+      const float shift = (ms_run == -INFINITY ? 0.f : ms_run) - kP8Bias;
+      // P in E4M3: byte b of k-group `half` of PV step st holds element b % 16
+      // of tile 2 st + b / 16.
+      i32x8 pk[NST];
+#pragma unroll
+      for (int st = 0; st < NST; ++st)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int t = 2 * st + (j >> 2), r0 = 4 * (j & 3);
+          pk[st][j] = pack4_fp8(fast_exp2(fmaf(s[t][r0], sl, -shift)), fast_exp2(fmaf(s[t][r0 + 1], sl, -shift)),
+                                fast_exp2(fmaf(s[t][r0 + 2], sl, -shift)), fast_exp2(fmaf(s[t][r0 + 3], sl, -shift)));
+        }
+      if (sub == 0) {
+        // This block's V has landed.  The next block's K copies are already
+        // in flight behind it only when the block has a single step.
+        if (has_next && BS / SUB == 1) RBS_WAIT_VMCNT(4); else RBS_WAIT_VMCNT(0);
+        __syncthreads();
+      }
+#pragma unroll
+      for (int st = 0; st < NST; ++st) {
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+          o[dt] = mfma_f8(read_vt32<BS>(v_lds, kbase, 32 * dt + l32, st, half), pk[st], o[dt]);
+        lsum = mfma_f8(ones, pk[st], lsum);
+      }
     }
     __syncthreads();  // every wave is done with this V tile
-    if (has_next) issue_tile8(vg + (size_t)kb_next * kHeadDim * BS, kHeadDim, v_base, wave, lane);
+    if (has_next) issue_tile8(vg + (size_t)kb_next * kHeadDim * BS, BS, v_base, wave, lane);
     kb = kb_next;
   }
 
@@ -348,20 +386,22 @@ __device__ __forceinline__ void attend_block_fp8(const AttnF8Args& c, int h, int
 }
 
 // One workgroup per (query head, query block), ordered by work_item.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fp8_kernel(AttnF8Args c) {
-  __shared__ __align__(1024) unsigned char k_lds[128 * 128];
-  __shared__ __align__(1024) unsigned char v_lds[kHeadDim * 128];
+template <int BS>
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fp8_kernel(AttnF8Args c) {
+  __shared__ __align__(1024) unsigned char k_lds[BS * 128];
+  __shared__ __align__(1024) unsigned char v_lds[kHeadDim * BS];
   int h, i;
   work_item(c.M, c.Hq / c.Hkv, h, i);
-  attend_block_fp8(c, h, i, k_lds, v_lds);
+  attend_block_fp8<BS>(c, h, i, k_lds, v_lds);
 }
 
 // Persistent form (the queues of take_slot): the same work slots on the same
 // XCDs in the same order, bit-identical results.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fp8_queue_kernel(
+template <int BS>
+__global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fp8_queue_kernel(
     AttnF8Args c, int* __restrict__ queue) {
-  __shared__ __align__(1024) unsigned char k_lds[128 * 128];
-  __shared__ __align__(1024) unsigned char v_lds[kHeadDim * 128];
+  __shared__ __align__(1024) unsigned char k_lds[BS * 128];
+  __shared__ __align__(1024) unsigned char v_lds[kHeadDim * BS];
   __shared__ int lds_slot;
   const int total = c.M * c.Hq;
   for (;;) {
@@ -369,7 +409,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     if (slot >= total) break;
     int h, i;
     work_of(slot, total, c.M, c.Hq / c.Hkv, h, i);
-    attend_block_fp8(c, h, i, k_lds, v_lds);
+    attend_block_fp8<BS>(c, h, i, k_lds, v_lds);
     __syncthreads();  // tiles and lds_slot free for the next item
   }
 }
@@ -391,21 +431,51 @@ hipError_t launch_fp8_amax(const uint16_t* Q, const uint16_t* K, const uint16_t*
 }
 
 hipError_t launch_fp8_pack(const uint16_t* Q, const uint16_t* K, const uint16_t* V, int n_tokens, int n_q_heads,
-                           int n_kv_heads, int n_blocks, const float* amax, uint8_t* Q8, uint8_t* K8, uint8_t* V8t,
-                           hipStream_t s) {
+                           int n_kv_heads, int block_size, int n_blocks, const float* amax, uint8_t* Q8, uint8_t* K8,
+                           uint8_t* V8t, hipStream_t s) {
   const int64_t chunks = (int64_t)n_tokens * kHeadDim / 8;
   const int gx = (int)((chunks + 255) / 256 < 512 ? (chunks + 255) / 256 : 512);
   hipLaunchKernelGGL(fp8_pack_rows_kernel, dim3(gx, n_q_heads), dim3(256), 0, s, Q, chunks, amax, Q8);
   hipLaunchKernelGGL(fp8_pack_rows_kernel, dim3(gx, n_kv_heads), dim3(256), 0, s, K, chunks, amax + n_q_heads, K8);
-  hipLaunchKernelGGL(fp8_pack_vt_kernel<128>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, n_tokens, n_blocks,
-                     amax + n_q_heads + n_kv_heads, V8t);
+  const float* amax_v = amax + n_q_heads + n_kv_heads;
+  switch (block_size) {
+    case 64:
+      hipLaunchKernelGGL(fp8_pack_vt_kernel<64>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, n_tokens, n_blocks,
+                         amax_v, V8t);
+      break;
+    case 128:
+      hipLaunchKernelGGL(fp8_pack_vt_kernel<128>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, n_tokens,
+                         n_blocks, amax_v, V8t);
+      break;
+    case 256:
+      hipLaunchKernelGGL(fp8_pack_vt_kernel<256>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, n_tokens,
+                         n_blocks, amax_v, V8t);
+      break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int BS>
+static hipError_t launch_attention_fp8_bs(const AttnF8Args& a, int* queue, hipStream_t s) {
+  const int total = a.M * a.Hq;
+  if (queue == nullptr) {
+    hipLaunchKernelGGL(attn_fp8_kernel<BS>, dim3(total), dim3(BS * 2), 0, s, a);
+    return hipGetLastError();
+  }
+  hipError_t e = reset_queues(queue, s);
+  if (e != hipSuccess) return e;
+  int grid = 0;
+  e = resident_grid<attn_fp8_queue_kernel<BS>>(BS * 2, total, &grid);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_fp8_queue_kernel<BS>, dim3(grid), dim3(BS * 2), 0, s, a, queue);
   return hipGetLastError();
 }
 
 hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint8_t* V8t, const float* amax,
-                                int n_tokens, int n_q_heads, int n_kv_heads, int n_blocks, const int32_t* counts,
-                                const int32_t* indices, int64_t capacity, float scale, uint16_t* O, float* lse,
-                                int* queue, hipStream_t s) {
+                                int n_tokens, int n_q_heads, int n_kv_heads, int block_size, int n_blocks,
+                                const int32_t* counts, const int32_t* indices, int64_t capacity, float scale,
+                                uint16_t* O, float* lse, int* queue, hipStream_t s) {
   AttnF8Args a;
   a.Q8 = Q8;
   a.K8 = K8;
@@ -421,18 +491,12 @@ hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint
   a.capacity = capacity;
   a.O = O;
   a.lse = lse;
-  const int total = n_blocks * n_q_heads;
-  if (queue == nullptr) {
-    hipLaunchKernelGGL(attn_fp8_kernel, dim3(total), dim3(256), 0, s, a);
-    return hipGetLastError();
+  switch (block_size) {
+    case 64: return launch_attention_fp8_bs<64>(a, queue, s);
+    case 128: return launch_attention_fp8_bs<128>(a, queue, s);
+    case 256: return launch_attention_fp8_bs<256>(a, queue, s);
+    default: return hipErrorInvalidValue;
   }
-  hipError_t e = reset_queues(queue, s);
-  if (e != hipSuccess) return e;
-  int grid = 0;
-  e = resident_grid<attn_fp8_queue_kernel>(256, total, &grid);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_fp8_queue_kernel, dim3(grid), dim3(256), 0, s, a, queue);
-  return hipGetLastError();
 }
 
 }  // namespace rbs

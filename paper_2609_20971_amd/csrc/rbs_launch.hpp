@@ -122,12 +122,12 @@ hipError_t launch_dense_indices(int n_q_heads, int n_blocks, int64_t capacity, i
 hipError_t launch_fp8_amax(const uint16_t* Q, const uint16_t* K, const uint16_t* V, int n_tokens, int n_q_heads,
                            int n_kv_heads, float* amax, hipStream_t s);
 hipError_t launch_fp8_pack(const uint16_t* Q, const uint16_t* K, const uint16_t* V, int n_tokens, int n_q_heads,
-                           int n_kv_heads, int n_blocks, const float* amax, uint8_t* Q8, uint8_t* K8, uint8_t* V8t,
-                           hipStream_t s);
+                           int n_kv_heads, int block_size, int n_blocks, const float* amax, uint8_t* Q8, uint8_t* K8,
+                           uint8_t* V8t, hipStream_t s);
 hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint8_t* V8t, const float* amax,
-                                int n_tokens, int n_q_heads, int n_kv_heads, int n_blocks, const int32_t* counts,
-                                const int32_t* indices, int64_t capacity, float scale, uint16_t* O, float* lse,
-                                int* queue, hipStream_t s);
+                                int n_tokens, int n_q_heads, int n_kv_heads, int block_size, int n_blocks,
+                                const int32_t* counts, const int32_t* indices, int64_t capacity, float scale,
+                                uint16_t* O, float* lse, int* queue, hipStream_t s);
 
 // Varlen launchers: the Args hold the batch totals (n_tokens = T, n_blocks and
 // capacity = the table's last offsets); every sequence runs in the same launch.

@@ -278,15 +278,18 @@ def test_fp8_sizes_and_validation():
     rbs, lib = _lib()
     s = rbs.make_shape(1000, 4, 2, 128)
     assert rbs.rbs_fp8_vt_bytes(s) == 2 * 8 * 128 * 128
-    assert rbs.rbs_fp8_vt_bytes(rbs.make_shape(1000, 4, 2, 64)) == 0
+    assert rbs.rbs_fp8_vt_bytes(rbs.make_shape(1000, 4, 2, 64)) == 2 * 16 * 128 * 64
+    assert rbs.rbs_fp8_vt_bytes(rbs.make_shape(1000, 4, 2, 256)) == 2 * 4 * 128 * 256
+    assert rbs.rbs_fp8_vt_bytes(rbs.make_shape(1000, 4, 2, 32)) == 0
     S = ctypes.byref(s)
     assert lib.rbs_fp8_amax(S, None, FAKE, FAKE, FAKE, None) == 1
     assert lib.rbs_fp8_amax(S, FAKE, FAKE, FAKE, MIS, None) == 5
     assert lib.rbs_fp8_pack(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == 1
     assert lib.rbs_fp8_pack(S, FAKE, FAKE, FAKE, FAKE, FAKE, MIS, FAKE, None) == 5
-    b64 = rbs.make_shape(1000, 4, 2, 64)
-    assert lib.rbs_fp8_pack(ctypes.byref(b64), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 3
-    assert lib.rbs_sparse_prefill_fp8(ctypes.byref(b64), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None,
+    # Block sizes other than 64/128/256 are refused before anything is launched.
+    b32 = rbs.make_shape(1000, 4, 2, 32)
+    assert lib.rbs_fp8_pack(ctypes.byref(b32), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 3
+    assert lib.rbs_sparse_prefill_fp8(ctypes.byref(b32), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None,
                                       None, None) == 3
     assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, None, FAKE, FAKE, FAKE, 0.0, FAKE, None, None, None) == 1
     assert lib.rbs_sparse_prefill_fp8(S, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, float("nan"), FAKE, None, None, None) == 4

@@ -43,6 +43,14 @@ def _vt_key(p: int) -> int:
     return 64 * s + 32 * (b >> 4) + 8 * (r >> 2) + 4 * g + (r & 3)
 
 
+def _vt_layout(T: np.ndarray, B: int) -> np.ndarray:
+    """Bytes of one block's V^T tile from its [d][position] matrix T, in the
+    documented layout: row-major [d][B], or for B = 256 two [d][128] halves."""
+    if B <= 128:
+        return T.reshape(-1)
+    return np.concatenate([T[:, :128].reshape(-1), T[:, 128:].reshape(-1)])
+
+
 def _run(w: Workload, tau=None, forced=None):
     import torch
     import paper_2609_20971_amd as rbs
@@ -80,15 +88,16 @@ def _check_pack(r, ref, w):
     assert np.array_equal(f8.Q8.cpu().numpy(), ref["q"][1]), "Q codes"
     assert np.array_equal(f8.K8.cpu().numpy(), ref["k"][1]), "K codes"
     M = w.n_blocks
-    vt = f8.V8t.cpu().numpy().reshape(Hkv, M, 128, B)
+    vt = f8.V8t.cpu().numpy().reshape(Hkv, M, 128 * B)
     keys = np.array([_vt_key(p) for p in range(B)])
+    assert np.array_equal(np.sort(keys), np.arange(B))  # a permutation of the block's keys
     vcodes = ref["v"][1]
     for g in range(Hkv):
         for b in range(M):
             want = np.zeros((B, 128), dtype=np.uint8)
             n = min(B, N - b * B)
             want[:n] = vcodes[g, b * B:b * B + n]
-            assert np.array_equal(vt[g, b], want[keys].T), f"V^T tile ({g}, {b})"
+            assert np.array_equal(vt[g, b], _vt_layout(want[keys].T, B)), f"V^T tile ({g}, {b})"
 
 
 def _bound(Qh, Kg, Vg, B, i, ids, O_ref, scale):
@@ -150,13 +159,16 @@ def _check_attention(r, ref, w, rows):
 
 
 @pytest.mark.parametrize("variant", [
-    dict(seq_len=1000, n_q_heads=4, n_kv_heads=2, seed=21),   # ragged tail, GQA 2:1
-    dict(seq_len=2048, n_q_heads=2, n_kv_heads=1, seed=22),
-    dict(seq_len=100, n_q_heads=2, n_kv_heads=2, seed=23),    # N < B
+    dict(seq_len=1000, n_q_heads=4, n_kv_heads=2, seed=21, block_size=128),   # ragged tail, GQA 2:1
+    dict(seq_len=2048, n_q_heads=2, n_kv_heads=1, seed=22, block_size=128),
+    dict(seq_len=100, n_q_heads=2, n_kv_heads=2, seed=23, block_size=128),    # N < B
+    dict(seq_len=1000, n_q_heads=4, n_kv_heads=2, seed=24, block_size=64),    # one 64-key PV step
+    dict(seq_len=1500, n_q_heads=4, n_kv_heads=2, seed=25, block_size=256),   # two 128-key softmax steps
+    dict(seq_len=200, n_q_heads=2, n_kv_heads=1, seed=26, block_size=256),    # N < B, one partial block
 ])
 def test_fp8_pack_and_attention(variant):
-    w = WORKLOADS["tiny-2k"].with_(name="fp8", block_size=128, needles_per_kv_head=2, **variant)
-    _say(f"[fp8] N={w.seq_len} Hq={w.n_q_heads} Hkv={w.n_kv_heads}")
+    w = WORKLOADS["tiny-2k"].with_(name="fp8", needles_per_kv_head=2, **variant)
+    _say(f"[fp8] B={w.block_size} N={w.seq_len} Hq={w.n_q_heads} Hkv={w.n_kv_heads}")
     r = _run(w)
     ref = _oracle_fp8(r["inp"])
     _check_pack(r, ref, w)
@@ -166,8 +178,9 @@ def test_fp8_pack_and_attention(variant):
     assert ratio <= 1.0
 
 
-def test_fp8_full_selection_is_dense_attention_on_the_fp8_values():
-    w = WORKLOADS["tiny-2k"].with_(name="fp8-dense", block_size=128, seq_len=1536, needles_per_kv_head=2, seed=24)
+@pytest.mark.parametrize("B", [64, 128, 256])
+def test_fp8_full_selection_is_dense_attention_on_the_fp8_values(B):
+    w = WORKLOADS["tiny-2k"].with_(name="fp8-dense", block_size=B, seq_len=1536, needles_per_kv_head=2, seed=24)
     r = _run(w, tau=(0.0, 0.0), forced=(1, 2, 0))
     counts = r["counts"].cpu().numpy()
     assert (counts == np.arange(w.n_blocks)[None, :] + 1).all()

@@ -127,12 +127,13 @@ def test_queue_varlen_equals_one_workgroup_per_item(B):
     _assert_same(out[0], out[1], f"varlen B={B}")
 
 
-def test_queue_fp8_equals_one_workgroup_per_item():
+@pytest.mark.parametrize("B", [64, 128, 256])
+def test_queue_fp8_equals_one_workgroup_per_item(B):
     import torch
     import paper_2609_20971_amd as rbs
-    w = WORKLOADS["tiny-2k"].with_(name="queue-fp8", seq_len=3000, n_q_heads=4, n_kv_heads=2, block_size=128,
+    w = WORKLOADS["tiny-2k"].with_(name="queue-fp8", seq_len=3000, n_q_heads=4, n_kv_heads=2, block_size=B,
                                    seed=44)
-    _say("[queue] fp8")
+    _say(f"[queue] fp8 B={B}")
     shape, Q, K, V, counts, indices = _setup(w)
     f8 = rbs.rbs_fp8_prepare(shape, Q, K, V)
     out = []
