@@ -73,6 +73,90 @@ def parse():
     return p.parse_args()
 
 
+PEAK_SCLK_MHZ = 2400.0        # clock the vendor MFMA figure assumes
+
+
+class SclkSampler:
+    """Shader clock while a region runs: a thread reads the current level of
+    the GPU's pp_dpm_sclk (sysfs, the starred line) every 5 ms.  None when the
+    file is not readable."""
+
+    def __init__(self):
+        import glob
+        files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = files[0] if len(files) == 1 else None
+        self.mhz = []
+        self._stop = False
+        self._thread = None
+
+    def _read(self):
+        try:
+            with open(self.path) as f:
+                for line in f:
+                    if line.rstrip().endswith("*"):
+                        return float(line.split(":")[1].strip().lower().split("mhz")[0])
+        except (OSError, ValueError, IndexError):
+            return None
+        return None
+
+    def _run(self):
+        while not self._stop:
+            v = self._read()
+            if v is not None:
+                self.mhz.append(v)
+            time.sleep(0.005)
+
+    def __enter__(self):
+        if self.path is not None:
+            import threading
+            self._thread = threading.Thread(target=self._run, daemon=True)
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop = True
+        if self._thread is not None:
+            self._thread.join()
+
+    def summary(self):
+        import numpy as np
+        if not self.mhz:
+            return None
+        a = np.array(self.mhz)
+        return {"median": float(np.median(a)), "min": float(a.min()), "max": float(a.max()), "samples": len(a),
+                "source": self.path}
+
+
+def copy_ceiling_gbps(torch, dev, reps: int = 5) -> float:
+    """Device-to-device copy of 1 GiB (read + write counted), median of reps."""
+    import numpy as np
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    ts = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b))
+    del src, dst
+    return 2.0 * (1 << 30) / (float(np.median(ts)) * 1e-3) / 1e9
+
+
+def exact_causal_flops(w, counts_np) -> int:
+    """QK^T and PV flops over the (query, key) pairs with key <= query of the
+    executed blocks: full B x B blocks off the diagonal (every list holds the
+    diagonal block, and only the last key block can be partial, which only a
+    diagonal can be), nq (nq + 1) / 2 pairs on it."""
+    import numpy as np
+    N, B, d, M = w.seq_len, w.block_size, w.head_dim, w.n_blocks
+    nq = np.minimum(B, N - np.arange(M) * B).astype(np.int64)
+    per_row = (counts_np.astype(np.int64) - 1) * nq[None, :] * B + (nq * (nq + 1) // 2)[None, :]
+    return int(4 * d * per_row.sum())
+
+
 def algorithmic(w, counts_sum: int):
     """Bytes / flops each stage must move or compute per launch."""
     N, Hq, Hkv, d, B = w.seq_len, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size
@@ -202,11 +286,12 @@ def main():
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for k in range(args.steps):
-        step(events[k])
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
+    with SclkSampler() as sclk:
+        t_start = time.perf_counter()
+        for k in range(args.steps):
+            step(events[k])
+        torch.cuda.synchronize()
+        wall_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
     stage_ms = np.zeros(3)
     for ev in events:
         stage_ms += [ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])]
@@ -251,6 +336,10 @@ def main():
     counts_sum = int(counts_np.sum())
     alg = algorithmic(w, counts_sum)
     density = counts_sum / alg["pairs"]
+    causal_flops = exact_causal_flops(w, counts_np)
+    sclk_summary = sclk.summary()
+    copy_gbps = copy_ceiling_gbps(torch, dev)
+    _log(f"[bench] shader clock during the timed steps: {sclk_summary}; 1 GiB copy {copy_gbps:.0f} GB/s")
 
     # Own dense path: same attention kernel over every causal block.
     dense_ms = None
@@ -305,13 +394,21 @@ def main():
                        "alg_flops": alg["select_flops"], "TFLOPs": round(select_tflops, 1),
                        "mfma_frac": round(select_tflops / PEAK_BF16_TFLOPS, 4)},
             "attn": {"ms": round(float(stage_ms[2]), 4), "alg_flops": alg["attn_flops"],
-                     "TFLOPs": round(attn_tflops, 1), "executed_pairs": counts_sum},
+                     "TFLOPs": round(attn_tflops, 1), "executed_pairs": counts_sum,
+                     "causal_flops": causal_flops,
+                     "exps": counts_sum * w.block_size * w.block_size},
         },
         "fused": ({"ms_per_step": round(sum(fused_ms), 4), "stats_ms": round(fused_ms[0], 4),
                    "select_attend_ms": round(fused_ms[1], 4), "steps": args.fused_steps}
                   if fused_ms else None),
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic},
+        # Context for the roofline: the shader clock measured while the steps
+        # ran (the vendor peak assumes 2.4 GHz) and a plain copy's bandwidth.
+        "sclk_mhz": sclk_summary,
+        "mfma_frac_at_sclk": (round(attn_tflops / (PEAK_BF16_TFLOPS * sclk_summary["median"] / PEAK_SCLK_MHZ), 4)
+                              if sclk_summary else None),
+        "copy_GBps": round(copy_gbps, 1),
     }
 
     if not args.no_cpu_baseline:

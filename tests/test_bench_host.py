@@ -1,0 +1,46 @@
+"""Host-side accounting of bench.py (no GPU): the exact causal flop count and
+the argument contract for several GPUs."""
+
+from __future__ import annotations
+
+import subprocess
+import sys
+from pathlib import Path
+
+import numpy as np
+
+import bench
+from synth import WORKLOADS
+
+ROOT = Path(__file__).resolve().parents[1]
+
+
+def test_exact_causal_flops_of_full_lists_is_the_dense_causal_count():
+    # Every block 0..i in every row: the pairs (query, key <= query) of dense
+    # causal attention, N (N + 1) / 2 per head, 4 d flops each (QK^T and PV).
+    for n in (2048, 2000, 64, 1):
+        w = WORKLOADS["tiny-2k"].with_(seq_len=n)
+        counts = np.tile(np.arange(1, w.n_blocks + 1), (w.n_q_heads, 1))
+        assert bench.exact_causal_flops(w, counts) == 4 * w.head_dim * w.n_q_heads * n * (n + 1) // 2
+
+
+def test_exact_causal_flops_of_diagonal_only_lists():
+    # Only the diagonal block of each row: B (B + 1) / 2 pairs per full block.
+    w = WORKLOADS["tiny-2k"]
+    B = w.block_size
+    counts = np.ones((w.n_q_heads, w.n_blocks), dtype=np.int64)
+    assert bench.exact_causal_flops(w, counts) == 4 * w.head_dim * w.n_q_heads * w.n_blocks * B * (B + 1) // 2
+
+
+def test_algorithmic_attention_flops_count_whole_blocks():
+    w = WORKLOADS["tiny-2k"]
+    alg = bench.algorithmic(w, 10)
+    assert alg["attn_flops"] == 4 * w.block_size ** 2 * w.head_dim * 10
+    assert alg["pairs"] == w.n_q_heads * w.n_blocks * (w.n_blocks + 1) // 2
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, str(ROOT / "bench.py"), "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in (r.stdout + r.stderr) or "1 GPU" in (r.stdout + r.stderr)
