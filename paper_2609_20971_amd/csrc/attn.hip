@@ -118,10 +118,6 @@ __global__ void dense_indices_kernel(int M, int64_t capacity, int32_t* __restric
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int total = a.n_blocks * a.n_q_heads;
   const AttnCore c = make_attn_core(a);
-  if (a.queue != nullptr) {
-    hipError_t e = reset_queues(a.queue, s);
-    if (e != hipSuccess) return e;
-  }
   int grid = 0;
 #define RBS_ATTN_CASE(BSZ)                                                                                     \
   case BSZ:                                                                                                    \
@@ -129,7 +125,8 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(attn_kernel<BSZ>, dim3(total), dim3(BSZ * 2), 0, s, c, a.counts, a.indices,          \
                          a.capacity);                                                                          \
     } else {                                                                                                   \
-      const hipError_t e = resident_grid<attn_queue_kernel<BSZ>>(BSZ * 2, total, &grid);                       \
+      hipError_t e = resident_grid<attn_queue_kernel<BSZ>>(BSZ * 2, total, &grid);                             \
+      if (e == hipSuccess) e = reset_queues(a.queue, s);                                                       \
       if (e != hipSuccess) return e;                                                                           \
       hipLaunchKernelGGL(attn_queue_kernel<BSZ>, dim3(grid), dim3(BSZ * 2), 0, s, c, a.counts, a.indices,     \
                          a.capacity, total, a.queue);                                                          \
@@ -158,17 +155,14 @@ __global__ void dense_indices_varlen_kernel(const SeqTable t, int32_t* __restric
 hipError_t launch_attention_varlen(const AttnArgs& a, const SeqTable& t, hipStream_t s) {
   const int total = t.blk[t.n] * a.n_q_heads;
   const AttnCore c = make_attn_core(a);
-  if (a.queue != nullptr) {
-    hipError_t e = reset_queues(a.queue, s);
-    if (e != hipSuccess) return e;
-  }
   int grid = 0;
 #define RBS_ATTN_VARLEN_CASE(BSZ)                                                                              \
   case BSZ:                                                                                                    \
     if (a.queue == nullptr) {                                                                                  \
       hipLaunchKernelGGL(attn_varlen_kernel<BSZ>, dim3(total), dim3(BSZ * 2), 0, s, c, a.counts, a.indices, t); \
     } else {                                                                                                   \
-      const hipError_t e = resident_grid<attn_varlen_queue_kernel<BSZ>>(BSZ * 2, total, &grid);                \
+      hipError_t e = resident_grid<attn_varlen_queue_kernel<BSZ>>(BSZ * 2, total, &grid);                      \
+      if (e == hipSuccess) e = reset_queues(a.queue, s);                                                       \
       if (e != hipSuccess) return e;                                                                           \
       hipLaunchKernelGGL(attn_varlen_queue_kernel<BSZ>, dim3(grid), dim3(BSZ * 2), 0, s, c, a.counts,         \
                          a.indices, t, total, a.queue);                                                        \

@@ -463,10 +463,9 @@ static hipError_t launch_attention_fp8_bs(const AttnF8Args& a, int* queue, hipSt
     hipLaunchKernelGGL(attn_fp8_kernel<BS>, dim3(total), dim3(BS * 2), 0, s, a);
     return hipGetLastError();
   }
-  hipError_t e = reset_queues(queue, s);
-  if (e != hipSuccess) return e;
   int grid = 0;
-  e = resident_grid<attn_fp8_queue_kernel<BS>>(BS * 2, total, &grid);
+  hipError_t e = resident_grid<attn_fp8_queue_kernel<BS>>(BS * 2, total, &grid);
+  if (e == hipSuccess) e = reset_queues(queue, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(attn_fp8_queue_kernel<BS>, dim3(grid), dim3(BS * 2), 0, s, a, queue);
   return hipGetLastError();

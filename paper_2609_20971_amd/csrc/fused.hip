@@ -74,10 +74,6 @@ hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStr
   const SelectCore sc = make_select_core(sa);
   const AttnCore ac = make_attn_core(aa);
   const size_t smem = fused_smem_bytes(sa.block_size, sa.n_blocks);
-  if (aa.queue != nullptr) {
-    hipError_t e = reset_queues(aa.queue, s);
-    if (e != hipSuccess) return e;
-  }
   int grid = 0;
 #define RBS_FUSED_CASE(BSZ)                                                                                   \
   case BSZ: {                                                                                                 \
@@ -91,6 +87,7 @@ hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStr
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);              \
       if (e != hipSuccess) return e;                                                                          \
       e = resident_grid<select_attend_queue_kernel<BSZ>>(BSZ * 2, total, &grid, smem);                        \
+      if (e == hipSuccess) e = reset_queues(aa.queue, s);                                                     \
       if (e != hipSuccess) return e;                                                                          \
       hipLaunchKernelGGL(select_attend_queue_kernel<BSZ>, dim3(grid), dim3(BSZ * 2), smem, s, sc, ac, total,  \
                          aa.queue);                                                                           \
