@@ -310,23 +310,41 @@ __device__ __forceinline__ void work_item(int M, int group, int& h, int& i) {
 // reads the K/V blocks) it would have run in the one-per-slot launch, in the
 // same order, but a workgroup takes its next slot as soon as it is free
 // instead of waiting for the in-order dispatcher, which holds back every XCD
-// while one of them has no free slot.  kQueueInts int32 counters, zeroed by
-// reset_queues before each launch.
+// while one of them has no free slot.  Once its own queue is empty, a
+// workgroup takes the remaining slots of the other queues in turn (queue
+// j % 8 + 1, + 2, ... modulo 8), so that the XCDs that run faster share the
+// tail of the slower ones.  kQueueInts int32 counters, zeroed by reset_queues
+// before each launch.
 
-// The next work slot of this workgroup's queue, the same value in every
-// thread.  Wave 0 takes the ticket (one increment, made by its lane 0; the
-// other lanes add zero) and passes it through LDS; the barrier makes it
-// visible and is also the one every wave passes before the tiles of the
-// previous item may be overwritten.  Control flow stays uniform throughout:
-// no lane-divergent branch surrounds the barrier.
-__device__ __forceinline__ int take_slot(int* queue, int* lds_slot) {
-  const int x = blockIdx.x & (kQueues - 1);
-  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) == 0) {
-    const int t = atomicAdd(queue + x, (threadIdx.x & 63) == 0 ? 1 : 0);
-    *lds_slot = __builtin_amdgcn_readfirstlane(t);
+// Cursor of a workgroup over the queues: the queue it takes tickets from and
+// the number of queues it has not yet found empty.
+struct QueueCursor {
+  int q, left;
+};
+
+__device__ __forceinline__ QueueCursor first_queue() { return {(int)(blockIdx.x & (kQueues - 1)), kQueues}; }
+
+// The next work slot (< total) for this workgroup, the same value in every
+// thread, or -1 once every queue is empty.  Wave 0 takes a ticket (one
+// increment, made by its lane 0; the other lanes add zero) and passes it
+// through LDS; the barrier makes it visible and is also the one every wave
+// passes before the tiles of the previous item may be overwritten.  A ticket
+// past the end of its queue means the queue is empty (tickets only grow).
+// Control flow stays uniform throughout: no lane-divergent branch surrounds a
+// barrier.
+__device__ __forceinline__ int next_slot(int* queue, int total, int* lds_slot, QueueCursor& cur) {
+  for (;;) {
+    if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) == 0) {
+      const int t = atomicAdd(queue + cur.q, (threadIdx.x & 63) == 0 ? 1 : 0);
+      *lds_slot = __builtin_amdgcn_readfirstlane(t);
+    }
+    __syncthreads();
+    const int slot = kQueues * __builtin_amdgcn_readfirstlane(*lds_slot) + cur.q;
+    if (slot < total) return slot;
+    if (--cur.left == 0) return -1;
+    cur.q = (cur.q + 1) & (kQueues - 1);
+    __syncthreads();  // every wave has read lds_slot before wave 0 writes the next ticket
   }
-  __syncthreads();
-  return kQueues * __builtin_amdgcn_readfirstlane(*lds_slot) + x;
 }
 
 // Zero the kQueueInts counters of a persistent launch (a kernel, not a memset,

@@ -2,9 +2,10 @@
 // step).  The work of one (query head, query block) is attend_block
 // (attend_block.hpp).  Two launches of the same work: one workgroup per
 // (query head, query block), or a persistent grid that takes them from the
-// per-XCD queues of take_slot (same slots on the same XCDs, in the same
-// order, bit-identical results; fewer idle workgroup slots when the rows'
-// lengths differ a lot, as a sparse selection's do).
+// per-XCD queues of next_slot (the same slots on the same XCDs in the same
+// order, apart from the tail that other XCDs take over; bit-identical
+// results; fewer idle workgroup slots when the rows' lengths differ a lot,
+// as a sparse selection's do).
 #include "attend_block.hpp"
 #include "rbs_launch.hpp"
 
@@ -37,9 +38,10 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   __shared__ __align__(1024) unsigned char k_lds[BS * 256];
   __shared__ __align__(1024) unsigned char v_lds[BS * 256];
   __shared__ int lds_slot;
+  QueueCursor cur = first_queue();
   for (;;) {
-    const int slot = take_slot(queue, &lds_slot);
-    if (slot >= total) break;
+    const int slot = next_slot(queue, total, &lds_slot, cur);
+    if (slot < 0) break;
     attend_slot<BS>(c, counts, indices, capacity, slot, total, k_lds, v_lds);
     __syncthreads();  // tiles and lds_slot free for the next item
   }
@@ -89,9 +91,10 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   __shared__ __align__(1024) unsigned char k_lds[BS * 256];
   __shared__ __align__(1024) unsigned char v_lds[BS * 256];
   __shared__ int lds_slot;
+  QueueCursor cur = first_queue();
   for (;;) {
-    const int slot = take_slot(queue, &lds_slot);
-    if (slot >= total) break;
+    const int slot = next_slot(queue, total, &lds_slot, cur);
+    if (slot < 0) break;
     attend_slot_varlen<BS>(c, counts, indices, t, slot, total, k_lds, v_lds);
     __syncthreads();
   }

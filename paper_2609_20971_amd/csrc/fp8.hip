@@ -395,8 +395,8 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   attend_block_fp8<BS>(c, h, i, k_lds, v_lds);
 }
 
-// Persistent form (the queues of take_slot): the same work slots on the same
-// XCDs in the same order, bit-identical results.
+// Persistent form (the queues of next_slot): the same work slots, on the same
+// XCDs in the same order apart from the tail, bit-identical results.
 template <int BS>
 __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fp8_queue_kernel(
     AttnF8Args c, int* __restrict__ queue) {
@@ -404,9 +404,10 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   __shared__ __align__(1024) unsigned char v_lds[kHeadDim * BS];
   __shared__ int lds_slot;
   const int total = c.M * c.Hq;
+  QueueCursor cur = first_queue();
   for (;;) {
-    const int slot = take_slot(queue, &lds_slot);
-    if (slot >= total) break;
+    const int slot = next_slot(queue, total, &lds_slot, cur);
+    if (slot < 0) break;
     int h, i;
     work_of(slot, total, c.M, c.Hq / c.Hkv, h, i);
     attend_block_fp8<BS>(c, h, i, k_lds, v_lds);

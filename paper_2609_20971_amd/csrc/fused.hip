@@ -36,8 +36,8 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       smem + BS * 256);
 }
 
-// Persistent form (the queues of take_slot): the same work slots on the same
-// XCDs in the same order, bit-identical results.
+// Persistent form (the queues of next_slot): the same work slots, on the same
+// XCDs in the same order apart from the tail, bit-identical results.
 template <int BS>
 __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void select_attend_queue_kernel(
     SelectCore sc, AttnCore ac, int total, int* __restrict__ queue) {
@@ -45,9 +45,10 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   __shared__ int lds_slot;
   typedef __attribute__((address_space(3))) int32_t lds_i32;
   lds_i32* list_lds = (lds_i32*)(smem + fused_region_bytes<BS>(ac.M));
+  QueueCursor cur = first_queue();
   for (;;) {
-    const int slot = take_slot(queue, &lds_slot);
-    if (slot >= total) break;
+    const int slot = next_slot(queue, total, &lds_slot, cur);
+    if (slot < 0) break;
     int h, i;
     work_of(slot, total, ac.M, ac.group, h, i);
     const int count = select_block<BS>(sc, h, i, smem, list_lds);
