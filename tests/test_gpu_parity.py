@@ -208,9 +208,20 @@ def test_qwen3_30b_32k_select_full_attention_sampled():
 def test_qwen3_30b_128k_sampled():
     """The headline shape, in the launch configuration the benchmark times;
     selection and attention checked on sampled rows."""
+    import torch
+    import paper_2609_20971_amd as rbs
     w = WORKLOADS["qwen3-30b-a3b-128k"]
     rows = H.sample_rows(w.n_q_heads, w.n_blocks, 24, seed=2, include=[(5, 1023), (31, 700), (0, 3)])
-    _full_check(w, select_rows=rows, attn_rows=rows[:10])
+    r, _ = _full_check(w, select_rows=rows, attn_rows=rows[:10])
+    # The benchmark's (persistent) launch against one workgroup per (head,
+    # query block) on the same lists: every output bit identical.
+    lse = torch.empty_like(r["lse"])
+    O = rbs.rbs_sparse_prefill(r["shape"], r["Qd"], r["Kd"], r["Vd"], r["counts"], r["indices"], 0.0, lse=lse,
+                               workspace=None)
+    torch.cuda.synchronize()
+    assert torch.equal(O.view(torch.int16), r["O"].view(torch.int16))
+    assert torch.equal(lse, r["lse"])
+    _say(f"[parity] {w.name}: persistent and per-item launches bit-identical")
 
 
 @pytest.mark.slow
