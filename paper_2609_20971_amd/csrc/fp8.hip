@@ -175,8 +175,9 @@ __global__ __launch_bounds__(256) void fp8_pack_vt_kernel(const uint16_t* __rest
 // Physical 16-byte chunk of logical chunk c in a staged 128-byte row r.
 __device__ __forceinline__ int f8swz(int r, int c) { return c ^ (r & 7); }
 
-// Wave w copies rows 32w .. 32w + 31 of a 128 x 128-byte tile (4 copies of 8
-// rows each).  Rows at or past nrows repeat row nrows - 1.
+// Wave w copies rows 32w .. 32w + 31 of a tile of 128-byte rows (4 copies of
+// 8 rows each; the B / 32 waves of a workgroup cover B rows).  Rows at or past
+// nrows repeat row nrows - 1.
 __device__ __forceinline__ void issue_tile8(const uint8_t* tile_base, int nrows, uint32_t lds_base, int wave,
                                             int lane) {
   const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds_base + (uint32_t)(32 * wave) * 128u);
