@@ -167,7 +167,9 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
     RBS_WAIT_VMCNT(8);  // this block's K has landed (its V may still be in flight)
     __syncthreads();
 
-#pragma unroll
+    // Softmax steps of a block kept as a loop: unrolled, B = 256's two steps
+    // spilled inside the block loop (~230 scratch accesses per block).
+#pragma unroll 1
     for (int sub = 0; sub < BS / SUB; ++sub) {
       const int kbase = sub * SUB;
       f32x16 s[KT];
