@@ -7,7 +7,7 @@
 // centroid), plus the select-ready f16 copy of the centroid.
 //
 // quantile_kernel: one workgroup per KV head finds the head's 0.5 / 0.9 radius
-// quantiles with an in-LDS radix select over its M radii and writes beta and
+// quantiles with an in-LDS radix select over its M radii (order_stats4) and writes beta and
 // the select-ready uplift of every block.  It is a separate launch because a
 // device-wide "last workgroup" hand-off would need an agent-scope release per
 // workgroup, which on a multi-XCD gfx950 writes back the whole L2 each time.
@@ -19,56 +19,126 @@ namespace rbs {
 constexpr int kStatsThreads = 256;
 constexpr int kMaxBlocks = 4096;
 
-// Values of four order statistics (0-based ranks) of n non-negative floats
+// Values of the order statistics of ranks ka, ka + 1, kb and kb + 1 (0-based;
+// a rank past n - 1 takes the value of rank n - 1) of n non-negative floats
 // held as their uint32 bit patterns in LDS.  Non-negative IEEE floats order
-// like their bit patterns, so an MSB-first radix select with 8-bit digits
-// finds each rank in four histogram passes; the four ranks share the passes.
-__device__ void radix_select4(const uint32_t* keys, int n, int rank0, int rank1, int rank2, int rank3,
-                              uint32_t* hist /*4*256*/, uint32_t* prefix /*4*/, int* remaining /*4*/,
-                              uint32_t* out /*4*/) {
+// like their bit patterns, so an MSB-first radix select finds a rank digit by
+// digit.  The bits that every key shares (radii of one head mostly share their
+// exponent) are found first with an AND / OR reduction and skipped; the
+// remaining bits are taken in digits of up to 8, each wave counting its keys
+// in a histogram of its own (fewer colliding LDS atomics); ranks ka + 1 and
+// kb + 1 then follow from one count-and-minimum pass.
+__device__ void order_stats4(const uint32_t* keys, int n, int ka, int kb, uint32_t* hist /*4 waves x 2 x 256*/,
+                             uint32_t* red /*8*/, uint32_t* prefix /*2*/, int* remaining /*2*/,
+                             uint32_t* out /*4*/) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid < 4) {
-    prefix[tid] = 0u;
-    remaining[tid] = tid == 0 ? rank0 : tid == 1 ? rank1 : tid == 2 ? rank2 : rank3;
+  uint32_t a = 0xffffffffu, o = 0u;
+  for (int e = tid; e < n; e += kStatsThreads) {
+    a &= keys[e];
+    o |= keys[e];
   }
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    const uint32_t hi_mask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
-    for (int e = tid; e < 4 * 256; e += kStatsThreads) hist[e] = 0u;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    a &= (uint32_t)__shfl_xor((int)a, off, kWave);
+    o |= (uint32_t)__shfl_xor((int)o, off, kWave);
+  }
+  if (lane == 0) {
+    red[wave] = a;
+    red[4 + wave] = o;
+  }
+  __syncthreads();
+  a = red[0] & red[1] & red[2] & red[3];
+  o = red[4] | red[5] | red[6] | red[7];
+  const uint32_t diff = a ^ o;
+  int bits = diff == 0u ? 0 : 32 - __clz((int)diff);  // the low bits that differ between keys
+  if (tid < 2) {
+    prefix[tid] = bits >= 32 ? 0u : (a >> bits) << bits;  // the shared high bits
+    remaining[tid] = tid == 0 ? ka : kb;
+  }
+  while (bits > 0) {
+    const int width = bits >= 8 ? 8 : bits;
+    const int shift = bits - width;
+    const uint32_t hi_mask = bits >= 32 ? 0u : (0xffffffffu << bits);
+    const uint32_t digit_mask = (1u << width) - 1u;
+    for (int e = tid; e < 4 * 2 * 256; e += kStatsThreads) hist[e] = 0u;
     __syncthreads();
-    const uint32_t p0 = prefix[0], p1 = prefix[1], p2 = prefix[2], p3 = prefix[3];
+    const uint32_t p0 = prefix[0], p1 = prefix[1];
+    uint32_t* own = hist + wave * 2 * 256;
     for (int e = tid; e < n; e += kStatsThreads) {
       const uint32_t x = keys[e];
-      const uint32_t hx = x & hi_mask, digit = (x >> shift) & 255u;
-      if (hx == p0) atomicAdd(&hist[0 * 256 + digit], 1u);
-      if (hx == p1) atomicAdd(&hist[1 * 256 + digit], 1u);
-      if (hx == p2) atomicAdd(&hist[2 * 256 + digit], 1u);
-      if (hx == p3) atomicAdd(&hist[3 * 256 + digit], 1u);
+      const uint32_t hx = x & hi_mask, digit = (x >> shift) & digit_mask;
+      if (hx == p0) atomicAdd(&own[digit], 1u);
+      if (hx == p1) atomicAdd(&own[256 + digit], 1u);
     }
     __syncthreads();
-    if (wave < 4) {
-      const uint32_t* h = hist + wave * 256 + 4 * lane;
-      const int c0 = (int)h[0], c1 = (int)h[1], c2 = (int)h[2], c3 = (int)h[3];
-      const int own = c0 + c1 + c2 + c3;
-      int incl = own;
+    if (wave < 2) {
+      int c[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int bin = wave * 256 + 4 * lane + j;
+        c[j] = (int)(hist[bin] + hist[2 * 256 + bin] + hist[4 * 256 + bin] + hist[6 * 256 + bin]);
+      }
+      const int own_count = c[0] + c[1] + c[2] + c[3];
+      int incl = own_count;
       for (int off = 1; off < 64; off <<= 1) {
         const int v = __shfl_up(incl, off, kWave);
         if (lane >= off) incl += v;
       }
-      const int excl = incl - own;
+      const int excl = incl - own_count;
       const int k = remaining[wave];
       if (excl <= k && k < incl) {
         int kr = k - excl, digit = 4 * lane;
-        if (kr >= c0) { kr -= c0; ++digit;
-          if (kr >= c1) { kr -= c1; ++digit;
-            if (kr >= c2) { kr -= c2; ++digit; } } }
+        if (kr >= c[0]) { kr -= c[0]; ++digit;
+          if (kr >= c[1]) { kr -= c[1]; ++digit;
+            if (kr >= c[2]) { kr -= c[2]; ++digit; } } }
         prefix[wave] |= (uint32_t)digit << shift;
         remaining[wave] = kr;
       }
     }
-    __syncthreads();
+    __syncthreads();  // the histograms are read and the prefixes written before the next digit
+    bits -= width;
   }
-  if (tid < 4) out[tid] = prefix[tid];
+  __syncthreads();
+  // Rank k + 1: the same value when more than k + 1 keys are <= it, else the
+  // smallest key above it.
+  const uint32_t xa = prefix[0], xb = prefix[1];
+  uint32_t na = 0u, nb = 0u, ma = 0xffffffffu, mb = 0xffffffffu;
+  for (int e = tid; e < n; e += kStatsThreads) {
+    const uint32_t x = keys[e];
+    na += x <= xa ? 1u : 0u;
+    nb += x <= xb ? 1u : 0u;
+    if (x > xa) ma = x < ma ? x : ma;
+    if (x > xb) mb = x < mb ? x : mb;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    na += (uint32_t)__shfl_xor((int)na, off, kWave);
+    nb += (uint32_t)__shfl_xor((int)nb, off, kWave);
+    const uint32_t ya = (uint32_t)__shfl_xor((int)ma, off, kWave), yb = (uint32_t)__shfl_xor((int)mb, off, kWave);
+    ma = ya < ma ? ya : ma;
+    mb = yb < mb ? yb : mb;
+  }
+  __syncthreads();  // every wave is done reading red and prefix above
+  if (lane == 0) {
+    red[wave] = na + (nb << 16);  // n <= 4096: both counts fit in 16 bits
+    red[4 + wave] = 0u;
+    hist[wave] = ma;
+    hist[4 + wave] = mb;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t cnt = 0u, mina = 0xffffffffu, minb = 0xffffffffu;
+    for (int w = 0; w < 4; ++w) {
+      cnt += red[w];
+      mina = hist[w] < mina ? hist[w] : mina;
+      minb = hist[4 + w] < minb ? hist[4 + w] : minb;
+    }
+    const int ca = (int)(cnt & 0xffffu), cb = (int)(cnt >> 16);
+    out[0] = xa;
+    out[1] = (ka + 1 > n - 1 || ca >= ka + 2) ? xa : mina;
+    out[2] = xb;
+    out[3] = (kb + 1 > n - 1 || cb >= kb + 2) ? xb : minb;
+  }
   __syncthreads();
 }
 
@@ -257,9 +327,10 @@ __global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __
                                                                 float* __restrict__ quantiles,
                                                                 float* __restrict__ uplift, float sel_scale) {
   __shared__ uint32_t keys[kMaxBlocks];
-  __shared__ uint32_t hist[4 * 256];
-  __shared__ uint32_t sel_prefix[4];
-  __shared__ int sel_remaining[4];
+  __shared__ uint32_t hist[4 * 2 * 256];
+  __shared__ uint32_t sel_red[8];
+  __shared__ uint32_t sel_prefix[2];
+  __shared__ int sel_remaining[2];
   __shared__ uint32_t sel_out[4];
   const int g = blockIdx.x, sq = blockIdx.y, tid = threadIdx.x;
   const int M = t.blk[sq + 1] - t.blk[sq];
@@ -274,8 +345,7 @@ __global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __
   const int k50 = n1 / 2, k90 = (9 * n1) / 10;
   const float f50 = (n1 % 2) ? 0.5f : 0.0f;
   const float f90 = (float)((9 * n1) % 10) / 10.0f;
-  radix_select4(keys, M, k50, min(k50 + 1, n1), k90, min(k90 + 1, n1), hist, sel_prefix, sel_remaining,
-                sel_out);
+  order_stats4(keys, M, k50, k90, hist, sel_red, sel_prefix, sel_remaining, sel_out);
   const float x50 = __uint_as_float(sel_out[0]), x50b = __uint_as_float(sel_out[1]);
   const float x90 = __uint_as_float(sel_out[2]), x90b = __uint_as_float(sel_out[3]);
   const float r_low = x50 + f50 * (x50b - x50);
