@@ -839,6 +839,7 @@ KERNEL_SOURCES = {
     "attn_queue_kernel": ["attn.hip", "attend_block.hpp", "rbs_device.hpp", "rbs_launch.hpp", "../build.py"],
     "select_attend_queue_kernel": ["fused.hip", "select_block.hpp", "attend_block.hpp", "rbs_device.hpp",
                                    "rbs_launch.hpp", "../build.py"],
+    "attn_fp8_queue_kernel": ["fp8.hip", "attend_block.hpp", "rbs_device.hpp", "rbs_launch.hpp", "../build.py"],
 }
 
 
