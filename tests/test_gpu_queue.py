@@ -172,3 +172,32 @@ def test_queue_fused_equals_one_workgroup_per_item(B):
             assert np.array_equal(a[h, o:o + cnt[h, i]], b[h, o:o + cnt[h, i]]), (h, i)
     assert torch.equal(out[0][2], out[1][2]), "O"
     assert torch.equal(out[0][3], out[1][3]), "lse"
+
+
+def test_persistent_attention_replays_from_a_graph():
+    """The persistent launch captured in a graph (the queue reset is a kernel,
+    not a memset): every replay equals the eager result, with eager calls on
+    the same workspace between replays."""
+    import torch
+    import paper_2609_20971_amd as rbs
+    w = WORKLOADS["tiny-2k"].with_(name="queue-graph", seq_len=3000, n_q_heads=8, n_kv_heads=2, block_size=128,
+                                   seed=47)
+    _say("[queue] graph replays")
+    shape, Q, K, V, counts, indices = _setup(w)
+    ws = torch.empty(64, dtype=torch.int32, device="cuda")
+    ref = _attend(shape, Q, K, V, counts, indices, ws)
+    torch.cuda.synchronize()
+    O = torch.empty_like(Q)
+    lse = torch.empty((w.n_q_heads, w.seq_len), dtype=torch.float32, device="cuda")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        rbs.rbs_sparse_prefill(shape, Q, K, V, counts, indices, 0.0, O, lse=lse, workspace=ws)
+    for rep in range(3):
+        O.zero_()
+        lse.fill_(7.0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(O, ref[0]), f"replay {rep}: O differs"
+        assert torch.equal(lse, ref[1]), f"replay {rep}: lse differs"
+        eager = _attend(shape, Q, K, V, counts, indices, ws)  # the same workspace, between replays
+        _assert_same(eager, ref, f"eager call after replay {rep}")
