@@ -169,6 +169,9 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
  * in the two calls; counts/indices are still written (same layout and values
  * as rbs_select), and O/lse equal those of rbs_sparse_prefill on those lists.
  * Saves the second read of Q and the round trip of the lists through memory.
+ * The persistent launch (workspace non-NULL) is taken at B = 128 only; at
+ * B = 64 and 256 the call runs one workgroup per item and leaves the
+ * workspace unused.
  * Validation and errors: the union of the two calls' rules.
  */
 int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, const void* V,
