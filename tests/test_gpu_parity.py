@@ -38,6 +38,35 @@ def _run(w: Workload, inputs=None, tau=None, forced=None):
                 O=O, lse=lse, tau=(tb, tr), forced=(sink, local, recent))
 
 
+def _oracle_check(w: Workload, inp, counts, indices, O, tau, forced, rows=None, attn_rows=None, label=None):
+    """Lists and O of one HIP call against the oracle: masks bit for bit outside
+    the near-threshold band, the lists' structure, and O on the GPU's own lists
+    within the attention tolerance.  Returns (near-threshold flips, density)."""
+    Kf = f64_from_bf16_bits(inp["k"])
+    C, R = oracle.block_stats(Kf, w.block_size)
+    beta, _ = oracle.rescue_coefficients(R)
+    M = w.n_blocks
+    rows = rows or [(h, i) for h in range(w.n_q_heads) for i in range(M)]
+    Qf = f64_from_bf16_bits(inp["q"])
+    tb, tr = tau
+    sink, local, recent = forced
+    ref = oracle.select(Qf, C, R, beta, w.block_size, tb, tr, sink, local, recent, rows=rows)
+    lists = H.gpu_rows(counts, indices, rows)
+    H.check_lists(lists, M, sink, local, recent)
+    n_rows, compared, near = H.compare_masks(lists, ref)
+    dens_gpu = sum(len(v) for v in lists.values()) / compared
+    dens_ref = oracle.density([ref[k]["final"] for k in rows])
+    arows = attn_rows or rows
+    alists = H.gpu_rows(counts, indices, arows)
+    Og = H.bf16_tensor_to_f64(O)
+    Vf = f64_from_bf16_bits(inp["v"])
+    err = H.max_abs_attention_error(Og, Qf, Kf, Vf, w.group, w.block_size, alists, w.seq_len)
+    _say(f"[parity] {label or w.name}: rows {n_rows} blocks {compared} near-threshold flips {near}; "
+         f"density gpu {dens_gpu:.4f} oracle {dens_ref:.4f}; attention max-abs {err:.3e} ({len(arows)} rows)")
+    assert err <= H.ATTN_ATOL
+    return near, dens_gpu
+
+
 def _full_check(w: Workload, tau=None, forced=None, attn_rows=None, select_rows=None, inputs=None):
     _say(f"[parity] workload={w.name} N={w.seq_len} Hq={w.n_q_heads} Hkv={w.n_kv_heads} B={w.block_size} "
          f"tau={tau} forced={forced}")
@@ -47,25 +76,9 @@ def _full_check(w: Workload, tau=None, forced=None, attn_rows=None, select_rows=
     C, R = oracle.block_stats(Kf, w.block_size)
     beta, rq = oracle.rescue_coefficients(R)
     rep = H.check_stats(r["stats"], C, R, beta, rq)
-    M = w.n_blocks
-    rows = select_rows or [(h, i) for h in range(w.n_q_heads) for i in range(M)]
-    Qf = f64_from_bf16_bits(inp["q"])
-    tb, tr = r["tau"]
-    sink, local, recent = r["forced"]
-    ref = oracle.select(Qf, C, R, beta, w.block_size, tb, tr, sink, local, recent, rows=rows)
-    lists = H.gpu_rows(r["counts"], r["indices"], rows)
-    H.check_lists(lists, M, sink, local, recent)
-    n_rows, compared, near = H.compare_masks(lists, ref)
-    dens_gpu = sum(len(v) for v in lists.values()) / compared
-    dens_ref = oracle.density([ref[k]["final"] for k in rows])
-    arows = attn_rows or rows
-    alists = H.gpu_rows(r["counts"], r["indices"], arows)
-    Og = H.bf16_tensor_to_f64(r["O"])
-    Vf = f64_from_bf16_bits(inp["v"])
-    err = H.max_abs_attention_error(Og, Qf, Kf, Vf, w.group, w.block_size, alists, w.seq_len)
-    _say(f"[parity] {w.name}: stats {rep}; rows {n_rows} blocks {compared} near-threshold flips {near}; "
-         f"density gpu {dens_gpu:.4f} oracle {dens_ref:.4f}; attention max-abs {err:.3e}")
-    assert err <= H.ATTN_ATOL
+    _say(f"[parity] {w.name}: stats {rep}")
+    near, _ = _oracle_check(w, inp, r["counts"], r["indices"], r["O"], r["tau"], r["forced"], rows=select_rows,
+                            attn_rows=attn_rows)
     return r, near
 
 
@@ -257,9 +270,10 @@ def test_layer_schedule_layers_sampled(layer):
     _full_check(w, select_rows=rows, attn_rows=rows[:6])
 
 
-def _fused_matches_two_calls(w: Workload, tau=None, forced=None):
-    """The fused entry point against rbs_select + rbs_sparse_prefill on the same
-    inputs: lists, O and LSE bit for bit."""
+def _fused_matches_two_calls(w: Workload, tau=None, forced=None, rows=None, attn_rows=None):
+    """The fused entry point against the oracle (its own lists and O, as the
+    two-call path is checked) and against rbs_select + rbs_sparse_prefill on
+    the same inputs: lists, O and LSE bit for bit."""
     import torch
     import paper_2609_20971_amd as rbs
     r = _run(w, tau=tau, forced=forced)
@@ -269,10 +283,12 @@ def _fused_matches_two_calls(w: Workload, tau=None, forced=None):
     counts, indices, O = rbs.rbs_select_attend(r["shape"], r["Qd"], r["Kd"], r["Vd"], r["stats"], tb, tr, sink,
                                                local, recent, 0.0, lse=lse)
     torch.cuda.synchronize()
+    _oracle_check(w, r["inputs"], counts, indices, O, r["tau"], r["forced"], rows=rows, attn_rows=attn_rows,
+                  label=f"fused {w.name} N={w.seq_len} B={w.block_size}")
     M = w.n_blocks
     assert torch.equal(counts, r["counts"])
-    rows = [(h, i) for h in range(w.n_q_heads) for i in range(M)]
-    assert H.gpu_rows(counts, indices, rows) == H.gpu_rows(r["counts"], r["indices"], rows)
+    all_rows = [(h, i) for h in range(w.n_q_heads) for i in range(M)]
+    assert H.gpu_rows(counts, indices, all_rows) == H.gpu_rows(r["counts"], r["indices"], all_rows)
     assert torch.equal(O.view(torch.int16), r["O"].view(torch.int16))
     assert torch.equal(lse, r["lse"])
     _say(f"[parity] fused {w.name} N={w.seq_len} B={w.block_size}: lists, O and LSE identical to the two calls")
@@ -289,7 +305,11 @@ def _fused_matches_two_calls(w: Workload, tau=None, forced=None):
 ])
 def test_fused_select_attend_matches_two_calls(variant):
     w = WORKLOADS["tiny-2k"].with_(name="fused", **variant)
-    _fused_matches_two_calls(w)
+    M = w.n_blocks
+    attn = None
+    if M > 32:  # attention against the oracle on a sample of rows, the ragged last row included
+        attn = H.sample_rows(w.n_q_heads, M, 16, seed=w.seed, include=[(0, M - 1), (w.n_q_heads - 1, M - 2)])
+    _fused_matches_two_calls(w, attn_rows=attn)
 
 
 def test_fused_select_attend_forced_and_dense_rows():
@@ -300,8 +320,11 @@ def test_fused_select_attend_forced_and_dense_rows():
 
 @pytest.mark.slow
 def test_fused_select_attend_128k_matches_two_calls():
-    """The headline layer through the fused entry point: identical to the two calls."""
-    _fused_matches_two_calls(WORKLOADS["qwen3-30b-a3b-128k"])
+    """The headline layer through the fused entry point: sampled rows against
+    the oracle, and identical to the two calls."""
+    w = WORKLOADS["qwen3-30b-a3b-128k"]
+    rows = H.sample_rows(w.n_q_heads, w.n_blocks, 24, seed=12, include=[(5, 1023), (31, 700), (0, 3)])
+    _fused_matches_two_calls(w, rows=rows, attn_rows=rows[:10])
 
 
 # ------------------------------------------------ supporting selectors (Table selector_ablation)

@@ -473,6 +473,35 @@ def test_variant_rows_keep_forced_blocks_and_threshold_extremes():
     assert len(box_all) == M
 
 
+def test_variant_aggregation_sums_scaled_exponentials_over_tokens():
+    """Sec. 3.2 Eq. block_aggregation applied to the supporting selectors of
+    Table selector_ablation (centroid, Eq. full_l2_bound, Eq. quest_box): each
+    block score sums exp(logit / sqrt d) over the query block's tokens.  Two
+    different queries make the sum, the max over tokens and the mean logit
+    disagree, and d = 4 makes the 1/sqrt(d) scale matter (tests/golden)."""
+    case = _load("variant_aggregation_case.json")
+    ex = case["expected"]
+    B = case["block_size"]
+    K = np.array(case["keys"], dtype=np.float64)[None]
+    Q = np.array(case["queries"], dtype=np.float64)[None]
+    C, R = oracle.block_stats(K, B)
+    Vc, Hw = oracle.block_box(K, B)
+    np.testing.assert_allclose(C[0], ex["centroids"], atol=1e-15)
+    np.testing.assert_allclose(R[0], ex["radii"], atol=1e-15)
+    np.testing.assert_allclose(Vc[0], ex["box_center"], atol=1e-15)
+    np.testing.assert_allclose(Hw[0], ex["box_half"], atol=1e-15)
+    Qi = Q[0, B:2 * B]
+    for variant, ratio in ex["row1_ratio"].items():
+        log_s = oracle.variant_log_scores(Qi, C[0], R[0], Vc[0], Hw[0], 2, variant)
+        assert log_s[0] - log_s[1] == pytest.approx(math.log(ratio), abs=1e-12), variant
+    M = K.shape[1] // B
+    for key, final in ex["row1_final"].items():
+        variant, param = key.rsplit("_", 1)
+        row = oracle.select_variant_row(Qi, C[0], R[0], Vc[0], Hw[0], 1, M, variant, float(param),
+                                        case["n_sink"], case["n_local"], case["n_recent"])
+        assert _ids(row["final"]) == final, key
+
+
 # ---------------------------------------------------------------- batches
 # App. "Additional A100 System Measurements", prompt throughput: batched
 # prompts are independent causal sequences, none concatenated into another.
