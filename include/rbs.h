@@ -23,8 +23,15 @@
  *                       concatenated sequence)
  *
  * Conventions shared by every call
- *   - Tensors are dense, row-major, in device memory:
- *       Q, O   bf16 [H_q][N][d]      K, V   bf16 [H_kv][N][d]
+ *   - Tensors live in device memory.  Q, K, V and O are indexed by (head,
+ *     token, dimension) with the dimension contiguous and the head and token
+ *     strides given in rbs_shape (in elements):
+ *       Q, O   bf16, element (h, t, j) at h q_stride_head + t q_stride_tok + j
+ *       K, V   bf16, element (g, t, j) at g kv_stride_head + t kv_stride_tok + j
+ *     Zero strides mean the dense head-major layout [H][N][d]; a serving
+ *     stack's token-major [N][H][d] buffers have stride_head = d and
+ *     stride_tok = H d.  O is written with Q's strides.  The remaining
+ *     arrays (statistics, lists, lse) are dense as documented at each call.
  *     d (head_dim) must be 128.  Query head h reads KV head h / (H_q / H_kv).
  *   - Blocks: M = ceil(N / B) blocks of B tokens (the last may be short);
  *     query and key blocks use the same B, one of 64, 128, 256.
@@ -53,7 +60,7 @@ extern "C" {
 enum {
   RBS_OK = 0,
   RBS_ERR_NULL = 1,        /* a required pointer is NULL                      */
-  RBS_ERR_SHAPE = 2,       /* N < 1, H < 1, H_q % H_kv != 0, limits exceeded  */
+  RBS_ERR_SHAPE = 2,       /* N < 1, H < 1, H_q % H_kv != 0, limits, strides */
   RBS_ERR_UNSUPPORTED = 3, /* head_dim != 128 or block size not 64/128/256    */
   RBS_ERR_ARG = 4,         /* tau outside [0,1], negative or zero window, ... */
   RBS_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned         */
@@ -66,6 +73,17 @@ typedef struct {
   int32_t n_kv_heads; /* H_kv, divides H_q          */
   int32_t head_dim;   /* d, must be 128             */
   int32_t block_size; /* B: 64, 128 or 256          */
+  /* Element strides of Q (and O) and of K and V between consecutive heads
+   * and consecutive tokens; 0 selects the dense [H][N][d] value (N d for a
+   * head, d for a token).  Each must be a multiple of 8 (16-byte rows); the
+   * rows of distinct (head, token) pairs must not overlap, which the call
+   * checks as: stride_tok >= d and stride_head >= N stride_tok (head-major),
+   * or stride_head >= d and stride_tok >= H stride_head (token-major); and
+   * the token strides are at most 2^23.  Otherwise RBS_ERR_SHAPE. */
+  int64_t q_stride_head;
+  int64_t q_stride_tok;
+  int64_t kv_stride_head;
+  int64_t kv_stride_tok;
 } rbs_shape;
 
 /*
@@ -82,8 +100,10 @@ typedef struct {
  *   summary    rbs_summary_bytes() bytes: the select-ready copy of the summaries
  *              (centroids as f16 pre-scaled by log2(e)/sqrt(d), the per-block
  *              rescue uplift r_b beta_b log2(e)/sqrt(d), and the norms of the
- *              scaled centroids).  Opaque; written by rbs_block_stats, read by
- *              rbs_select and rbs_select_attend.
+ *              scaled centroids).  Opaque; written by rbs_block_stats (or by
+ *              rbs_stats_summarize from centroids, radii and beta that the
+ *              caller computed elsewhere), read by rbs_select,
+ *              rbs_select_attend and rbs_select_variant.
  */
 typedef struct {
   float* centroids;
@@ -121,10 +141,21 @@ size_t rbs_attention_workspace_bytes(void);
 
 /*
  * Stage 1 (Sec. 3.1; Algorithm 1, statistics loops).
- * K: bf16 [H_kv][N][d].  Fills every field of *stats: one pass over K for the
+ * K: bf16, strides as in rbs_shape.  Fills every field of *stats: one pass over K for the
  * centroids and radii, then one workgroup per KV head for the quantiles and beta.
  */
 int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stats, void* stream);
+
+/*
+ * The select-ready summary from statistics the caller already holds (Sec. 3.1:
+ * centroids, radii and beta, e.g. persisted with a prefix cache as the paper's
+ * metadata accounting assumes, or computed by another implementation):
+ * reads stats->centroids, radii and beta (device memory, layouts as above) and
+ * writes stats->summary.  rbs_block_stats writes the same summary itself.  The
+ * quantiles are neither read nor written.  Errors: RBS_ERR_NULL for a missing
+ * pointer, RBS_ERR_ALIGN, shape errors as rbs_block_stats.
+ */
+int rbs_stats_summarize(const rbs_shape* shape, const rbs_stats* stats, void* stream);
 
 /*
  * Stage 2 (Sec. 3.2; Algorithm 1, selection loop).
@@ -135,7 +166,8 @@ int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stat
  *   final = M^base U M^rescue U forced, where forced holds the first n_sink
  *           blocks, the n_local blocks ending at the diagonal, and every
  *           candidate when i >= M - n_recent.
- * Q: bf16 [H_q][N][d]; stats: filled by rbs_block_stats on the same K and shape.
+ * Q: bf16, strides as in rbs_shape; stats: its summary filled by
+ * rbs_block_stats on the same K and shape, or by rbs_stats_summarize.
  * tau_base, tau_rescue in [0, 1]; n_sink >= 0, n_local >= 1, n_recent >= 0.
  * Outputs: counts int32 [H_q][M]; indices int32 [H_q][rbs_index_capacity(M)],
  * row (h, i) ascending, unique, all <= i, always containing i.  Slots past
@@ -242,7 +274,8 @@ int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices,
  * fp32 first; dequantisation multiplies by amax_h / 448 (fp32).  An all-zero
  * head uses scale 1.
  *   amax   fp32 [H_q + 2 H_kv]: Q heads, K heads, V heads
- *   Q8     E4M3 [H_q][N][d]      K8  E4M3 [H_kv][N][d]  (row-major copies)
+ *   Q8     E4M3 [H_q][N][d]      K8  E4M3 [H_kv][N][d]  (dense row-major
+ *          copies, whatever the strides of the bf16 inputs)
  *   V8t    rbs_fp8_vt_bytes() bytes: per KV head and key block, the d x B
  *          tile of V transposed, keys in the order the attention kernel
  *          consumes them (B = 256: as two d x 128 halves; opaque to the
@@ -269,7 +302,8 @@ int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K
  * causal attention.  All sequences of a batch share one launch per stage.
  *
  * Layout: the sequences are packed along the token axis,
- *   Q, O  bf16 [H_q][T][d]    K, V  bf16 [H_kv][T][d]    lse  fp32 [H_q][T]
+ *   Q, O  bf16 (H_q heads, T tokens)    K, V  bf16 (H_kv heads, T tokens)
+ *   with the strides of rbs_shape (zero: dense [H][T][d]);  lse  fp32 [H_q][T]
  * with T = shape->n_tokens = sum of seq_tokens; sequence s holds tokens
  * t_s .. t_s + n_s - 1, t_s = n_0 + ... + n_(s-1).  Blocks restart at every
  * sequence: sequence s has M_s = ceil(n_s / B) blocks, and the block arrays

@@ -1,6 +1,7 @@
 """RBS-Attention sparse prefill on MI355X (gfx950): HIP kernels behind a C ABI.
 
     stats = rbs_block_stats(shape, K)                                  # Sec. 3.1
+    rbs_stats_summarize(shape, stats)   # select-ready summary from centroids/radii/beta held elsewhere
     counts, indices = rbs_select(shape, Q, stats, tau_b, tau_r, sink, local, recent)  # Sec. 3.2
     O = rbs_sparse_prefill(shape, Q, K, V, counts, indices)            # Sec. 3.3
     counts, indices, O = rbs_select_attend(shape, Q, K, V, stats, ...)   # Sec. 3.2-3.3 in one pass
@@ -45,6 +46,7 @@ from ._lib import (  # noqa: F401
     make_shape,
     n_blocks,
     rbs_block_stats,
+    rbs_stats_summarize,
     rbs_dense_indices,
     rbs_index_capacity,
     rbs_select,

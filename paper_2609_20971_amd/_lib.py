@@ -34,6 +34,10 @@ class rbs_shape(ctypes.Structure):
         ("n_kv_heads", ctypes.c_int32),
         ("head_dim", ctypes.c_int32),
         ("block_size", ctypes.c_int32),
+        ("q_stride_head", ctypes.c_int64),
+        ("q_stride_tok", ctypes.c_int64),
+        ("kv_stride_head", ctypes.c_int64),
+        ("kv_stride_tok", ctypes.c_int64),
     ]
 
 
@@ -85,6 +89,8 @@ def load() -> ctypes.CDLL:
     lib.rbs_index_capacity.restype = I64
     lib.rbs_block_stats.argtypes = [SP, P, ctypes.POINTER(rbs_stats), P]
     lib.rbs_block_stats.restype = ctypes.c_int
+    lib.rbs_stats_summarize.argtypes = [SP, ctypes.POINTER(rbs_stats), P]
+    lib.rbs_stats_summarize.restype = ctypes.c_int
     lib.rbs_select.argtypes = [SP, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, P, P, P]
     lib.rbs_select.restype = ctypes.c_int
     lib.rbs_attention_workspace_bytes.argtypes = []
@@ -192,7 +198,128 @@ def _workspace(workspace, device, stream):
 
 
 def make_shape(n_tokens: int, n_q_heads: int, n_kv_heads: int, block_size: int, head_dim: int = 128) -> rbs_shape:
-    return rbs_shape(n_tokens, n_q_heads, n_kv_heads, head_dim, block_size)
+    """Shape with zero (dense) strides; the calls fill the strides in from the
+    tensors they are given."""
+    return rbs_shape(n_tokens, n_q_heads, n_kv_heads, head_dim, block_size, 0, 0, 0, 0)
+
+
+# ------------------------------------------------------------------ argument checks
+# Every call checks its tensors here, before anything reaches the library:
+# dtype, sizes and layout of each tensor first, then that all of them sit on
+# one GPU.  Q/K/V/O strides go into the rbs_shape passed on.  A mismatch
+# raises ValueError; nothing is launched.
+
+def _device_index(t) -> int:
+    if t.device.type != "cuda":
+        return -1
+    return t.device.index if t.device.index is not None else torch.cuda.current_device()
+
+
+def _check_tensor(name: str, t, dtype, sizes, contiguous=True):
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor, not {type(t).__name__}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, not {t.dtype}")
+    if tuple(t.shape) != tuple(sizes):
+        raise ValueError(f"{name} must have shape {tuple(sizes)}, not {tuple(t.shape)}")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() > 0 and t.stride(-1) != 1:
+        raise ValueError(f"{name} must have a contiguous last dimension")
+
+
+def _on_gpu(*named) -> int:
+    """All (name, tensor) pairs (None tensors skipped) on one GPU; its index."""
+    dev = None
+    for name, t in named:
+        if t is None:
+            continue
+        if t.device.type != "cuda":
+            raise ValueError(f"{name} must be on a GPU, not {t.device}")
+        if dev is None:
+            dev = _device_index(t)
+        elif _device_index(t) != dev:
+            raise ValueError(f"{name} is on cuda:{_device_index(t)}, the other arguments on cuda:{dev}")
+    return dev
+
+
+def _heads_tokens(name: str, t, n_heads: int, n_tokens: int, head_dim: int):
+    """A bf16 (head, token, dimension) tensor of any strides with a contiguous
+    last dimension; returns its (head stride, token stride)."""
+    _check_tensor(name, t, torch.bfloat16, (n_heads, n_tokens, head_dim), contiguous=False)
+    return t.stride(0), t.stride(1)
+
+
+def _with_strides(shape: rbs_shape, q=None, kv=None) -> rbs_shape:
+    """A copy of shape with the Q and/or K, V strides of the given tensors.
+    Strides already set in shape must agree with the tensors'."""
+    out = rbs_shape.from_buffer_copy(shape)
+    for pair, fields in ((q, ("q_stride_head", "q_stride_tok")), (kv, ("kv_stride_head", "kv_stride_tok"))):
+        if pair is None:
+            continue
+        for value, field in zip(pair, fields):
+            given = getattr(shape, field)
+            if given not in (0, value):
+                raise ValueError(f"shape.{field} = {given} disagrees with the tensor's stride {value}")
+            setattr(out, field, value)
+    return out
+
+
+def _check_q(shape: rbs_shape, Q):
+    return _heads_tokens("Q", Q, shape.n_q_heads, shape.n_tokens, shape.head_dim)
+
+
+def _check_kv(shape: rbs_shape, K, V=None):
+    kv = _heads_tokens("K", K, shape.n_kv_heads, shape.n_tokens, shape.head_dim)
+    if V is not None:
+        v = _heads_tokens("V", V, shape.n_kv_heads, shape.n_tokens, shape.head_dim)
+        if v != kv:
+            raise ValueError(f"V strides {v} differ from K strides {kv}; the library takes one pair")
+    return kv
+
+
+def _check_out(O, Q):
+    """O: bf16 with Q's sizes and strides (the library writes O with Q's strides)."""
+    _check_tensor("O", O, torch.bfloat16, tuple(Q.shape), contiguous=False)
+    if O.stride() != Q.stride():
+        raise ValueError(f"O strides {O.stride()} must equal Q strides {Q.stride()}")
+
+
+def _check_lse(shape: rbs_shape, lse):
+    if lse is not None:
+        _check_tensor("lse", lse, torch.float32, (shape.n_q_heads, shape.n_tokens))
+
+
+def _check_lists(shape: rbs_shape, counts, indices, n_blocks_total=None, capacity=None):
+    m = n_blocks(shape) if n_blocks_total is None else n_blocks_total
+    cap = rbs_index_capacity(m) if capacity is None else capacity
+    _check_tensor("counts", counts, torch.int32, (shape.n_q_heads, m))
+    _check_tensor("indices", indices, torch.int32, (shape.n_q_heads, cap))
+
+
+def _check_stats(shape: rbs_shape, stats, n_blocks_total=None, n_seqs=1, summary_bytes=None, need_fp32=True):
+    """The BlockStats tensors a call reads or writes; returns them named, for _on_gpu."""
+    if not isinstance(stats, BlockStats):
+        raise ValueError("stats must be a BlockStats")
+    m = n_blocks(shape) if n_blocks_total is None else n_blocks_total
+    hk, d = shape.n_kv_heads, shape.head_dim
+    named = []
+    if need_fp32:
+        _check_tensor("stats.centroids", stats.centroids, torch.float32, (hk, m, d))
+        _check_tensor("stats.radii", stats.radii, torch.float32, (hk, m))
+        _check_tensor("stats.beta", stats.beta, torch.float32, (hk, m))
+        qshape = (hk, 2) if n_blocks_total is None else (n_seqs, hk, 2)
+        _check_tensor("stats.quantiles", stats.quantiles, torch.float32, qshape)
+        named += [("stats.centroids", stats.centroids), ("stats.radii", stats.radii), ("stats.beta", stats.beta),
+                  ("stats.quantiles", stats.quantiles)]
+    nbytes = rbs_summary_bytes(shape) if summary_bytes is None else summary_bytes
+    _check_tensor("stats.summary", stats.summary, torch.uint8, (nbytes,))
+    return named + [("stats.summary", stats.summary)]
+
+
+def _like_q(Q):
+    """An output with Q's sizes and strides (the layout the library writes O in)."""
+    return torch.empty_strided(tuple(Q.shape), Q.stride(), dtype=torch.bfloat16, device=Q.device)
 
 
 def n_blocks(shape: rbs_shape) -> int:
@@ -235,10 +362,22 @@ class BlockStats:
 
 def rbs_block_stats(shape: rbs_shape, K: torch.Tensor, stats: BlockStats | None = None, stream=None) -> BlockStats:
     """Stage 1: centroids, radii, radius quantiles and beta of every key block."""
+    kvs = _check_kv(shape, K)
     if stats is None:
         stats = BlockStats.allocate(shape, K.device)
+    _on_gpu(("K", K), *_check_stats(shape, stats))
+    sh = _with_strides(shape, kv=kvs)
     c = stats.as_c()
-    _check("rbs_block_stats", load().rbs_block_stats(ctypes.byref(shape), _ptr(K), ctypes.byref(c), _stream(stream)))
+    _check("rbs_block_stats", load().rbs_block_stats(ctypes.byref(sh), _ptr(K), ctypes.byref(c), _stream(stream)))
+    return stats
+
+
+def rbs_stats_summarize(shape: rbs_shape, stats: BlockStats, stream=None) -> BlockStats:
+    """The select-ready summary from stats.centroids, radii and beta (statistics
+    computed elsewhere); rbs_block_stats writes the same summary itself."""
+    _on_gpu(*_check_stats(shape, stats))
+    c = stats.as_c()
+    _check("rbs_stats_summarize", load().rbs_stats_summarize(ctypes.byref(shape), ctypes.byref(c), _stream(stream)))
     return stats
 
 
@@ -264,12 +403,26 @@ class BoxStats:
         return rbs_box(_ptr(self.center), _ptr(self.half), _ptr(self.summary))
 
 
+def _check_box(shape: rbs_shape, box):
+    if not isinstance(box, BoxStats):
+        raise ValueError("box must be a BoxStats")
+    m, hk, d = n_blocks(shape), shape.n_kv_heads, shape.head_dim
+    _check_tensor("box.center", box.center, torch.float32, (hk, m, d))
+    _check_tensor("box.half", box.half, torch.float32, (hk, m, d))
+    nbytes = int(load().rbs_box_summary_bytes(ctypes.byref(shape)))
+    _check_tensor("box.summary", box.summary, torch.uint8, (nbytes,))
+    return [("box.center", box.center), ("box.half", box.half), ("box.summary", box.summary)]
+
+
 def rbs_block_box(shape: rbs_shape, K: torch.Tensor, box: BoxStats | None = None, stream=None) -> BoxStats:
     """Coordinate-wise key box of every block (centre, half-width)."""
+    kvs = _check_kv(shape, K)
     if box is None:
         box = BoxStats.allocate(shape, K.device)
+    _on_gpu(("K", K), *_check_box(shape, box))
+    sh = _with_strides(shape, kv=kvs)
     c = box.as_c()
-    _check("rbs_block_box", load().rbs_block_box(ctypes.byref(shape), _ptr(K), ctypes.byref(c), _stream(stream)))
+    _check("rbs_block_box", load().rbs_block_box(ctypes.byref(sh), _ptr(K), ctypes.byref(c), _stream(stream)))
     return box
 
 
@@ -278,12 +431,19 @@ def rbs_select_variant(shape: rbs_shape, Q: torch.Tensor, stats: BlockStats, sel
                        indices=None, stream=None):
     """A supporting selector ("centroid", "full_l2", "box" or its RBS_SELECTOR_* code)."""
     sel = SELECTORS[selector] if isinstance(selector, str) else int(selector)
+    qs = _check_q(shape, Q)
+    named = _check_stats(shape, stats)
+    if box is not None:
+        named += _check_box(shape, box)
     if counts is None or indices is None:
         counts, indices = allocate_lists(shape, Q.device)
+    _check_lists(shape, counts, indices)
+    _on_gpu(("Q", Q), *named, ("counts", counts), ("indices", indices))
+    sh = _with_strides(shape, q=qs)
     c = stats.as_c()
     b = box.as_c() if box is not None else None
     _check("rbs_select_variant", load().rbs_select_variant(
-        ctypes.byref(shape), _ptr(Q), ctypes.byref(c), ctypes.byref(b) if b is not None else None, sel,
+        ctypes.byref(sh), _ptr(Q), ctypes.byref(c), ctypes.byref(b) if b is not None else None, sel,
         float(param), int(n_sink), int(n_local), int(n_recent), _ptr(counts), _ptr(indices), _stream(stream)))
     return counts, indices
 
@@ -298,10 +458,15 @@ def allocate_lists(shape: rbs_shape, device="cuda"):
 def rbs_select(shape: rbs_shape, Q: torch.Tensor, stats: BlockStats, tau_base: float, tau_rescue: float,
                n_sink: int, n_local: int, n_recent: int, counts=None, indices=None, stream=None):
     """Stage 2: per (query head, query block) ascending key-block index lists."""
+    qs = _check_q(shape, Q)
+    named = _check_stats(shape, stats, need_fp32=False)
     if counts is None or indices is None:
         counts, indices = allocate_lists(shape, Q.device)
+    _check_lists(shape, counts, indices)
+    _on_gpu(("Q", Q), *named, ("counts", counts), ("indices", indices))
+    sh = _with_strides(shape, q=qs)
     c = stats.as_c()
-    _check("rbs_select", load().rbs_select(ctypes.byref(shape), _ptr(Q), ctypes.byref(c), float(tau_base),
+    _check("rbs_select", load().rbs_select(ctypes.byref(sh), _ptr(Q), ctypes.byref(c), float(tau_base),
                                            float(tau_rescue), int(n_sink), int(n_local), int(n_recent),
                                            _ptr(counts), _ptr(indices), _stream(stream)))
     return counts, indices
@@ -309,11 +474,19 @@ def rbs_select(shape: rbs_shape, Q: torch.Tensor, stats: BlockStats, tau_base: f
 
 def rbs_sparse_prefill(shape: rbs_shape, Q, K, V, counts, indices, softmax_scale: float = 0.0, O=None,
                        lse=None, stream=None, workspace=AUTO):
-    """Stage 3: causal GQA block-sparse attention; returns O (bf16 [H_q][N][d])."""
+    """Stage 3: causal GQA block-sparse attention; returns O (bf16, Q's sizes and strides)."""
+    qs = _check_q(shape, Q)
+    kvs = _check_kv(shape, K, V)
+    _check_lists(shape, counts, indices)
+    if O is not None:
+        _check_out(O, Q)
+    _check_lse(shape, lse)
+    _on_gpu(("Q", Q), ("K", K), ("V", V), ("counts", counts), ("indices", indices), ("O", O), ("lse", lse))
     if O is None:
-        O = torch.empty_like(Q)
+        O = _like_q(Q)
     ws = _workspace(workspace, Q.device, stream)
-    _check("rbs_sparse_prefill", load().rbs_sparse_prefill(ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V),
+    sh = _with_strides(shape, q=qs, kv=kvs)
+    _check("rbs_sparse_prefill", load().rbs_sparse_prefill(ctypes.byref(sh), _ptr(Q), _ptr(K), _ptr(V),
                                                            _ptr(counts), _ptr(indices), float(softmax_scale),
                                                            _ptr(O), _ptr(lse), _ptr(ws), _stream(stream)))
     return O
@@ -323,14 +496,24 @@ def rbs_select_attend(shape: rbs_shape, Q, K, V, stats: BlockStats, tau_base: fl
                       n_sink: int, n_local: int, n_recent: int, softmax_scale: float = 0.0, counts=None,
                       indices=None, O=None, lse=None, stream=None, workspace=AUTO):
     """Stages 2 and 3 in one pass; returns (counts, indices, O) as the two calls would."""
+    qs = _check_q(shape, Q)
+    kvs = _check_kv(shape, K, V)
+    named = _check_stats(shape, stats, need_fp32=False)
     if counts is None or indices is None:
         counts, indices = allocate_lists(shape, Q.device)
+    _check_lists(shape, counts, indices)
+    if O is not None:
+        _check_out(O, Q)
+    _check_lse(shape, lse)
+    _on_gpu(("Q", Q), ("K", K), ("V", V), *named, ("counts", counts), ("indices", indices), ("O", O),
+            ("lse", lse))
     if O is None:
-        O = torch.empty_like(Q)
+        O = _like_q(Q)
     c = stats.as_c()
     ws = _workspace(workspace, Q.device, stream)
+    sh = _with_strides(shape, q=qs, kv=kvs)
     _check("rbs_select_attend", load().rbs_select_attend(
-        ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V), ctypes.byref(c), float(tau_base), float(tau_rescue),
+        ctypes.byref(sh), _ptr(Q), _ptr(K), _ptr(V), ctypes.byref(c), float(tau_base), float(tau_rescue),
         int(n_sink), int(n_local), int(n_recent), float(softmax_scale), _ptr(counts), _ptr(indices), _ptr(O),
         _ptr(lse), _ptr(ws), _stream(stream)))
     return counts, indices, O
@@ -340,6 +523,8 @@ def rbs_dense_indices(shape: rbs_shape, counts=None, indices=None, stream=None, 
     """Full causal lists: the dense path through the same attention kernel."""
     if counts is None or indices is None:
         counts, indices = allocate_lists(shape, device)
+    _check_lists(shape, counts, indices)
+    _on_gpu(("counts", counts), ("indices", indices))
     _check("rbs_dense_indices", load().rbs_dense_indices(ctypes.byref(shape), _ptr(counts), _ptr(indices),
                                                          _stream(stream)))
     return counts, indices
@@ -415,11 +600,15 @@ def allocate_lists_varlen(shape: rbs_shape, batch: Batch, device="cuda"):
 def rbs_block_stats_varlen(shape: rbs_shape, batch: Batch, K: torch.Tensor, stats: BlockStats | None = None,
                            stream=None) -> BlockStats:
     """Stage 1 for every sequence of a batch (one launch)."""
+    kvs = _check_kv(shape, K)
     if stats is None:
         stats = allocate_stats_varlen(shape, batch, K.device)
+    _on_gpu(("K", K), *_check_stats(shape, stats, n_blocks_total=rbs_varlen_blocks(shape, batch),
+                                    n_seqs=batch.n_seqs, summary_bytes=rbs_varlen_summary_bytes(shape, batch)))
+    sh = _with_strides(shape, kv=kvs)
     c = stats.as_c()
     _check("rbs_block_stats_varlen", load().rbs_block_stats_varlen(
-        ctypes.byref(shape), ctypes.byref(batch.c), _ptr(K), ctypes.byref(c), _stream(stream)))
+        ctypes.byref(sh), ctypes.byref(batch.c), _ptr(K), ctypes.byref(c), _stream(stream)))
     return stats
 
 
@@ -427,11 +616,18 @@ def rbs_select_varlen(shape: rbs_shape, batch: Batch, Q: torch.Tensor, stats: Bl
                       tau_rescue: float, n_sink: int, n_local: int, n_recent: int, counts=None, indices=None,
                       stream=None):
     """Stage 2 for every sequence of a batch (one launch)."""
+    qs = _check_q(shape, Q)
+    m, cap = rbs_varlen_blocks(shape, batch), rbs_varlen_index_capacity(shape, batch)
+    named = _check_stats(shape, stats, n_blocks_total=m, n_seqs=batch.n_seqs,
+                         summary_bytes=rbs_varlen_summary_bytes(shape, batch), need_fp32=False)
     if counts is None or indices is None:
         counts, indices = allocate_lists_varlen(shape, batch, Q.device)
+    _check_lists(shape, counts, indices, n_blocks_total=m, capacity=cap)
+    _on_gpu(("Q", Q), *named, ("counts", counts), ("indices", indices))
+    sh = _with_strides(shape, q=qs)
     c = stats.as_c()
     _check("rbs_select_varlen", load().rbs_select_varlen(
-        ctypes.byref(shape), ctypes.byref(batch.c), _ptr(Q), ctypes.byref(c), float(tau_base), float(tau_rescue),
+        ctypes.byref(sh), ctypes.byref(batch.c), _ptr(Q), ctypes.byref(c), float(tau_base), float(tau_rescue),
         int(n_sink), int(n_local), int(n_recent), _ptr(counts), _ptr(indices), _stream(stream)))
     return counts, indices
 
@@ -439,11 +635,20 @@ def rbs_select_varlen(shape: rbs_shape, batch: Batch, Q: torch.Tensor, stats: Bl
 def rbs_sparse_prefill_varlen(shape: rbs_shape, batch: Batch, Q, K, V, counts, indices, softmax_scale: float = 0.0,
                               O=None, lse=None, stream=None, workspace=AUTO):
     """Stage 3 for every sequence of a batch (one launch); returns O."""
+    qs = _check_q(shape, Q)
+    kvs = _check_kv(shape, K, V)
+    _check_lists(shape, counts, indices, n_blocks_total=rbs_varlen_blocks(shape, batch),
+                 capacity=rbs_varlen_index_capacity(shape, batch))
+    if O is not None:
+        _check_out(O, Q)
+    _check_lse(shape, lse)
+    _on_gpu(("Q", Q), ("K", K), ("V", V), ("counts", counts), ("indices", indices), ("O", O), ("lse", lse))
     if O is None:
-        O = torch.empty_like(Q)
+        O = _like_q(Q)
     ws = _workspace(workspace, Q.device, stream)
+    sh = _with_strides(shape, q=qs, kv=kvs)
     _check("rbs_sparse_prefill_varlen", load().rbs_sparse_prefill_varlen(
-        ctypes.byref(shape), ctypes.byref(batch.c), _ptr(Q), _ptr(K), _ptr(V), _ptr(counts), _ptr(indices),
+        ctypes.byref(sh), ctypes.byref(batch.c), _ptr(Q), _ptr(K), _ptr(V), _ptr(counts), _ptr(indices),
         float(softmax_scale), _ptr(O), _ptr(lse), _ptr(ws), _stream(stream)))
     return O
 
@@ -453,6 +658,9 @@ def rbs_dense_indices_varlen(shape: rbs_shape, batch: Batch, counts=None, indice
     """Full causal lists of every sequence of a batch."""
     if counts is None or indices is None:
         counts, indices = allocate_lists_varlen(shape, batch, device)
+    _check_lists(shape, counts, indices, n_blocks_total=rbs_varlen_blocks(shape, batch),
+                 capacity=rbs_varlen_index_capacity(shape, batch))
+    _on_gpu(("counts", counts), ("indices", indices))
     _check("rbs_dense_indices_varlen", load().rbs_dense_indices_varlen(
         ctypes.byref(shape), ctypes.byref(batch.c), _ptr(counts), _ptr(indices), _stream(stream)))
     return counts, indices
@@ -484,14 +692,34 @@ def allocate_fp8(shape: rbs_shape, device="cuda") -> Fp8Inputs:
                      torch.empty(nvt, **u8))
 
 
+def _check_fp8(shape: rbs_shape, f8):
+    if not isinstance(f8, Fp8Inputs):
+        raise ValueError("f8 must be Fp8Inputs")
+    n, d = shape.n_tokens, shape.head_dim
+    _check_tensor("f8.amax", f8.amax, torch.float32, (shape.n_q_heads + 2 * shape.n_kv_heads,))
+    _check_tensor("f8.Q8", f8.Q8, torch.uint8, (shape.n_q_heads, n, d))
+    _check_tensor("f8.K8", f8.K8, torch.uint8, (shape.n_kv_heads, n, d))
+    _check_tensor("f8.V8t", f8.V8t, torch.uint8, (rbs_fp8_vt_bytes(shape),))
+    return [("f8.amax", f8.amax), ("f8.Q8", f8.Q8), ("f8.K8", f8.K8), ("f8.V8t", f8.V8t)]
+
+
 def rbs_fp8_amax(shape: rbs_shape, Q, K, V, amax, stream=None):
-    _check("rbs_fp8_amax", load().rbs_fp8_amax(ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V), _ptr(amax),
+    qs = _check_q(shape, Q)
+    kvs = _check_kv(shape, K, V)
+    _check_tensor("amax", amax, torch.float32, (shape.n_q_heads + 2 * shape.n_kv_heads,))
+    _on_gpu(("Q", Q), ("K", K), ("V", V), ("amax", amax))
+    sh = _with_strides(shape, q=qs, kv=kvs)
+    _check("rbs_fp8_amax", load().rbs_fp8_amax(ctypes.byref(sh), _ptr(Q), _ptr(K), _ptr(V), _ptr(amax),
                                                _stream(stream)))
     return amax
 
 
 def rbs_fp8_pack(shape: rbs_shape, Q, K, V, f8: Fp8Inputs, stream=None) -> Fp8Inputs:
-    _check("rbs_fp8_pack", load().rbs_fp8_pack(ctypes.byref(shape), _ptr(Q), _ptr(K), _ptr(V), _ptr(f8.amax),
+    qs = _check_q(shape, Q)
+    kvs = _check_kv(shape, K, V)
+    _on_gpu(("Q", Q), ("K", K), ("V", V), *_check_fp8(shape, f8))
+    sh = _with_strides(shape, q=qs, kv=kvs)
+    _check("rbs_fp8_pack", load().rbs_fp8_pack(ctypes.byref(sh), _ptr(Q), _ptr(K), _ptr(V), _ptr(f8.amax),
                                                _ptr(f8.Q8), _ptr(f8.K8), _ptr(f8.V8t), _stream(stream)))
     return f8
 
@@ -506,12 +734,18 @@ def rbs_fp8_prepare(shape: rbs_shape, Q, K, V, f8: Fp8Inputs | None = None, stre
 
 def rbs_sparse_prefill_fp8(shape: rbs_shape, f8: Fp8Inputs, counts, indices, softmax_scale: float = 0.0, O=None,
                            lse=None, stream=None, workspace=AUTO):
-    """Stage 3 on the E4M3 inputs; returns O (bf16 [H_q][N][d])."""
+    """Stage 3 on the E4M3 inputs; returns O (bf16 [H_q][N][d], or the strides of the O given)."""
+    named = _check_fp8(shape, f8)
+    _check_lists(shape, counts, indices)
     if O is None:
         O = torch.empty((shape.n_q_heads, shape.n_tokens, shape.head_dim), dtype=torch.bfloat16,
                         device=f8.Q8.device)
+    qs = _heads_tokens("O", O, shape.n_q_heads, shape.n_tokens, shape.head_dim)
+    _check_lse(shape, lse)
+    _on_gpu(*named, ("counts", counts), ("indices", indices), ("O", O), ("lse", lse))
     ws = _workspace(workspace, f8.Q8.device, stream)
+    sh = _with_strides(shape, q=qs)
     _check("rbs_sparse_prefill_fp8", load().rbs_sparse_prefill_fp8(
-        ctypes.byref(shape), _ptr(f8.Q8), _ptr(f8.K8), _ptr(f8.V8t), _ptr(f8.amax), _ptr(counts), _ptr(indices),
+        ctypes.byref(sh), _ptr(f8.Q8), _ptr(f8.K8), _ptr(f8.V8t), _ptr(f8.amax), _ptr(counts), _ptr(indices),
         float(softmax_scale), _ptr(O), _ptr(lse), _ptr(ws), _stream(stream)))
     return O

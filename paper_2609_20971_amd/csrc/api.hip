@@ -16,6 +16,32 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 int blocks_of(const rbs_shape* s) { return (s->n_tokens + s->block_size - 1) / s->block_size; }
 
+constexpr int64_t kMaxTokStride = int64_t(1) << 23;  // (B - 1) rows of it, in bytes, fit the copies' 32-bit offsets
+
+// Strides of one tensor of H heads and T tokens of d = 128 (zero: the dense
+// value), validated: multiples of 8 elements (16-byte rows), token strides
+// within kMaxTokStride, and rows of distinct (head, token) pairs disjoint
+// (head-major or token-major nesting).
+int resolve_strides(int64_t head_in, int64_t tok_in, int H, int64_t T, int64_t* head, int64_t* tok) {
+  const int64_t st = tok_in == 0 ? 128 : tok_in;
+  const int64_t sh = head_in == 0 ? T * 128 : head_in;
+  if (st < 0 || sh < 0 || st % 8 != 0 || sh % 8 != 0 || st > kMaxTokStride) return RBS_ERR_SHAPE;
+  const bool head_major = st >= 128 && sh >= T * st;
+  const bool tok_major = sh >= 128 && st >= (int64_t)H * sh;
+  if (!head_major && !tok_major) return RBS_ERR_SHAPE;
+  *head = sh;
+  *tok = st;
+  return RBS_OK;
+}
+
+// The strides of Q (and O) and of K and V, resolved and validated.
+int strides_of(const rbs_shape* s, rbs::Strides* out) {
+  int rc = resolve_strides(s->q_stride_head, s->q_stride_tok, s->n_q_heads, s->n_tokens, &out->q_head, &out->q_tok);
+  if (rc != RBS_OK) return rc;
+  return resolve_strides(s->kv_stride_head, s->kv_stride_tok, s->n_kv_heads, s->n_tokens, &out->kv_head,
+                         &out->kv_tok);
+}
+
 int check_shape(const rbs_shape* s) {
   if (s == nullptr) return RBS_ERR_NULL;
   if (s->head_dim != 128) return RBS_ERR_UNSUPPORTED;
@@ -25,7 +51,8 @@ int check_shape(const rbs_shape* s) {
   if (s->n_q_heads % s->n_kv_heads != 0) return RBS_ERR_SHAPE;
   if (blocks_of(s) > kMaxBlocks) return RBS_ERR_SHAPE;
   if ((int64_t)s->n_q_heads * blocks_of(s) > INT32_MAX / 2) return RBS_ERR_SHAPE;
-  return RBS_OK;
+  rbs::Strides st;
+  return strides_of(s, &st);
 }
 
 int check_stats_ptrs(const rbs_stats* st) {
@@ -67,7 +94,8 @@ int check_batch(const rbs_shape* s, const rbs_batch* b, rbs::SeqTable* t) {
   }
   if (tok != s->n_tokens) return RBS_ERR_SHAPE;
   if ((int64_t)s->n_q_heads * blk > INT32_MAX / 2) return RBS_ERR_SHAPE;
-  return RBS_OK;
+  rbs::Strides st;
+  return strides_of(s, &st);
 }
 
 // Byte offset of the half-widths in the box summary (centres first, 256-aligned).
@@ -98,8 +126,12 @@ int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stat
   if ((rc = check_stats_ptrs(stats)) != RBS_OK) return rc;
   if (!aligned16(K)) return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
+  rbs::Strides st;
+  strides_of(shape, &st);
   rbs::StatsArgs a;
   a.K = static_cast<const uint16_t*>(K);
+  a.kv_head = st.kv_head;
+  a.kv_tok = st.kv_tok;
   a.n_tokens = shape->n_tokens;
   a.n_kv_heads = shape->n_kv_heads;
   a.block_size = shape->block_size;
@@ -116,6 +148,24 @@ int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stat
   return from_hip(rbs::launch_stats(a, static_cast<hipStream_t>(stream)));
 }
 
+int rbs_stats_summarize(const rbs_shape* shape, const rbs_stats* stats, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (stats == nullptr || stats->centroids == nullptr || stats->radii == nullptr || stats->beta == nullptr ||
+      stats->summary == nullptr)
+    return RBS_ERR_NULL;
+  if (!aligned16(stats->centroids) || !aligned16(stats->radii) || !aligned16(stats->beta) ||
+      !aligned16(stats->summary))
+    return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  unsigned char* sum = static_cast<unsigned char*>(stats->summary);
+  return from_hip(rbs::launch_summarize(
+      stats->centroids, stats->radii, stats->beta, shape->n_kv_heads, M, reinterpret_cast<_Float16*>(sum),
+      reinterpret_cast<float*>(sum + rbs::summary_uplift_offset(shape->n_kv_heads, M)),
+      reinterpret_cast<float*>(sum + rbs::summary_cnorm_offset(shape->n_kv_heads, M)),
+      static_cast<hipStream_t>(stream)));
+}
+
 int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats, float tau_base, float tau_rescue,
                int32_t n_sink, int32_t n_local, int32_t n_recent, int32_t* counts, int32_t* indices,
                void* stream) {
@@ -127,8 +177,12 @@ int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats, fl
   if (n_sink < 0 || n_local < 1 || n_recent < 0) return RBS_ERR_ARG;
   if (!aligned16(Q) || !aligned16(counts) || !aligned16(indices) || !aligned16(stats->summary)) return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
+  rbs::Strides st;
+  strides_of(shape, &st);
   rbs::SelectArgs a;
   a.Q = static_cast<const uint16_t*>(Q);
+  a.q_head = st.q_head;
+  a.q_tok = st.q_tok;
   a.n_tokens = shape->n_tokens;
   a.n_q_heads = shape->n_q_heads;
   a.n_kv_heads = shape->n_kv_heads;
@@ -166,6 +220,7 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
   a.Q = static_cast<const uint16_t*>(Q);
   a.K = static_cast<const uint16_t*>(K);
   a.V = static_cast<const uint16_t*>(V);
+  strides_of(shape, &a.st);
   a.n_tokens = shape->n_tokens;
   a.n_q_heads = shape->n_q_heads;
   a.n_kv_heads = shape->n_kv_heads;
@@ -198,8 +253,12 @@ int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, cons
       (workspace != nullptr && !aligned16(workspace)))
     return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
+  rbs::Strides st;
+  strides_of(shape, &st);
   rbs::SelectArgs sa;
   sa.Q = static_cast<const uint16_t*>(Q);
+  sa.q_head = st.q_head;
+  sa.q_tok = st.q_tok;
   sa.n_tokens = shape->n_tokens;
   sa.n_q_heads = shape->n_q_heads;
   sa.n_kv_heads = shape->n_kv_heads;
@@ -222,6 +281,7 @@ int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, cons
   aa.Q = sa.Q;
   aa.K = static_cast<const uint16_t*>(K);
   aa.V = static_cast<const uint16_t*>(V);
+  aa.st = st;
   aa.n_tokens = shape->n_tokens;
   aa.n_q_heads = shape->n_q_heads;
   aa.n_kv_heads = shape->n_kv_heads;
@@ -250,8 +310,12 @@ int rbs_block_box(const rbs_shape* shape, const void* K, const rbs_box* box, voi
   if (!aligned16(K) || !aligned16(box->center) || !aligned16(box->half) || !aligned16(box->summary))
     return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
+  rbs::Strides st;
+  strides_of(shape, &st);
   rbs::BoxArgs a;
   a.K = static_cast<const uint16_t*>(K);
+  a.kv_head = st.kv_head;
+  a.kv_tok = st.kv_tok;
   a.n_tokens = shape->n_tokens;
   a.n_kv_heads = shape->n_kv_heads;
   a.block_size = shape->block_size;
@@ -287,8 +351,12 @@ int rbs_select_variant(const rbs_shape* shape, const void* Q, const rbs_stats* s
   if (n_sink < 0 || n_local < 1 || n_recent < 0) return RBS_ERR_ARG;
   if (!aligned16(Q) || !aligned16(counts) || !aligned16(indices) || !aligned16(stats->summary)) return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
+  rbs::Strides st;
+  strides_of(shape, &st);
   rbs::SelectArgs a;
   a.Q = static_cast<const uint16_t*>(Q);
+  a.q_head = st.q_head;
+  a.q_tok = st.q_tok;
   a.n_tokens = shape->n_tokens;
   a.n_q_heads = shape->n_q_heads;
   a.n_kv_heads = shape->n_kv_heads;
@@ -351,8 +419,12 @@ int rbs_block_stats_varlen(const rbs_shape* shape, const rbs_batch* batch, const
   if ((rc = check_stats_ptrs(stats)) != RBS_OK) return rc;
   if (!aligned16(K)) return RBS_ERR_ALIGN;
   const int M = t.blk[t.n];
+  rbs::Strides st;
+  strides_of(shape, &st);
   rbs::StatsArgs a;
   a.K = static_cast<const uint16_t*>(K);
+  a.kv_head = st.kv_head;
+  a.kv_tok = st.kv_tok;
   a.n_tokens = shape->n_tokens;
   a.n_kv_heads = shape->n_kv_heads;
   a.block_size = shape->block_size;
@@ -381,8 +453,12 @@ int rbs_select_varlen(const rbs_shape* shape, const rbs_batch* batch, const void
   if (n_sink < 0 || n_local < 1 || n_recent < 0) return RBS_ERR_ARG;
   if (!aligned16(Q) || !aligned16(counts) || !aligned16(indices) || !aligned16(stats->summary)) return RBS_ERR_ALIGN;
   const int M = t.blk[t.n];
+  rbs::Strides st;
+  strides_of(shape, &st);
   rbs::SelectArgs a;
   a.Q = static_cast<const uint16_t*>(Q);
+  a.q_head = st.q_head;
+  a.q_tok = st.q_tok;
   a.n_tokens = shape->n_tokens;
   a.n_q_heads = shape->n_q_heads;
   a.n_kv_heads = shape->n_kv_heads;
@@ -420,6 +496,7 @@ int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, co
   a.Q = static_cast<const uint16_t*>(Q);
   a.K = static_cast<const uint16_t*>(K);
   a.V = static_cast<const uint16_t*>(V);
+  strides_of(shape, &a.st);
   a.n_tokens = shape->n_tokens;
   a.n_q_heads = shape->n_q_heads;
   a.n_kv_heads = shape->n_kv_heads;
@@ -456,8 +533,10 @@ int rbs_fp8_amax(const rbs_shape* shape, const void* Q, const void* K, const voi
   if (rc != RBS_OK) return rc;
   if (Q == nullptr || K == nullptr || V == nullptr || amax == nullptr) return RBS_ERR_NULL;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(amax)) return RBS_ERR_ALIGN;
+  rbs::Strides st;
+  strides_of(shape, &st);
   return from_hip(rbs::launch_fp8_amax(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
-                                       static_cast<const uint16_t*>(V), shape->n_tokens, shape->n_q_heads,
+                                       static_cast<const uint16_t*>(V), st, shape->n_tokens, shape->n_q_heads,
                                        shape->n_kv_heads, amax, static_cast<hipStream_t>(stream)));
 }
 
@@ -471,8 +550,10 @@ int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const voi
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(amax) || !aligned16(Q8) || !aligned16(K8) ||
       !aligned16(V8t))
     return RBS_ERR_ALIGN;
+  rbs::Strides st;
+  strides_of(shape, &st);
   return from_hip(rbs::launch_fp8_pack(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
-                                       static_cast<const uint16_t*>(V), shape->n_tokens, shape->n_q_heads,
+                                       static_cast<const uint16_t*>(V), st, shape->n_tokens, shape->n_q_heads,
                                        shape->n_kv_heads, shape->block_size, blocks_of(shape), amax,
                                        static_cast<uint8_t*>(Q8),
                                        static_cast<uint8_t*>(K8), static_cast<uint8_t*>(V8t),
@@ -494,18 +575,20 @@ int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K
     return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
+  rbs::Strides st;
+  strides_of(shape, &st);
   return from_hip(rbs::launch_attention_fp8(
       static_cast<const uint8_t*>(Q8), static_cast<const uint8_t*>(K8), static_cast<const uint8_t*>(V8t), amax,
       shape->n_tokens, shape->n_q_heads, shape->n_kv_heads, shape->block_size, M, counts, indices,
-      rbs_index_capacity(M), scale,
-      static_cast<uint16_t*>(O), lse, static_cast<int*>(workspace), static_cast<hipStream_t>(stream)));
+      rbs_index_capacity(M), scale, static_cast<uint16_t*>(O), st.q_head, st.q_tok, lse,
+      static_cast<int*>(workspace), static_cast<hipStream_t>(stream)));
 }
 
 const char* rbs_status_str(int status) {
   switch (status) {
     case RBS_OK: return "ok";
     case RBS_ERR_NULL: return "null pointer argument";
-    case RBS_ERR_SHAPE: return "invalid shape (token/head counts, head ratio or size limits)";
+    case RBS_ERR_SHAPE: return "invalid shape (token/head counts, head ratio, size limits or strides)";
     case RBS_ERR_UNSUPPORTED: return "unsupported head_dim or block_size (need d = 128, B in {64, 128, 256})";
     case RBS_ERR_ARG: return "invalid argument (threshold outside [0, 1], window < 1, bad scale)";
     case RBS_ERR_ALIGN: return "device pointer not 16-byte aligned";

@@ -66,19 +66,53 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)p;
 }
 
-// Wave w copies rows 32w .. 32w + 31 of a B x 128 bf16 tile (8 copies of
-// 4 rows each).  Rows at or past nk repeat row nk - 1 (masked later).
-__device__ __forceinline__ void issue_tile(const uint16_t* tile_base, int nk, uint32_t lds_base, int wave, int lane,
-                                           bool is_v) {
+// Wave w copies rows 32w .. 32w + 31 of a B x 128 bf16 tile whose rows are
+// row_bytes apart in global memory (8 copies of 4 rows each).  Rows at or
+// past nk repeat row nk - 1 (masked later).  Used for a sequence's short last
+// block only; kept a loop so that its offset arithmetic is not hoisted into
+// the common path.
+__device__ __forceinline__ void issue_tile(const uint16_t* tile_base, int nk, uint32_t row_bytes, uint32_t lds_base,
+                                           int wave, int lane, bool is_v) {
   const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds_base + (uint32_t)(32 * wave) * 256u);
   const int pc = lane & 15;
-#pragma unroll
+#pragma unroll 1
   for (int j = 0; j < 8; ++j) {
     const int row = 32 * wave + 4 * j + (lane >> 4);
     const int c = is_v ? vswz(row, pc) : kswz(row, pc);
-    const uint32_t voff = (uint32_t)min(row, nk - 1) * 256u + 16u * (uint32_t)c;
+    const uint32_t voff = (uint32_t)min(row, nk - 1) * row_bytes + 16u * (uint32_t)c;
     lds_dma16(tile_base, voff, lds_wave + (uint32_t)j * 1024u);
   }
+}
+
+// Per-lane offsets of the copies of a full tile (every row inside the block):
+// copy j of wave w moves row 32w + 4j + lane/16, chunk lane%16.  With the
+// row's low bits fixed by (j, lane) -- 32w is a multiple of 16 -- a K copy's
+// offset from the copy's first row depends on j % 4 only, and a V copy's not
+// on j at all; the 4j rows move into the scalar base address.
+struct TileOffsets {
+  uint32_t k[4];
+  uint32_t v;
+};
+
+__device__ __forceinline__ TileOffsets tile_offsets(uint32_t row_bytes, int wave, int lane) {
+  TileOffsets t;
+  const int l4 = lane >> 4, pc = lane & 15;
+  const uint32_t row0 = (uint32_t)(32 * wave + l4) * row_bytes;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) t.k[j] = row0 + 16u * (uint32_t)kswz(4 * j + l4, pc);
+  t.v = row0 + 16u * (uint32_t)vswz(l4, pc);
+  return t;
+}
+
+// issue_tile for a tile with all B rows inside the block (nk == B), from
+// precomputed offsets: no per-copy vector arithmetic.
+__device__ __forceinline__ void issue_tile_full(const uint16_t* tile_base, uint32_t row_bytes, const TileOffsets& t,
+                                                uint32_t lds_base, int wave, bool is_v) {
+  const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds_base + (uint32_t)(32 * wave) * 256u);
+  const unsigned char* base = reinterpret_cast<const unsigned char*>(tile_base);
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    lds_dma16(base + (size_t)j * 4u * row_bytes, is_v ? t.v : t.k[j & 3], lds_wave + (uint32_t)j * 1024u);
 }
 
 // Rescale threshold of the online softmax, in log2 units.
@@ -89,8 +123,10 @@ struct AttnCore {
   const uint16_t* Q;
   const uint16_t* K;
   const uint16_t* V;
+  int64_t q_head, q_tok;    // element strides of Q and O between heads and between tokens
+  int64_t kv_head, kv_tok;  // the same for K and V
   int N, M, group;
-  int ld;  // tokens between consecutive heads of Q, K, V, O, lse (N, or the batch's total)
+  int ld;  // tokens between consecutive heads of lse (N, or the batch's total)
   float scale_log2;
   uint16_t* O;
   float* lse;
@@ -99,7 +135,7 @@ struct AttnCore {
 // Attention of query block i of query head h over the count key blocks that
 // list_at(0 .. count - 1) returns (wave-uniform, ascending, each <= i), by the
 // B/32 waves of the calling workgroup.  k_lds and v_lds: B * 256 bytes of LDS
-// each, 256-byte aligned.  VARLEN: the head stride c.ld differs from N (a
+// each, 256-byte aligned.  VARLEN: the lse head stride c.ld differs from N (a
 // sequence of a batch); otherwise it is N and c.ld is not read.
 template <int BS, bool VARLEN = false, typename ListAt>
 __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, int count, ListAt list_at,
@@ -119,7 +155,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
 
   bf16x8 qreg[8];
   {
-    const uint16_t* qrow = Q + ((size_t)h * ld + qpos) * kHeadDim + 8 * half;
+    const uint16_t* qrow = Q + h * c.q_head + (int64_t)qpos * c.q_tok + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       const uint4 v = q_ok ? *reinterpret_cast<const uint4*>(qrow + 16 * ks) : make_uint4(0u, 0u, 0u, 0u);
@@ -131,8 +167,19 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   // would also wait for them.
   RBS_WAIT_VMCNT(0);
 
-  const uint16_t* kg = c.K + g * ld * kHeadDim;
-  const uint16_t* vg = c.V + g * ld * kHeadDim;
+  const uint16_t* kg = c.K + g * c.kv_head;
+  const uint16_t* vg = c.V + g * c.kv_head;
+  const int64_t tile_stride = (int64_t)BS * c.kv_tok;  // elements between consecutive key blocks
+  const uint32_t row_bytes = (uint32_t)(c.kv_tok * 2);
+  const TileOffsets toff = tile_offsets(row_bytes, wave, lane);
+  // Copies of key block b's K or V tile (nb rows inside the sequence).
+  auto copy_tile = [&](const uint16_t* base, int b, uint32_t lds_base, bool is_v) __attribute__((always_inline)) {
+    const int nb = min(BS, N - b * BS);
+    if (nb == BS)
+      issue_tile_full(base + b * tile_stride, row_bytes, toff, lds_base, wave, is_v);
+    else
+      issue_tile(base + b * tile_stride, nb, row_bytes, lds_base, wave, lane, is_v);
+  };
 
   float ms_run = -INFINITY;  // running reference maximum, log2 units
   float l_run = 0.f;         // this lane's share of the softmax denominator
@@ -154,8 +201,8 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   int kb_ahead = count > 1 ? list_at(1) : 0;
   if (count > 0) {
     const int nk0 = min(BS, N - kb * BS);
-    issue_tile(kg + (size_t)kb * BS * kHeadDim, nk0, k_base, wave, lane, false);
-    issue_tile(vg + (size_t)kb * BS * kHeadDim, nk0, v_base, wave, lane, true);
+    copy_tile(kg, kb, k_base, false);
+    copy_tile(vg, kb, v_base, true);
   }
   for (int n = 0; n < count; ++n) {
     const bool has_next = n + 1 < count;
@@ -189,23 +236,31 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
       if (sub == BS / SUB - 1) {
         __syncthreads();  // every wave is done with this K tile
         if (has_next)
-          issue_tile(kg + (size_t)kb_next * BS * kHeadDim, min(BS, N - kb_next * BS), k_base, wave, lane, false);
+          copy_tile(kg, kb_next, k_base, false);
       }
       if (diag || nk < BS) {
+        // Keys past limit are masked: past the block's end, and on the
+        // diagonal past the query.  Element r of tile mt holds key
+        // kbase + 32 mt + 4 half + (8 (r / 4) + r % 4).  Each compare is used
+        // at once (a scheduling barrier per element): hoisted together, the
+        // 64 compare masks overflowed the scalar registers.
+        const int limit = diag ? min(q_local, nk - 1) : nk - 1;
 #pragma unroll
-        for (int mt = 0; mt < KT; ++mt)
+        for (int mt = 0; mt < KT; ++mt) {
+          const int lim = limit - kbase - 32 * mt - 4 * half;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int key = kbase + 32 * mt + mfma_row(r, lane);
-            if (key >= nk || (diag && key > q_local)) s[mt][r] = -INFINITY;
+            s[mt][r] = (8 * (r >> 2) + (r & 3)) > lim ? -INFINITY : s[mt][r];
+            __builtin_amdgcn_sched_barrier(0);
           }
+        }
       }
       float mx = -INFINITY;
 #pragma unroll
       for (int mt = 0; mt < KT; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
-      mx = fmaxf(mx, wave_xor_f(mx, 32));
+      mx = half_max(mx);
       // Lazily raised reference maximum (log2 units): O and the denominator
       // are rescaled only when some row's maximum exceeds the reference by
       // more than kRescaleSlack, so the exponentials stay below 2^kRescaleSlack.
@@ -262,14 +317,14 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
     }
     __syncthreads();  // every wave is done with this V tile
     if (has_next)
-      issue_tile(vg + (size_t)kb_next * BS * kHeadDim, min(BS, N - kb_next * BS), v_base, wave, lane, true);
+      copy_tile(vg, kb_next, v_base, true);
     kb = kb_next;
   }
 
   const float l_tot = l_run + wave_xor_f(l_run, 32);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   if (q_ok) {
-    uint16_t* orow = c.O + ((size_t)h * ld + qpos) * kHeadDim;
+    uint16_t* orow = c.O + h * c.q_head + (int64_t)qpos * c.q_tok;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -385,6 +440,10 @@ inline AttnCore make_attn_core(const AttnArgs& a) {
   c.Q = a.Q;
   c.K = a.K;
   c.V = a.V;
+  c.q_head = a.st.q_head;
+  c.q_tok = a.st.q_tok;
+  c.kv_head = a.st.kv_head;
+  c.kv_tok = a.st.kv_tok;
   c.N = a.n_tokens;
   c.M = a.n_blocks;
   c.group = a.n_q_heads / a.n_kv_heads;

@@ -64,11 +64,11 @@ __device__ __forceinline__ void attend_slot_varlen(AttnCore c, const int32_t* __
   const int rem = local - g * per_group;
   const int i = c.M - 1 - rem / c.group;
   const int h = g * c.group + rem % c.group;
-  const size_t tok0 = (size_t)t.tok[sq] * kHeadDim;
-  c.Q += tok0;
-  c.K += tok0;
-  c.V += tok0;
-  c.O += tok0;
+  const int64_t tok0 = t.tok[sq];
+  c.Q += tok0 * c.q_tok;
+  c.K += tok0 * c.kv_tok;
+  c.V += tok0 * c.kv_tok;
+  c.O += tok0 * c.q_tok;
   if (c.lse != nullptr) c.lse += t.tok[sq];
   const int count = min(max(counts[(size_t)h * t.blk[t.n] + t.blk[sq] + i], 0), i + 1);
   const int32_t* list = indices + (int64_t)h * t.cap[t.n] + t.cap[sq] + (int64_t)i * (i + 1) / 2;

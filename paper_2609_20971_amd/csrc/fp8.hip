@@ -80,17 +80,24 @@ __global__ void fp8_zero_kernel(uint32_t* __restrict__ x, int n) {
   if (i < n) x[i] = 0u;
 }
 
-// Largest |x| of every head of a [heads][N][d] bf16 tensor; blockIdx.y = head,
+// 16-byte chunk c (token c / 16, dimensions 8 (c % 16) ..) of head `head` of a
+// bf16 tensor with element strides (head_stride, tok_stride).
+__device__ __forceinline__ uint4 load_chunk(const uint16_t* X, int64_t head_stride, int64_t tok_stride, int head,
+                                            int64_t c) {
+  return *reinterpret_cast<const uint4*>(X + head * head_stride + (c >> 4) * tok_stride + 8 * (c & 15));
+}
+
+// Largest |x| of every head of a bf16 tensor of N tokens; blockIdx.y = head,
 // blockIdx.x strides over the head's 16-byte chunks.  Non-negative floats order
 // like their bit patterns, so the maximum is an integer atomic max.
-__global__ __launch_bounds__(256) void fp8_amax_kernel(const uint16_t* __restrict__ X, int64_t chunks_per_head,
+__global__ __launch_bounds__(256) void fp8_amax_kernel(const uint16_t* __restrict__ X, int64_t head_stride,
+                                                       int64_t tok_stride, int64_t chunks_per_head,
                                                        uint32_t* __restrict__ amax_bits) {
   const int head = blockIdx.y;
-  const uint4* src = reinterpret_cast<const uint4*>(X) + (size_t)head * chunks_per_head;
   float m = 0.f;
   for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < chunks_per_head;
        c += (int64_t)gridDim.x * blockDim.x) {
-    const uint4 v = src[c];
+    const uint4 v = load_chunk(X, head_stride, tok_stride, head, c);
     float f[8];
     unpack8(v, f);
 #pragma unroll
@@ -110,18 +117,19 @@ __global__ __launch_bounds__(256) void fp8_amax_kernel(const uint16_t* __restric
 
 // ------------------------------------------------------------------ pack
 
-// Row-major E4M3 copy of a [heads][N][d] bf16 tensor: 8 elements per thread.
-__global__ __launch_bounds__(256) void fp8_pack_rows_kernel(const uint16_t* __restrict__ X, int64_t chunks_per_head,
+// Dense row-major E4M3 copy [heads][N][d] of a strided bf16 tensor: 8
+// elements per thread.
+__global__ __launch_bounds__(256) void fp8_pack_rows_kernel(const uint16_t* __restrict__ X, int64_t head_stride,
+                                                            int64_t tok_stride, int64_t chunks_per_head,
                                                             const float* __restrict__ amax,
                                                             uint8_t* __restrict__ X8) {
   const int head = blockIdx.y;
   const float inv = fp8_inv_scale(amax[head]);
-  const uint4* src = reinterpret_cast<const uint4*>(X) + (size_t)head * chunks_per_head;
   uint2* dst = reinterpret_cast<uint2*>(X8) + (size_t)head * chunks_per_head;
   for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < chunks_per_head;
        c += (int64_t)gridDim.x * blockDim.x) {
     float f[8];
-    unpack8(src[c], f);
+    unpack8(load_chunk(X, head_stride, tok_stride, head, c), f);
     uint2 o;
     o.x = (uint32_t)pack4_fp8(f[0] * inv, f[1] * inv, f[2] * inv, f[3] * inv);
     o.y = (uint32_t)pack4_fp8(f[4] * inv, f[5] * inv, f[6] * inv, f[7] * inv);
@@ -133,21 +141,22 @@ __global__ __launch_bounds__(256) void fp8_pack_rows_kernel(const uint16_t* __re
 // values, rounds them to E4M3 into LDS [key][d], and writes the d x B tile with
 // the keys in vt_key order, laid out by vt_offset (keys past N are zero).
 template <int BS>
-__global__ __launch_bounds__(256) void fp8_pack_vt_kernel(const uint16_t* __restrict__ V, int N, int M,
+__global__ __launch_bounds__(256) void fp8_pack_vt_kernel(const uint16_t* __restrict__ V, int64_t head_stride,
+                                                          int64_t tok_stride, int N, int M,
                                                           const float* __restrict__ amax_v,
                                                           uint8_t* __restrict__ V8t) {
   __shared__ uint8_t tile[BS * kHeadDim];
   const int kb = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
   const float inv = fp8_inv_scale(amax_v[g]);
   const int nk = min(BS, N - kb * BS);
-  const uint4* src = reinterpret_cast<const uint4*>(V + ((size_t)g * N + (size_t)kb * BS) * kHeadDim);
+  const uint16_t* src = V + g * head_stride + (int64_t)kb * BS * tok_stride;
   // BS rows x 16 chunks of 8 elements.
   for (int c = tid; c < BS * 16; c += 256) {
     const int key = c >> 4;
     uint2 o = make_uint2(0u, 0u);
     if (key < nk) {
       float f[8];
-      unpack8(src[c], f);
+      unpack8(*reinterpret_cast<const uint4*>(src + key * tok_stride + 8 * (c & 15)), f);
       o.x = (uint32_t)pack4_fp8(f[0] * inv, f[1] * inv, f[2] * inv, f[3] * inv);
       o.y = (uint32_t)pack4_fp8(f[4] * inv, f[5] * inv, f[6] * inv, f[7] * inv);
     }
@@ -212,6 +221,7 @@ struct AttnF8Args {
   const int32_t* indices;
   int64_t capacity;
   uint16_t* O;
+  int64_t o_head, o_tok;  // element strides of O (those of the bf16 Q)
   float* lse;
 };
 
@@ -368,7 +378,7 @@ __device__ __forceinline__ void attend_block_fp8(const AttnF8Args& c, int h, int
   const float l_tot = lsum[0];
   const float inv = l_tot > 0.f ? v_deq / l_tot : 0.f;
   if (q_ok) {
-    uint16_t* orow = c.O + ((size_t)h * N + qpos) * kHeadDim;
+    uint16_t* orow = c.O + h * c.o_head + (int64_t)qpos * c.o_tok;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -418,40 +428,43 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
 
 // ------------------------------------------------------------------ launchers
 
-hipError_t launch_fp8_amax(const uint16_t* Q, const uint16_t* K, const uint16_t* V, int n_tokens, int n_q_heads,
-                           int n_kv_heads, float* amax, hipStream_t s) {
+hipError_t launch_fp8_amax(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const Strides& st, int n_tokens,
+                           int n_q_heads, int n_kv_heads, float* amax, hipStream_t s) {
   const int n = n_q_heads + 2 * n_kv_heads;
   uint32_t* bits = reinterpret_cast<uint32_t*>(amax);
   hipLaunchKernelGGL(fp8_zero_kernel, dim3((n + 255) / 256), dim3(256), 0, s, bits, n);
   const int64_t chunks = (int64_t)n_tokens * kHeadDim / 8;
   const int gx = (int)((chunks + 255) / 256 < 64 ? (chunks + 255) / 256 : 64);
-  hipLaunchKernelGGL(fp8_amax_kernel, dim3(gx, n_q_heads), dim3(256), 0, s, Q, chunks, bits);
-  hipLaunchKernelGGL(fp8_amax_kernel, dim3(gx, n_kv_heads), dim3(256), 0, s, K, chunks, bits + n_q_heads);
-  hipLaunchKernelGGL(fp8_amax_kernel, dim3(gx, n_kv_heads), dim3(256), 0, s, V, chunks,
+  hipLaunchKernelGGL(fp8_amax_kernel, dim3(gx, n_q_heads), dim3(256), 0, s, Q, st.q_head, st.q_tok, chunks, bits);
+  hipLaunchKernelGGL(fp8_amax_kernel, dim3(gx, n_kv_heads), dim3(256), 0, s, K, st.kv_head, st.kv_tok, chunks,
+                     bits + n_q_heads);
+  hipLaunchKernelGGL(fp8_amax_kernel, dim3(gx, n_kv_heads), dim3(256), 0, s, V, st.kv_head, st.kv_tok, chunks,
                      bits + n_q_heads + n_kv_heads);
   return hipGetLastError();
 }
 
-hipError_t launch_fp8_pack(const uint16_t* Q, const uint16_t* K, const uint16_t* V, int n_tokens, int n_q_heads,
-                           int n_kv_heads, int block_size, int n_blocks, const float* amax, uint8_t* Q8, uint8_t* K8,
-                           uint8_t* V8t, hipStream_t s) {
+hipError_t launch_fp8_pack(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const Strides& st, int n_tokens,
+                           int n_q_heads, int n_kv_heads, int block_size, int n_blocks, const float* amax, uint8_t* Q8,
+                           uint8_t* K8, uint8_t* V8t, hipStream_t s) {
   const int64_t chunks = (int64_t)n_tokens * kHeadDim / 8;
   const int gx = (int)((chunks + 255) / 256 < 512 ? (chunks + 255) / 256 : 512);
-  hipLaunchKernelGGL(fp8_pack_rows_kernel, dim3(gx, n_q_heads), dim3(256), 0, s, Q, chunks, amax, Q8);
-  hipLaunchKernelGGL(fp8_pack_rows_kernel, dim3(gx, n_kv_heads), dim3(256), 0, s, K, chunks, amax + n_q_heads, K8);
+  hipLaunchKernelGGL(fp8_pack_rows_kernel, dim3(gx, n_q_heads), dim3(256), 0, s, Q, st.q_head, st.q_tok, chunks,
+                     amax, Q8);
+  hipLaunchKernelGGL(fp8_pack_rows_kernel, dim3(gx, n_kv_heads), dim3(256), 0, s, K, st.kv_head, st.kv_tok, chunks,
+                     amax + n_q_heads, K8);
   const float* amax_v = amax + n_q_heads + n_kv_heads;
   switch (block_size) {
     case 64:
-      hipLaunchKernelGGL(fp8_pack_vt_kernel<64>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, n_tokens, n_blocks,
-                         amax_v, V8t);
+      hipLaunchKernelGGL(fp8_pack_vt_kernel<64>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, st.kv_head,
+                         st.kv_tok, n_tokens, n_blocks, amax_v, V8t);
       break;
     case 128:
-      hipLaunchKernelGGL(fp8_pack_vt_kernel<128>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, n_tokens,
-                         n_blocks, amax_v, V8t);
+      hipLaunchKernelGGL(fp8_pack_vt_kernel<128>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, st.kv_head,
+                         st.kv_tok, n_tokens, n_blocks, amax_v, V8t);
       break;
     case 256:
-      hipLaunchKernelGGL(fp8_pack_vt_kernel<256>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, n_tokens,
-                         n_blocks, amax_v, V8t);
+      hipLaunchKernelGGL(fp8_pack_vt_kernel<256>, dim3(n_blocks, n_kv_heads), dim3(256), 0, s, V, st.kv_head,
+                         st.kv_tok, n_tokens, n_blocks, amax_v, V8t);
       break;
     default: return hipErrorInvalidValue;
   }
@@ -476,7 +489,7 @@ static hipError_t launch_attention_fp8_bs(const AttnF8Args& a, int* queue, hipSt
 hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint8_t* V8t, const float* amax,
                                 int n_tokens, int n_q_heads, int n_kv_heads, int block_size, int n_blocks,
                                 const int32_t* counts, const int32_t* indices, int64_t capacity, float scale,
-                                uint16_t* O, float* lse, int* queue, hipStream_t s) {
+                                uint16_t* O, int64_t o_head, int64_t o_tok, float* lse, int* queue, hipStream_t s) {
   AttnF8Args a;
   a.Q8 = Q8;
   a.K8 = K8;
@@ -491,6 +504,8 @@ hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint
   a.indices = indices;
   a.capacity = capacity;
   a.O = O;
+  a.o_head = o_head;
+  a.o_tok = o_tok;
   a.lse = lse;
   switch (block_size) {
     case 64: return launch_attention_fp8_bs<64>(a, queue, s);

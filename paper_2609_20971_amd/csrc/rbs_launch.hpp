@@ -7,8 +7,15 @@
 
 namespace rbs {
 
+// Element strides of the bf16 tensors between heads and between tokens (the
+// head dimension is contiguous): Q and O share q_*, K and V share kv_*.
+struct Strides {
+  int64_t q_head, q_tok, kv_head, kv_tok;
+};
+
 struct StatsArgs {
   const uint16_t* K;
+  int64_t kv_head, kv_tok;  // K strides
   int n_tokens, n_kv_heads, block_size, n_blocks;
   float* centroids;
   float* radii;
@@ -21,6 +28,7 @@ struct StatsArgs {
 
 struct BoxArgs {
   const uint16_t* K;
+  int64_t kv_head, kv_tok;  // K strides
   int n_tokens, n_kv_heads, block_size, n_blocks;
   float* center;
   float* half;
@@ -30,6 +38,7 @@ struct BoxArgs {
 
 struct SelectArgs {
   const uint16_t* Q;
+  int64_t q_head, q_tok;  // Q strides
   int n_tokens, n_q_heads, n_kv_heads, block_size, n_blocks;
   int mode = 0;                       // SelectMode (select_block.hpp)
   const _Float16* cent16;             // box: scaled box centres
@@ -49,6 +58,7 @@ struct AttnArgs {
   const uint16_t* Q;
   const uint16_t* K;
   const uint16_t* V;
+  Strides st;  // Q and O; K and V
   int n_tokens, n_q_heads, n_kv_heads, block_size, n_blocks;
   const int32_t* counts;
   const int32_t* indices;
@@ -110,6 +120,9 @@ inline SeqTable single_sequence(int n_tokens, int n_blocks) {
 }
 
 hipError_t launch_stats(const StatsArgs& a, hipStream_t s);
+// The select-ready summary from fp32 centroids, radii and beta [H_kv][M].
+hipError_t launch_summarize(const float* centroids, const float* radii, const float* beta, int n_kv_heads,
+                            int n_blocks, _Float16* cent16, float* uplift, float* cnorm, hipStream_t s);
 hipError_t launch_box(const BoxArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
@@ -118,16 +131,17 @@ size_t fused_smem_bytes(int block_size, int n_blocks);
 hipError_t launch_dense_indices(int n_q_heads, int n_blocks, int64_t capacity, int32_t* counts,
                                 int32_t* indices, hipStream_t s);
 
-// FP8 attention inputs (fp8.hip).
-hipError_t launch_fp8_amax(const uint16_t* Q, const uint16_t* K, const uint16_t* V, int n_tokens, int n_q_heads,
-                           int n_kv_heads, float* amax, hipStream_t s);
-hipError_t launch_fp8_pack(const uint16_t* Q, const uint16_t* K, const uint16_t* V, int n_tokens, int n_q_heads,
-                           int n_kv_heads, int block_size, int n_blocks, const float* amax, uint8_t* Q8, uint8_t* K8,
-                           uint8_t* V8t, hipStream_t s);
+// FP8 attention inputs (fp8.hip).  The bf16 inputs have the strides st; the
+// FP8 copies are dense; O is written with Q's strides.
+hipError_t launch_fp8_amax(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const Strides& st, int n_tokens,
+                           int n_q_heads, int n_kv_heads, float* amax, hipStream_t s);
+hipError_t launch_fp8_pack(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const Strides& st, int n_tokens,
+                           int n_q_heads, int n_kv_heads, int block_size, int n_blocks, const float* amax, uint8_t* Q8,
+                           uint8_t* K8, uint8_t* V8t, hipStream_t s);
 hipError_t launch_attention_fp8(const uint8_t* Q8, const uint8_t* K8, const uint8_t* V8t, const float* amax,
                                 int n_tokens, int n_q_heads, int n_kv_heads, int block_size, int n_blocks,
                                 const int32_t* counts, const int32_t* indices, int64_t capacity, float scale,
-                                uint16_t* O, float* lse, int* queue, hipStream_t s);
+                                uint16_t* O, int64_t o_head, int64_t o_tok, float* lse, int* queue, hipStream_t s);
 
 // Varlen launchers: the Args hold the batch totals (n_tokens = T, n_blocks and
 // capacity = the table's last offsets); every sequence runs in the same launch.

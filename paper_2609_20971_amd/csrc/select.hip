@@ -29,7 +29,7 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(4))) voi
   const int local = work - Hq * t.blk[sq];
   c.N = t.tok[sq + 1] - t.tok[sq];
   c.M = t.blk[sq + 1] - t.blk[sq];
-  c.Q += (size_t)t.tok[sq] * kHeadDim;
+  c.Q += t.tok[sq] * c.q_tok;
   c.cent16 += (size_t)t.blk[sq] * kHeadDim;
   c.uplift += t.blk[sq];
   c.cnorm += t.blk[sq];

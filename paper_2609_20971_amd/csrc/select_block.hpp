@@ -28,7 +28,13 @@
 namespace rbs {
 
 constexpr int kTile = 32;  // centroids per tile
-constexpr float kPlainBound = 120.0f;  // |exponent| bound for unshifted exp2 sums (fp32 normal range: 2^-126)
+// |exponent| bound for unshifted exp2 sums.  A block's sum adds at most 256
+// terms (8 waves of 32 tokens at B = 256), each below 2^(112 (1 + 2^-10)) --
+// the bound is tested with the fp32 centroid norm, and the f16-rounded
+// centroid the MFMA uses is at most 2^-11 relatively longer -- so a sum stays
+// below 2^121, inside fp32's range, and every term above fp32's normal
+// minimum 2^-126.
+constexpr float kPlainBound = 112.0f;
 constexpr float kCandSlack = 1e-2f;    // log2 units: rounding allowance of the rescue-candidate test
 
 // Branches a tile pass scores.
@@ -53,8 +59,8 @@ enum SelectMode {
 // Arguments of one selection, shared by the stand-alone and the fused kernel.
 struct SelectCore {
   const uint16_t* Q;
+  int64_t q_head, q_tok;  // element strides of Q between heads and between tokens
   int N, M, group;
-  int ldq;  // tokens between consecutive query heads of Q (N, or the batch's total)
   int ldm;  // blocks between consecutive heads of the block arrays and counts (M, or the batch's total)
   const _Float16* cent16;     // dual, centroid, full-L2: scaled centroids; box: scaled box centres
   const _Float16* half16;     // box: scaled box half-widths
@@ -119,7 +125,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   f16x8 qabs[MODE == kSelectBox ? 8 : 1];  // |q| for the box half-widths
   float sq = 0.f;
   {
-    const uint16_t* qrow = Q + ((size_t)h * c.ldq + row0 + t_local) * kHeadDim + 8 * half;
+    const uint16_t* qrow = Q + h * c.q_head + (int64_t)(row0 + t_local) * c.q_tok + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       uint4 v = row_ok ? *reinterpret_cast<const uint4*>(qrow + 16 * ks) : make_uint4(0u, 0u, 0u, 0u);
@@ -490,10 +496,11 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
 inline SelectCore make_select_core(const SelectArgs& a) {
   SelectCore c;
   c.Q = a.Q;
+  c.q_head = a.q_head;
+  c.q_tok = a.q_tok;
   c.N = a.n_tokens;
   c.M = a.n_blocks;
   c.group = a.n_q_heads / a.n_kv_heads;
-  c.ldq = a.n_tokens;
   c.ldm = a.n_blocks;
   c.cent16 = a.cent16;
   c.half16 = a.half16;

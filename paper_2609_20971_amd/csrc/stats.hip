@@ -145,7 +145,8 @@ __device__ void order_stats4(const uint32_t* keys, int n, int ka, int kb, uint32
 // Block blockIdx.x of all the sequences' blocks (sequence s owns blocks
 // t.blk[s] .. t.blk[s+1]-1 and tokens t.tok[s] .. t.tok[s+1]-1), KV head blockIdx.y.
 template <int BS>
-__global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __restrict__ K, const SeqTable t,
+__global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __restrict__ K, int64_t kv_head,
+                                                             int64_t kv_tok, const SeqTable t,
                                                              float* __restrict__ centroids,
                                                              float* __restrict__ radii,
                                                              _Float16* __restrict__ cent16,
@@ -157,19 +158,19 @@ __global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __
   const int bg = blockIdx.x, g = blockIdx.y;
   const int sq = seq_of(t.blk, t.n, bg);
   const int b = bg - t.blk[sq];
-  const int T = t.tok[t.n], M = t.blk[t.n];
+  const int M = t.blk[t.n];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int chunk = tid & 15;  // 8 consecutive dims: 8*chunk .. 8*chunk+7
   const int rg = tid >> 4;     // row group: rows rg, rg+16, ...
   const int row0 = b * BS;
   const int nb = min(BS, t.tok[sq + 1] - t.tok[sq] - row0);
-  const uint16_t* kb = K + ((size_t)g * T + t.tok[sq] + row0) * kHeadDim + chunk * 8;
+  const uint16_t* kb = K + g * kv_head + (int64_t)(t.tok[sq] + row0) * kv_tok + chunk * 8;
 
   uint4 raw[kRowsPerThread];
 #pragma unroll
   for (int k = 0; k < kRowsPerThread; ++k) {
     const int r = rg + 16 * k;
-    raw[k] = r < nb ? *reinterpret_cast<const uint4*>(kb + (size_t)r * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+    raw[k] = r < nb ? *reinterpret_cast<const uint4*>(kb + r * kv_tok) : make_uint4(0u, 0u, 0u, 0u);
   }
 
   // Column sums: own rows, then the four row groups of this wave, then waves.
@@ -254,7 +255,8 @@ __global__ __launch_bounds__(kStatsThreads) void stats_kernel(const uint16_t* __
 // log2(e)/sqrt(d) for the selector's MFMA.  Same layout and row mapping as
 // stats_kernel: one workgroup per (KV head, key block), 16 lanes per row.
 template <int BS>
-__global__ __launch_bounds__(kStatsThreads) void box_kernel(const uint16_t* __restrict__ K, int N, int M,
+__global__ __launch_bounds__(kStatsThreads) void box_kernel(const uint16_t* __restrict__ K, int64_t kv_head,
+                                                           int64_t kv_tok, int N, int M,
                                                            float* __restrict__ center, float* __restrict__ half,
                                                            _Float16* __restrict__ center16,
                                                            _Float16* __restrict__ half16, float sel_scale) {
@@ -266,7 +268,7 @@ __global__ __launch_bounds__(kStatsThreads) void box_kernel(const uint16_t* __re
   const int chunk = tid & 15, rg = tid >> 4;
   const int row0 = b * BS;
   const int nb = min(BS, N - row0);
-  const uint16_t* kb = K + ((size_t)g * N + row0) * kHeadDim + chunk * 8;
+  const uint16_t* kb = K + g * kv_head + (int64_t)row0 * kv_tok + chunk * 8;
   float lo[8], hi[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -278,7 +280,7 @@ __global__ __launch_bounds__(kStatsThreads) void box_kernel(const uint16_t* __re
     const int r = rg + 16 * k;
     if (r < nb) {
       float f[8];
-      unpack8(*reinterpret_cast<const uint4*>(kb + (size_t)r * kHeadDim), f);
+      unpack8(*reinterpret_cast<const uint4*>(kb + r * kv_tok), f);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         lo[e] = fminf(lo[e], f[e]);
@@ -367,13 +369,59 @@ __global__ __launch_bounds__(kStatsThreads) void quantile_kernel(const float* __
   }
 }
 
+// The select-ready summary from statistics computed elsewhere: one wave per
+// (KV head, block) converts the fp32 centroid (scaled by log2(e)/sqrt(d)) to
+// f16, the norm of the scaled centroid, and the uplift r_b beta_b
+// log2(e)/sqrt(d) -- the values stats_kernel and quantile_kernel write, from
+// the same fp32 inputs and with the same arithmetic.
+__global__ __launch_bounds__(256) void summarize_kernel(const float* __restrict__ centroids,
+                                                        const float* __restrict__ radii,
+                                                        const float* __restrict__ beta, int64_t n_rows,
+                                                        _Float16* __restrict__ cent16, float* __restrict__ uplift,
+                                                        float* __restrict__ cnorm, float sel_scale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (KV head, block), head-major
+  if (row >= n_rows) return;
+  // Lanes 0-15 each hold 8 consecutive dimensions, as in stats_kernel.
+  float n2 = 0.f;
+  if (lane < 16) {
+    const float4* src = reinterpret_cast<const float4*>(centroids + row * kHeadDim + lane * 8);
+    const float4 a = src[0], b = src[1];
+    const float c[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    f16x8 h;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      n2 = fmaf(c[e] * sel_scale, c[e] * sel_scale, n2);
+      h[e] = (_Float16)(c[e] * sel_scale);
+    }
+    *reinterpret_cast<f16x8*>(cent16 + row * kHeadDim + lane * 8) = h;
+  }
+  n2 += wave_xor_f(n2, 1);
+  n2 += wave_xor_f(n2, 2);
+  n2 += wave_xor_f(n2, 4);
+  n2 += wave_xor_f(n2, 8);
+  if (lane == 0) {
+    cnorm[row] = sqrtf(n2);
+    uplift[row] = radii[row] * beta[row] * sel_scale;
+  }
+}
+
+hipError_t launch_summarize(const float* centroids, const float* radii, const float* beta, int n_kv_heads,
+                            int n_blocks, _Float16* cent16, float* uplift, float* cnorm, hipStream_t s) {
+  const int64_t rows = (int64_t)n_kv_heads * n_blocks;
+  const float sel_scale = kLog2e / sqrtf((float)kHeadDim);
+  hipLaunchKernelGGL(summarize_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, centroids, radii, beta,
+                     rows, cent16, uplift, cnorm, sel_scale);
+  return hipGetLastError();
+}
+
 hipError_t launch_stats_varlen(const StatsArgs& a, const SeqTable& t, hipStream_t s) {
   const dim3 grid(t.blk[t.n], a.n_kv_heads);
   const float sel_scale = kLog2e / sqrtf((float)kHeadDim);
 #define RBS_STATS_CASE(BSZ)                                                                                 \
   case BSZ:                                                                                                 \
-    hipLaunchKernelGGL(stats_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, t, a.centroids, a.radii,    \
-                       a.cent16, a.cnorm, sel_scale);                                                       \
+    hipLaunchKernelGGL(stats_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, a.kv_head, a.kv_tok, t,     \
+                       a.centroids, a.radii, a.cent16, a.cnorm, sel_scale);                                 \
     break;
   switch (a.block_size) {
     RBS_STATS_CASE(64)
@@ -398,8 +446,8 @@ hipError_t launch_box(const BoxArgs& a, hipStream_t s) {
   const float sel_scale = kLog2e / sqrtf((float)kHeadDim);
 #define RBS_BOX_CASE(BSZ)                                                                                   \
   case BSZ:                                                                                                 \
-    hipLaunchKernelGGL(box_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, a.n_tokens, a.n_blocks,       \
-                       a.center, a.half, a.center16, a.half16, sel_scale);                                  \
+    hipLaunchKernelGGL(box_kernel<BSZ>, grid, dim3(kStatsThreads), 0, s, a.K, a.kv_head, a.kv_tok,          \
+                       a.n_tokens, a.n_blocks, a.center, a.half, a.center16, a.half16, sel_scale);          \
     break;
   switch (a.block_size) {
     RBS_BOX_CASE(64)

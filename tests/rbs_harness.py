@@ -68,6 +68,25 @@ def check_stats(st, C, R, beta, rq):
             "beta_abs": float(np.abs(Bg - beta).max())}
 
 
+def summary_parts(summary, n_kv_heads: int, n_blocks: int):
+    """The written parts of a select-ready summary (f16 scaled centroids, fp32
+    uplift, fp32 centroid norms; each part starts on a 256-byte boundary and
+    the padding between them is never written), as byte views."""
+    def up(x):
+        return (x + 255) // 256 * 256
+    n = n_kv_heads * n_blocks
+    c_end = n * 128 * 2
+    u_off = up(c_end)
+    n_off = up(u_off + 4 * n)
+    return summary[:c_end], summary[u_off:u_off + 4 * n], summary[n_off:n_off + 4 * n]
+
+
+def summaries_equal(a, b, n_kv_heads: int, n_blocks: int) -> bool:
+    import torch
+    return all(torch.equal(x, y) for x, y in zip(summary_parts(a, n_kv_heads, n_blocks),
+                                                 summary_parts(b, n_kv_heads, n_blocks)))
+
+
 def gpu_rows(counts, indices, rows):
     """{(h, i): sorted list} from device counts/indices for the given rows."""
     cnt = counts.cpu().numpy()

@@ -317,3 +317,122 @@ def test_binding_workspace_argument():
         L._workspace(torch.zeros(63, dtype=torch.int32), "cpu", 0)
     with pytest.raises(ValueError):
         L._workspace("cached", "cpu", 0)
+
+
+# ------------------------------------------------------------------ strides (rbs_shape)
+
+@pytest.mark.parametrize("strides,ok", [
+    ((0, 0, 0, 0), True),                                   # dense [H][N][d]
+    ((128, 4 * 128, 128, 2 * 128), True),                   # token-major [N][H][d] (H_q = 4, H_kv = 2)
+    ((128, 6 * 128, 128, 6 * 128), True),                   # token-major rows of a wider buffer
+    ((1024 * 256, 256, 1024 * 256, 256), True),             # head-major with padded rows
+    ((128, 128, 0, 0), False),                              # Q rows of different heads overlap
+    ((0, 64, 0, 0), False),                                 # token stride shorter than a row
+    ((0, 0, 1024 * 128 - 8, 128), False),                   # heads overlap
+    ((0, 132, 0, 0), False),                                # not a multiple of 8 elements
+    ((0, 0, 128, -256), False),                             # negative
+    ((0, 0, 0, (1 << 23) + 8), False),                      # token stride past the copy offsets
+])
+def test_stride_validation(strides, ok):
+    rbs, lib = _lib()
+    s = rbs.make_shape(1024, 4, 2, 64)
+    s.q_stride_head, s.q_stride_tok, s.kv_stride_head, s.kv_stride_tok = strides
+    # NULL counts: a shape that passes reaches the pointer checks (status 1)
+    # and launches nothing; a bad one stops at the shape (status 2).
+    want = 1 if ok else 2
+    assert lib.rbs_sparse_prefill(ctypes.byref(s), FAKE, FAKE, FAKE, None, FAKE, 0.0, FAKE, None, None, None) == want
+    assert lib.rbs_block_stats(ctypes.byref(s), None, ctypes.byref(_stats(rbs)), None) == want
+    assert (lib.rbs_summary_bytes(ctypes.byref(s)) > 0) == ok
+
+
+def test_stats_summarize_validation():
+    rbs, lib = _lib()
+    s = rbs.make_shape(1024, 4, 2, 64)
+    assert lib.rbs_stats_summarize(ctypes.byref(s), ctypes.byref(_stats(rbs, beta=None)), None) == 1
+    assert lib.rbs_stats_summarize(ctypes.byref(s), None, None) == 1
+    assert lib.rbs_stats_summarize(ctypes.byref(s), ctypes.byref(_stats(rbs, summary=MIS)), None) == 5
+    bad = rbs.make_shape(1024, 4, 2, 64)
+    bad.head_dim = 64
+    assert lib.rbs_stats_summarize(ctypes.byref(bad), ctypes.byref(_stats(rbs)), None) == 3
+
+
+# ------------------------------------------------------------------ binding argument checks
+# The Python binding checks dtype, sizes, layout and device of every tensor
+# before calling the library; a mismatch raises ValueError and reaches no
+# C call.  These run on CPU tensors: every check before the device check is
+# exercised with otherwise valid CPU tensors, the device check with a CPU
+# tensor that passes the others.
+
+def _cpu_inputs(n=256, hq=4, hkv=2, d=128):
+    import torch
+    bf = dict(dtype=torch.bfloat16)
+    return (torch.zeros(hq, n, d, **bf), torch.zeros(hkv, n, d, **bf), torch.zeros(hkv, n, d, **bf))
+
+
+def test_binding_rejects_bad_attention_arguments():
+    import torch
+    rbs, _ = _lib()
+    shape = rbs.make_shape(256, 4, 2, 64)
+    Q, K, V = _cpu_inputs()
+    M = rbs.n_blocks(shape)
+    counts = torch.zeros(4, M, dtype=torch.int32)
+    indices = torch.zeros(4, rbs.rbs_index_capacity(M), dtype=torch.int32)
+    cases = [
+        (dict(Q=Q.float()), "must be torch.bfloat16"),
+        (dict(Q=Q[:, :128]), "must have shape"),
+        (dict(K=K[:1]), "must have shape"),
+        (dict(V=V.transpose(0, 1).contiguous().transpose(0, 1)), "differ from K strides"),
+        (dict(Q=Q.transpose(1, 2).contiguous().transpose(1, 2)), "contiguous last dimension"),
+        (dict(counts=counts.long()), "must be torch.int32"),
+        (dict(counts=counts[:, :-1]), "must have shape"),
+        (dict(indices=indices[:, :-1]), "must have shape"),
+        (dict(indices=indices.t().contiguous().t()), "must be contiguous"),
+        (dict(O=torch.zeros(4, 256, 128, dtype=torch.float32)), "must be torch.bfloat16"),
+        (dict(lse=torch.zeros(4, 255, dtype=torch.float32)), "must have shape"),
+        (dict(), "must be on a GPU"),
+    ]
+    for override, msg in cases:
+        args = dict(Q=Q, K=K, V=V, counts=counts, indices=indices, O=None, lse=None)
+        args.update(override)
+        with pytest.raises(ValueError, match=msg):
+            rbs.rbs_sparse_prefill(shape, args["Q"], args["K"], args["V"], args["counts"], args["indices"],
+                                   O=args["O"], lse=args["lse"], workspace=None)
+
+
+def test_binding_rejects_bad_selection_and_stats_arguments():
+    import torch
+    rbs, _ = _lib()
+    shape = rbs.make_shape(256, 4, 2, 64)
+    Q, K, _ = _cpu_inputs()
+    with pytest.raises(ValueError, match="must be torch.bfloat16"):
+        rbs.rbs_block_stats(shape, K.half())
+    with pytest.raises(ValueError, match="must have shape"):
+        rbs.rbs_block_stats(shape, K[:, :64])
+    with pytest.raises(ValueError, match="must be on a GPU"):
+        rbs.rbs_block_stats(shape, K)
+    M = rbs.n_blocks(shape)
+    f32 = dict(dtype=torch.float32)
+    stats = rbs.BlockStats(shape, torch.zeros(2, M, 128, **f32), torch.zeros(2, M, **f32), torch.zeros(2, M, **f32),
+                           torch.zeros(2, 2, **f32), torch.zeros(rbs.rbs_summary_bytes(shape), dtype=torch.uint8))
+    bad = rbs.BlockStats(shape, stats.centroids, stats.radii, stats.beta, stats.quantiles, stats.summary[:-16])
+    with pytest.raises(ValueError, match="stats.summary must have shape"):
+        rbs.rbs_select(shape, Q, bad, 0.9, 0.9, 1, 1, 0)
+    with pytest.raises(ValueError, match="must be a BlockStats"):
+        rbs.rbs_select(shape, Q, object(), 0.9, 0.9, 1, 1, 0)
+    with pytest.raises(ValueError, match="Q must be on a GPU"):
+        rbs.rbs_select(shape, Q, stats, 0.9, 0.9, 1, 1, 0)
+    with pytest.raises(ValueError, match="stats.centroids must have shape"):
+        rbs.rbs_stats_summarize(shape, rbs.BlockStats(shape, stats.centroids[:1], stats.radii, stats.beta,
+                                                      stats.quantiles, stats.summary))
+
+
+def test_binding_strides_come_from_the_tensors():
+    rbs, _ = _lib()
+    shape = rbs.make_shape(256, 4, 2, 64)
+    tok_major = rbs._lib._with_strides(shape, q=(128, 512), kv=(128, 256))
+    assert (tok_major.q_stride_head, tok_major.q_stride_tok, tok_major.kv_stride_head,
+            tok_major.kv_stride_tok) == (128, 512, 128, 256)
+    assert shape.q_stride_tok == 0  # the caller's shape is not modified
+    shape.q_stride_tok = 384
+    with pytest.raises(ValueError, match="disagrees"):
+        rbs._lib._with_strides(shape, q=(128, 512))
