@@ -195,6 +195,22 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
                        const int32_t* counts, const int32_t* indices, float softmax_scale,
                        void* O, float* lse, void* workspace, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * persistent launch of rbs_sparse_prefill without a workspace argument.  Its
+ * queue counters live in a static array of the library (RBS_ATTN_WORKSPACE_BYTES
+ * per device, held until the process ends, looked up on the first call on
+ * each device); the call allocates nothing and frees nothing.  The counters do
+ * not grow with the problem, so every shape rbs_sparse_prefill accepts is
+ * accepted.  Arguments, results (bit-identical to rbs_sparse_prefill) and
+ * errors as rbs_sparse_prefill; the counters are reset by a kernel on
+ * `stream` at each call.  Every call on a device shares that device's
+ * counters: calls that overlap in time on one device (other streams, other
+ * threads) race and give wrong results; order them. */
+int rbs_sparse_prefill_noalloc(const rbs_shape* shape, const void* Q, const void* K, const void* V,
+                               const int32_t* counts, const int32_t* indices, float softmax_scale, void* O,
+                               float* lse, void* stream);
+
 /* rbs_select then rbs_sparse_prefill in one pass (Algorithm 1, selection loop
  * and attention; Sec. 3.2-3.3): each (query head, query block) selects its key
  * blocks and attends over them at once, the list kept on chip.  Arguments as

@@ -53,6 +53,7 @@ from ._lib import (  # noqa: F401
     rbs_select_attend,
     rbs_shape,
     rbs_sparse_prefill,
+    rbs_sparse_prefill_noalloc,
     rbs_stats,
     rbs_status_str,
     rbs_summary_bytes,

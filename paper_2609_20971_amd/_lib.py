@@ -97,6 +97,8 @@ def load() -> ctypes.CDLL:
     lib.rbs_attention_workspace_bytes.restype = SZ
     lib.rbs_sparse_prefill.argtypes = [SP, P, P, P, P, P, F32, P, P, P, P]
     lib.rbs_sparse_prefill.restype = ctypes.c_int
+    lib.rbs_sparse_prefill_noalloc.argtypes = [SP, P, P, P, P, P, F32, P, P, P]
+    lib.rbs_sparse_prefill_noalloc.restype = ctypes.c_int
     lib.rbs_select_attend.argtypes = [SP, P, P, P, ctypes.POINTER(rbs_stats), F32, F32, I32, I32, I32, F32, P, P, P,
                                       P, P, P]
     lib.rbs_select_attend.restype = ctypes.c_int
@@ -489,6 +491,23 @@ def rbs_sparse_prefill(shape: rbs_shape, Q, K, V, counts, indices, softmax_scale
     _check("rbs_sparse_prefill", load().rbs_sparse_prefill(ctypes.byref(sh), _ptr(Q), _ptr(K), _ptr(V),
                                                            _ptr(counts), _ptr(indices), float(softmax_scale),
                                                            _ptr(O), _ptr(lse), _ptr(ws), _stream(stream)))
+    return O
+
+
+def rbs_sparse_prefill_noalloc(shape: rbs_shape, Q, K, V, counts, indices, O, softmax_scale: float = 0.0,
+                               lse=None, stream=None):
+    """Stage 3 through the allocation-free entry point (the persistent launch
+    with the library's static queue counters): O and lse must be given."""
+    qs = _check_q(shape, Q)
+    kvs = _check_kv(shape, K, V)
+    _check_lists(shape, counts, indices)
+    _check_out(O, Q)
+    _check_lse(shape, lse)
+    _on_gpu(("Q", Q), ("K", K), ("V", V), ("counts", counts), ("indices", indices), ("O", O), ("lse", lse))
+    sh = _with_strides(shape, q=qs, kv=kvs)
+    _check("rbs_sparse_prefill_noalloc", load().rbs_sparse_prefill_noalloc(
+        ctypes.byref(sh), _ptr(Q), _ptr(K), _ptr(V), _ptr(counts), _ptr(indices), float(softmax_scale), _ptr(O),
+        _ptr(lse), _stream(stream)))
     return O
 
 

@@ -236,6 +236,37 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
   return from_hip(rbs::launch_attention(a, static_cast<hipStream_t>(stream)));
 }
 
+int rbs_sparse_prefill_noalloc(const rbs_shape* shape, const void* Q, const void* K, const void* V,
+                               const int32_t* counts, const int32_t* indices, float softmax_scale, void* O,
+                               float* lse, void* stream) {
+  int rc = check_shape(shape);
+  if (rc != RBS_OK) return rc;
+  if (Q == nullptr || K == nullptr || V == nullptr || counts == nullptr || indices == nullptr || O == nullptr)
+    return RBS_ERR_NULL;
+  if (!(softmax_scale == softmax_scale) || isinf(softmax_scale)) return RBS_ERR_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(counts) || !aligned16(indices) ||
+      !aligned16(O) || (lse != nullptr && !aligned16(lse)))
+    return RBS_ERR_ALIGN;
+  const int M = blocks_of(shape);
+  rbs::AttnArgs a;
+  a.Q = static_cast<const uint16_t*>(Q);
+  a.K = static_cast<const uint16_t*>(K);
+  a.V = static_cast<const uint16_t*>(V);
+  strides_of(shape, &a.st);
+  a.n_tokens = shape->n_tokens;
+  a.n_q_heads = shape->n_q_heads;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.block_size = shape->block_size;
+  a.n_blocks = M;
+  a.counts = counts;
+  a.indices = indices;
+  a.capacity = rbs_index_capacity(M);
+  a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
+  a.O = static_cast<uint16_t*>(O);
+  a.lse = lse;
+  return from_hip(rbs::launch_attention_noalloc(a, static_cast<hipStream_t>(stream)));
+}
+
 int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, const void* V, const rbs_stats* stats,
                       float tau_base, float tau_rescue, int32_t n_sink, int32_t n_local, int32_t n_recent,
                       float softmax_scale, int32_t* counts, int32_t* indices, void* O, float* lse, void* workspace,

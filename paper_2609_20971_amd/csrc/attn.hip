@@ -100,6 +100,39 @@ __global__ __launch_bounds__(BS * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   }
 }
 
+// Scratch of the allocation-free entry point (rbs_sparse_prefill_noalloc):
+// the kQueueInts queue counters of its persistent launch.  Each device holds
+// its own copy until the process ends; host code must use the address that
+// hipGetSymbolAddress returns for the current device, never the name.
+static __device__ __align__(256) int scratch[kQueueInts];
+
+namespace {
+int* g_scratch_of_device[kMaxDevices] = {};
+}  // namespace
+
+// The device address of this device's scratch, looked up once per device.
+hipError_t noalloc_scratch(int** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  int* p = __atomic_load_n(&g_scratch_of_device[dev], __ATOMIC_ACQUIRE);
+  if (p == nullptr) {
+    e = hipGetSymbolAddress(reinterpret_cast<void**>(&p), HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    __atomic_store_n(&g_scratch_of_device[dev], p, __ATOMIC_RELEASE);  // concurrent first calls store the same value
+  }
+  *out = p;
+  return hipSuccess;
+}
+
+hipError_t launch_attention_noalloc(AttnArgs a, hipStream_t s) {
+  hipError_t e = noalloc_scratch(&a.queue);
+  if (e != hipSuccess) return e;
+  return launch_attention(a, s);
+}
+
 __global__ void reset_queues_kernel(int* __restrict__ queue) {
   if (threadIdx.x < kQueueInts) queue[threadIdx.x] = 0;
 }

@@ -126,6 +126,9 @@ hipError_t launch_summarize(const float* centroids, const float* radii, const fl
 hipError_t launch_box(const BoxArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+// The persistent attention launch with its queue counters in the library's
+// per-device static scratch (a.queue is ignored): allocates nothing.
+hipError_t launch_attention_noalloc(AttnArgs a, hipStream_t s);
 hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStream_t s);
 size_t fused_smem_bytes(int block_size, int n_blocks);
 hipError_t launch_dense_indices(int n_q_heads, int n_blocks, int64_t capacity, int32_t* counts,
