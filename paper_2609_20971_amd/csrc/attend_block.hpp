@@ -117,6 +117,10 @@ __device__ __forceinline__ void issue_tile_full(const uint16_t* tile_base, uint3
 
 // Rescale threshold of the online softmax, in log2 units.
 constexpr float kRescaleSlack = 8.0f;
+// Fixed-reference pass: the largest denominator share a lane may reach (2^64)
+// for the pass's result to stand; past it (or on inf / NaN) the item is
+// computed again with the running maximum.
+constexpr float kFixedRefBound = 18446744073709551616.0f;
 
 // Arguments of one attention pass, shared by the stand-alone and the fused kernel.
 struct AttnCore {
@@ -181,12 +185,6 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
       issue_tile(base + b * tile_stride, nb, row_bytes, lds_base, wave, lane, is_v);
   };
 
-  float ms_run = -INFINITY;  // running reference maximum, log2 units
-  float l_run = 0.f;         // this lane's share of the softmax denominator
-  f32x16 o[4];
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
-
   // Per-lane LDS read bases.  K: row 32mt + l32 of the step, chunk 2ks + half.
   // V (transposed read): lane sources row 16c + 4 half + (lane%16)/4 (and +8),
   // dims 32dt + 16((lane/16)%2) + 4(lane%4); it receives dim 32dt + l32.
@@ -195,6 +193,24 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   const int vbyte = 8 * (lane & 1);
 
   const uint32_t k_base = lds_offset(k_lds), v_base = lds_offset(v_lds);
+
+  // Softmax reference.  The first pass fixes it at the row maximum of the
+  // first listed block (a sink block, usually, or the diagonal) and computes
+  // no maximum for the other blocks: exponentials of later, larger logits
+  // simply exceed 1.  The denominator shares bound every exponential, so when
+  // each stays within kFixedRefBound the pass's O and LSE stand (P keeps its
+  // relative precision at any magnitude, and O its range for |v| < 2^45).
+  // Otherwise every wave of the workgroup computes the item again with the
+  // running maximum of the online softmax (raised lazily: only when a block's
+  // maximum exceeds it by more than kRescaleSlack).
+  float ms_run, l_run;  // reference maximum (log2 units); this lane's share of the denominator
+  f32x16 o[4];
+  for (int pass = 0; pass < 2; ++pass) {
+  const bool exact = pass == 1;
+  ms_run = -INFINITY;
+  l_run = 0.f;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
   int kb = count > 0 ? min(max(list_at(0), 0), i) : 0;
   // The index of block n + 1 is read one iteration ahead so that its scalar
   // load is off the critical path.
@@ -255,25 +271,27 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
           }
         }
       }
-      float mx = -INFINITY;
+      if (exact || (n == 0 && sub == 0)) {
+        float mx = -INFINITY;
 #pragma unroll
-      for (int mt = 0; mt < KT; ++mt)
+        for (int mt = 0; mt < KT; ++mt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
-      mx = half_max(mx);
-      // Lazily raised reference maximum (log2 units): O and the denominator
-      // are rescaled only when some row's maximum exceeds the reference by
-      // more than kRescaleSlack, so the exponentials stay below 2^kRescaleSlack.
-      const float mxs = mx * scale_log2;
-      if (__any(mxs > ms_run + kRescaleSlack)) {
-        const float ms_new = fmaxf(ms_run, mxs);
-        const float alpha = ms_new == ms_run ? 1.f : fast_exp2(ms_run - ms_new);
-        ms_run = ms_new;
-        l_run *= alpha;
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mt][r]);
+        mx = half_max(mx);
+        // Lazily raised reference maximum (log2 units): O and the denominator
+        // are rescaled only when some row's maximum exceeds the reference by
+        // more than kRescaleSlack, so the exponentials stay below 2^kRescaleSlack.
+        const float mxs = mx * scale_log2;
+        if (__any(mxs > ms_run + kRescaleSlack)) {
+          const float ms_new = fmaxf(ms_run, mxs);
+          const float alpha = ms_new == ms_run ? 1.f : fast_exp2(ms_run - ms_new);
+          ms_run = ms_new;
+          l_run *= alpha;
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
+          for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+            for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+        }
       }
       const float shift = ms_run == -INFINITY ? 0.f : ms_run;
 #pragma unroll
@@ -319,6 +337,22 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
     if (has_next)
       copy_tile(vg, kb_next, v_base, true);
     kb = kb_next;
+  }
+  if (exact) break;
+  // Did any lane of the workgroup leave the fixed reference's range?  The
+  // tiles are free (the loop ended at a barrier): the first words of the K
+  // tile take one flag per wave.
+  {
+    int* flags = reinterpret_cast<int*>(k_lds);
+    const bool bad = __any(!(l_run <= kFixedRefBound));
+    if (lane == 0) flags[wave] = bad ? 1 : 0;
+    __syncthreads();
+    int any_bad = 0;
+#pragma unroll
+    for (int w = 0; w < BS / 32; ++w) any_bad |= flags[w];
+    __syncthreads();  // every wave has read the flags before the next pass copies tiles
+    if (!any_bad) break;
+  }
   }
 
   const float l_tot = l_run + wave_xor_f(l_run, 32);
