@@ -22,12 +22,19 @@
 // with wave ballots and a cross-wave prefix.
 #pragma once
 
+#include <type_traits>
+
 #include "rbs_device.hpp"
 #include "rbs_launch.hpp"
 
 namespace rbs {
 
 constexpr int kTile = 32;  // centroids per tile
+// Staged tile rows: 16 chunks of 8 f16 plus one chunk of padding, so that the
+// 16 lanes of an MFMA operand read (rows l, same chunk) hit distinct banks and
+// a lane's 8 reads differ only by immediate offsets.
+constexpr int kRowChunks = 17;
+constexpr int kTileBytes = kTile * kRowChunks * 16;
 // |exponent| bound for unshifted exp2 sums.  A block's sum adds at most 256
 // terms (8 waves of 32 tokens at B = 256), each below 2^(112 (1 + 2^-10)) --
 // the bound is tested with the fp32 centroid norm, and the f16-rounded
@@ -44,7 +51,14 @@ struct TilePass {
   static constexpr bool res = RES;
 };
 
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
+// Candidate blocks 0 .. n - 1 in order, 32 per tile (-1 past the end).
+struct AllBlocks {
+  int n;
+  __device__ __forceinline__ int operator()(int t, int r) const {
+    const int s = t * kTile + r;
+    return s < n ? s : -1;
+  }
+};
 
 // Selection policies: the method's dual-branch selector and the three
 // supporting selectors of the paper's selector comparison (Table
@@ -77,7 +91,7 @@ struct SelectCore {
 
 template <int BS, int MODE = kSelectDual>
 constexpr size_t select_smem_bytes(int M) {
-  return (MODE == kSelectBox ? 4 : 2) * kTile * 256 + 2 * (BS / 32) * kTile * 16 + BS * 4 + 2 * (size_t)M * 4 +
+  return (MODE == kSelectBox ? 4 : 2) * kTileBytes + 2 * (BS / 32) * kTile * 16 + BS * 4 + 2 * (size_t)M * 4 +
          3 * (BS / 32) * 4 + (MODE == kSelectBox ? 2 * (BS / 32) * 4 : 0) + (MODE == kSelectDual ? (size_t)M * 4 : 0);
 }
 
@@ -92,13 +106,13 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   constexpr int NT = NW * kWave;
   const uint16_t* __restrict__ Q = c.Q;
   const int N = c.N, M = c.M;
-  // Layout: cbuf[2][32 rows][16 chunks of 8 f16] (| hbuf[2][32][16], box) | stage[2][NW][32][4] | nq[BS] |
+  // Layout: cbuf[2][32 rows][17 chunks of 8 f16] (| hbuf[2][32][17], box) | stage[2][NW][32][4] | nq[BS] |
   // L_base[M] | L_res[M] | red_f[2 NW] | red_i[NW] (| cnt[2][NW], box) (| cand[M], dual)
   constexpr int kTileBufs = MODE == kSelectBox ? 4 : 2;
   f16x8* cbuf = reinterpret_cast<f16x8*>(smem_raw);
-  f16x8* hbuf = cbuf + 2 * kTile * 16;
-  float4* stage = reinterpret_cast<float4*>(smem_raw + kTileBufs * kTile * 256);
-  float* nq_s = reinterpret_cast<float*>(smem_raw + kTileBufs * kTile * 256 + 2 * NW * kTile * 16);
+  f16x8* hbuf = cbuf + 2 * kTile * kRowChunks;
+  float4* stage = reinterpret_cast<float4*>(smem_raw + kTileBufs * kTileBytes);
+  float* nq_s = reinterpret_cast<float*>(smem_raw + kTileBufs * kTileBytes + 2 * NW * kTile * 16);
   float* L_base = nq_s + BS;
   float* L_res = L_base + M;
   float* red_f = L_res + M;
@@ -188,10 +202,31 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   float u_next = 0.f;   // uplift (or radius) of this lane's centroid in the next tile
   float cn_next = 0.f;  // and the norm of its scaled centroid (dual)
 
-  auto run_pass = [&](int n_tiles_p, auto id_at, auto flags) __attribute__((always_inline)) {
+  // PARTIAL: the query block is shorter than B (a sequence's last block), so
+  // the rows of some wave must be masked; a workgroup-uniform choice, taken
+  // outside the tile loop.
+  auto run_pass = [&](int n_tiles_p, auto id_at, auto flags, auto partial) __attribute__((always_inline)) {
     constexpr bool BASE = decltype(flags)::base;
     constexpr bool RES = decltype(flags)::res;
+    constexpr bool PARTIAL = decltype(partial)::value;
+    constexpr bool LINEAR = std::is_same_v<decltype(id_at), AllBlocks>;
     auto fetch = [&](int tile) __attribute__((always_inline)) {
+      if (LINEAR && tile * kTile + kTile <= n_cand) {
+        // A full tile of consecutive blocks: one uniform base per tile and
+        // the lane's fixed offsets.
+        const _Float16* tg = cg + (size_t)tile * kTile * kHeadDim;
+#pragma unroll
+        for (int p = 0; p < kLdPasses; ++p) {
+          const int off = (ld_row + p * kLdRowsPerPass) * kHeadDim + 8 * ld_chunk;
+          pre[p] = *reinterpret_cast<const f16x8*>(tg + off);
+          if constexpr (MODE == kSelectBox)
+            preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)tile * kTile * kHeadDim + off);
+        }
+        const int lb = tile * kTile + l32;
+        if constexpr (kRescue) u_next = ug[lb];
+        if constexpr (MODE == kSelectDual) cn_next = cng[lb];
+        return;
+      }
 #pragma unroll
       for (int p = 0; p < kLdPasses; ++p) {
         const int bb = max(id_at(tile, ld_row + p * kLdRowsPerPass), 0);
@@ -208,8 +243,8 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       for (int p = 0; p < kLdPasses; ++p) {
         const int r = ld_row + p * kLdRowsPerPass;
         if (r < kTile) {
-          cbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = pre[p];
-          if constexpr (MODE == kSelectBox) hbuf[buf * kTile * 16 + r * 16 + swz(r, ld_chunk)] = preh[p];
+          cbuf[(buf * kTile + r) * kRowChunks + ld_chunk] = pre[p];
+          if constexpr (MODE == kSelectBox) hbuf[(buf * kTile + r) * kRowChunks + ld_chunk] = preh[p];
         }
       }
     };
@@ -235,19 +270,21 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       if constexpr (MODE == kSelectDual) plain_tile = __all(b < 0 || nq_row * (cn_cur + u_cur) <= kPlainBound);
       if (wave_active) {
         f32x16 acc = {};
-        const f16x8* cb = cbuf + buf * kTile * 16 + l32 * 16;
+        const f16x8* cb = cbuf + (buf * kTile + l32) * kRowChunks + half;
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qa[ks], cb[swz(l32, 2 * ks + half)], acc);
+        for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qa[ks], cb[2 * ks], acc);
         if constexpr (MODE == kSelectBox) {
           // + |q| . h_b: Eq. quest_box written as q . v_b + |q|^T h_b.
-          const f16x8* hb = hbuf + buf * kTile * 16 + l32 * 16;
+          const f16x8* hb = hbuf + (buf * kTile + l32) * kRowChunks + half;
 #pragma unroll
-          for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qabs[ks], hb[swz(l32, 2 * ks + half)], acc);
+          for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qabs[ks], hb[2 * ks], acc);
         }
-        if (wave_partial) {
+        if constexpr (PARTIAL) {
+          if (wave_partial) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (32 * wave + mfma_row(r, lane) >= nb) acc[r] = -INFINITY;
+            for (int r = 0; r < 16; ++r)
+              if (32 * wave + mfma_row(r, lane) >= nb) acc[r] = -INFINITY;
+          }
         }
         // Per lane (key block b) and branch, a (shift, sum of exp2) pair over
         // this wave's tokens: S_b = exp2(shift) * sum.
@@ -331,9 +368,13 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     __syncthreads();
   };
 
-  auto all_blocks = [&](int t, int r) __attribute__((always_inline)) {
-    const int s = t * kTile + r;
-    return s < n_cand ? s : -1;
+  const AllBlocks all_blocks{n_cand};
+  // run_pass with the partial-block masking compiled in only where needed.
+  auto tile_pass = [&](int n_tiles_p, auto id_at, auto flags) __attribute__((always_inline)) {
+    if (nb < BS)
+      run_pass(n_tiles_p, id_at, flags, std::true_type{});
+    else
+      run_pass(n_tiles_p, id_at, flags, std::false_type{});
   };
   if constexpr (MODE == kSelectDual) {
     // Base scores of every candidate first.  The rescue branch then scores only
@@ -344,7 +385,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     // U(b) < LB + log2 tau_rescue can be neither selected by the rescue branch
     // nor its maximum; a block with u_b = 0 has L_res(b) = L_base(b).  The
     // remaining blocks (a few percent) get their exact rescue scores.
-    run_pass(n_tiles, all_blocks, TilePass<true, false>{});
+    tile_pass(n_tiles, all_blocks, TilePass<true, false>{});
     int n_c = 0;
     if (c.rescue_all) {
       for (int b = tid; b < n_cand; b += NT) L_res[b] = L_base[b];  // every block passes: scores unused
@@ -384,16 +425,16 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         __syncthreads();
       }
     }
-    run_pass((n_c + kTile - 1) / kTile,
+    tile_pass((n_c + kTile - 1) / kTile,
              [&](int t, int r) __attribute__((always_inline)) {
                const int s = t * kTile + r;
                return s < n_c ? cand[s] : -1;
              },
              TilePass<false, true>{});
   } else if constexpr (MODE == kSelectFullL2) {
-    run_pass(n_tiles, all_blocks, TilePass<false, true>{});
+    tile_pass(n_tiles, all_blocks, TilePass<false, true>{});
   } else {
-    run_pass(n_tiles, all_blocks, TilePass<true, false>{});
+    tile_pass(n_tiles, all_blocks, TilePass<true, false>{});
   }
 
   // ---- Row maxima of both branches.
