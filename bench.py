@@ -42,6 +42,16 @@ def parse():
                    help="workload name (default: qwen3-30b-a3b-128k; the study defaults to qwen3-30b-a3b-32k)")
     p.add_argument("--dense-reps", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--flush-gib", type=float, default=1.0,
+                   help="also time the steps with a write of this many GiB of scratch between them, outside "
+                        "the timed events, so that no step finds the previous one's data in L2 or the Infinity "
+                        "Cache (0 skips)")
+    p.add_argument("--no-extra-configs", action="store_true",
+                   help="skip the compact lines for the other workloads (128K at B = 64 and 256, 32K, the "
+                        "64-head 64K layer)")
+    p.add_argument("--unit-rates", action="store_true",
+                   help="instead of the benchmark line: the measured issue rates of the exponential, FMA, LDS "
+                        "and matrix instructions (the unit-rate probe, built with the library)")
     p.add_argument("--cpu-select-rows", type=int, default=256,
                    help="sampled (head, query block) rows for the oracle's selection timing")
     p.add_argument("--cpu-attn-rows", type=int, default=24,
@@ -171,31 +181,44 @@ def algorithmic(w, counts_sum: int):
                 attn_flops=attn_flops, dense_flops=dense_flops, pairs=pairs)
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(w, inp, counts_np, indices_np, n_select: int, n_attn: int):
-    """Time the float64 oracle on a bounded sample of the same workload and
-    scale it to one layer (ms/layer)."""
+    """Time the float64 oracle on the host cores, on a bounded sample of the
+    same workload, scaled to one layer (ms/layer): block statistics and radius
+    quantiles over every KV head in full; selection and attention (on the GPU's
+    lists) on random (query head, query block) rows, each scaled to all rows.
+    NumPy's BLAS threads are set to the cores this process may run on."""
     import numpy as np
     import oracle
     from synth import f64_from_bf16_bits
+    cores = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        cores = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)
     except Exception:  # pragma: no cover
-        cores = 1
+        limiter = None
     M, B, G = w.n_blocks, w.block_size, w.group
     rng = np.random.default_rng(123)
     rows = [(int(rng.integers(w.n_q_heads)), int(rng.integers(M))) for _ in range(max(n_select, n_attn))]
 
     t0 = time.perf_counter()
-    Kf0 = f64_from_bf16_bits(inp["k"][:1])
-    C0, R0 = oracle.block_stats(Kf0, B)
-    oracle.rescue_coefficients(R0)
-    t_stats = (time.perf_counter() - t0) * w.n_kv_heads          # one KV head, scaled to all
-
-    Kf = [f64_from_bf16_bits(inp["k"][g]) for g in range(w.n_kv_heads)]
-    Vf = [f64_from_bf16_bits(inp["v"][g]) for g in range(w.n_kv_heads)]
-    C, R = oracle.block_stats(np.stack(Kf), B)
+    Kf = f64_from_bf16_bits(inp["k"])
+    C, R = oracle.block_stats(Kf, B)
     beta, _ = oracle.rescue_coefficients(R)
+    t_stats = time.perf_counter() - t0
+
+    Vf = f64_from_bf16_bits(inp["v"])
     t_sel = 0.0
     t_att = 0.0
     for k, (h, i) in enumerate(rows):
@@ -215,13 +238,16 @@ def cpu_baseline(w, inp, counts_np, indices_np, n_select: int, n_attn: int):
         t0 = time.perf_counter()
         oracle.attention_rows(qh, Kf[h // G], Vf[h // G], B, i, ids)
         t_att += time.perf_counter() - t0
+    if limiter is not None:
+        limiter.unregister()
     total_rows = w.n_q_heads * M
     ms = (t_stats + t_sel / n_select * total_rows + t_att / n_attn * total_rows) * 1e3
-    return {"value": ms, "unit": "ms/layer", "cores": int(cores), "kind": "oracle",
-            "sample": (f"float64 numpy oracle: block stats of 1 of {w.n_kv_heads} KV heads (x{w.n_kv_heads}); "
-                       f"selection for {n_select} and attention (on the GPU's lists) for {n_attn} random "
-                       f"(head, query block) rows of {total_rows}, each scaled to all rows"),
-            "measured_s": t_stats / w.n_kv_heads + t_sel + t_att}
+    return {"value": ms, "unit": "ms/layer", "cores": int(cores), "kind": "oracle", "cpu": _cpu_model(),
+            "sample": (f"float64 numpy oracle on {cores} host cores: block statistics and radius quantiles of "
+                       f"all {w.n_kv_heads} KV heads in full ({t_stats:.2f} s); selection for {n_select} and "
+                       f"attention (on the GPU's lists) for {n_attn} random (query head, query block) rows of "
+                       f"{total_rows}, each scaled to all rows ({t_sel:.2f} s, {t_att:.2f} s measured)"),
+            "measured_s": t_stats + t_sel + t_att}
 
 
 def main():
@@ -246,6 +272,9 @@ def main():
         return layer_sweep(args)
     if args.fp8:
         return fp8_bench(args)
+    if args.unit_rates:
+        print(json.dumps(unit_rates()), flush=True)
+        return
     w = workload(args.workload or "qwen3-30b-a3b-128k")
     _log(f"[bench] workload {w.name}: N={w.seq_len} Hq={w.n_q_heads} Hkv={w.n_kv_heads} B={w.block_size}")
     t0 = time.perf_counter()
@@ -300,6 +329,27 @@ def main():
     _log(f"[bench] timed {args.steps} steps: stats {stage_ms[0]:.3f} ms, select {stage_ms[1]:.3f} ms, "
          f"attention {stage_ms[2]:.3f} ms (wall {wall_ms:.3f} ms/step)")
 
+    # The same steps with the caches flushed between them: a scratch write,
+    # outside the events, larger than L2 plus the 256 MiB Infinity Cache.
+    flushed = None
+    if args.flush_gib > 0:
+        scratch = torch.empty(int(args.flush_gib * (1 << 30)), dtype=torch.uint8, device=dev)
+        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        for k in range(args.steps):
+            scratch.fill_(k & 0xFF)
+            step(fev[k])
+        torch.cuda.synchronize()
+        fms = np.zeros(3)
+        for ev in fev:
+            fms += [ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])]
+        fms /= args.steps
+        del scratch
+        flushed = {"flush_gib": args.flush_gib, "ms_per_step": round(float(fms.sum()), 4),
+                   "stats_ms": round(float(fms[0]), 4), "select_ms": round(float(fms[1]), 4),
+                   "attn_ms": round(float(fms[2]), 4)}
+        _log(f"[bench] with a {args.flush_gib} GiB write between steps: stats {fms[0]:.3f} ms, "
+             f"select {fms[1]:.3f} ms, attention {fms[2]:.3f} ms")
+
     # The fused entry point over the same steps (same results, one pass).
     fused_ms = None
     if args.fused_steps > 0:
@@ -333,6 +383,7 @@ def main():
         del Of, fcounts, findices
 
     counts_np = counts.cpu().numpy()
+    indices_np = indices.cpu().numpy()
     counts_sum = int(counts_np.sum())
     alg = algorithmic(w, counts_sum)
     density = counts_sum / alg["pairs"]
@@ -398,6 +449,7 @@ def main():
                      "causal_flops": causal_flops,
                      "exps": counts_sum * w.block_size * w.block_size},
         },
+        "flushed": flushed,
         "fused": ({"ms_per_step": round(sum(fused_ms), 4), "stats_ms": round(fused_ms[0], 4),
                    "select_attend_ms": round(fused_ms[1], 4), "steps": args.fused_steps}
                   if fused_ms else None),
@@ -411,12 +463,117 @@ def main():
         "copy_GBps": round(copy_gbps, 1),
     }
 
+    rates = unit_rates(brief=True)
+    if rates is not None:
+        result["unit_rates"] = rates
+
+    if not args.no_extra_configs:
+        del Q, K, V, O, stats, counts, indices
+        torch.cuda.empty_cache()
+        result["other_configs"] = {}
+        for name in EXTRA_CONFIGS:
+            result["other_configs"][name] = _config_line(rbs, torch, np, workload(name), dev)
+            _log(f"[bench] {name}: {result['other_configs'][name]}")
+
     if not args.no_cpu_baseline:
         _log(f"[bench] timing the CPU oracle on sampled rows")
-        cb = cpu_baseline(w, inp, counts_np, indices.cpu().numpy(), args.cpu_select_rows, args.cpu_attn_rows)
+        cb = cpu_baseline(w, inp, counts_np, indices_np, args.cpu_select_rows, args.cpu_attn_rows)
         _log(f"[bench] CPU oracle measured {cb.pop('measured_s'):.1f}s")
         result["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in cb.items()}
     print(json.dumps(result), flush=True)
+
+
+# The other workloads of the benchmark's configurations, one compact line
+# each: the 128K layer at 64- and 256-token blocks (the block-size
+# trade-off), the 32K layer and the 64-head 64K layer.
+EXTRA_CONFIGS = ("qwen3-30b-a3b-128k-b64", "qwen3-30b-a3b-128k-b256", "qwen3-30b-a3b-32k", "qwen3-32b-64k")
+
+
+def _config_line(rbs, torch, np, w, dev, steps: int = 3) -> dict:
+    """Stage times (HIP events, mean of `steps` after one warm-up step), the
+    attention's executed bf16 rate and the own-dense attention time of one
+    workload."""
+    from synth import make_inputs
+    inp = make_inputs(w)
+
+    def up(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    Q, K, V = up(inp["q"]), up(inp["k"]), up(inp["v"])
+    del inp
+    shape = rbs.make_shape(w.seq_len, w.n_q_heads, w.n_kv_heads, w.block_size)
+    stats = rbs.BlockStats.allocate(shape, dev)
+    counts, indices = rbs.allocate_lists(shape, dev)
+    O = torch.empty_like(Q)
+    stream = torch.cuda.current_stream()
+    ms = np.zeros(3)
+    for k in range(steps + 1):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        rbs.rbs_block_stats(shape, K, stats, stream=stream)
+        ev[1].record(stream)
+        rbs.rbs_select(shape, Q, stats, w.tau_base, w.tau_rescue, w.n_sink, w.n_local, w.n_recent, counts,
+                       indices, stream=stream)
+        ev[2].record(stream)
+        rbs.rbs_sparse_prefill(shape, Q, K, V, counts, indices, 0.0, O, stream=stream)
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        if k > 0:
+            ms += [ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])]
+    ms /= steps
+    counts_sum = int(counts.sum().item())
+    alg = algorithmic(w, counts_sum)
+    dense_ms = _time_dense(rbs, torch, np, shape, Q, K, V, stream, 1)
+    del Q, K, V, O, stats, counts, indices
+    torch.cuda.empty_cache()
+    attn_tflops = alg["attn_flops"] / (ms[2] * 1e-3) / 1e12
+    return {"ms_per_layer": round(float(ms.sum()), 4), "stats_ms": round(float(ms[0]), 4),
+            "select_ms": round(float(ms[1]), 4), "attn_ms": round(float(ms[2]), 4),
+            "density": round(counts_sum / alg["pairs"], 6),
+            "attn_mfma_frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+            "stats_hbm_frac": round(alg["stats_bytes"] / (ms[0] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+            "select_hbm_frac": round(alg["select_bytes"] / (ms[1] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+            "dense_attn_ms": round(dense_ms, 3), "speedup_vs_dense": round(dense_ms / float(ms.sum()), 3)}
+
+
+UNIT_RATES_BIN = os.path.join(ROOT, "paper_2609_20971_amd", "rbs_unit_rates")
+
+
+def unit_rates(brief: bool = False):
+    """Run the unit-rate probe (a separate program, built with the library)
+    and return its cases; brief: cycles per wave64 instruction of the
+    exponential, the FMA and the 32x32x16 bf16 matrix op alone, and the
+    matrix op's cycles with the attention's softmax mix beside it."""
+    import subprocess
+    if not os.path.exists(UNIT_RATES_BIN):
+        if brief:
+            return None
+        raise SystemExit(f"{UNIT_RATES_BIN} is missing: build with `python -m paper_2609_20971_amd.build`")
+    out = subprocess.run([UNIT_RATES_BIN], stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
+    if out.returncode != 0:
+        if brief:
+            return None
+        raise SystemExit(f"unit-rate probe failed: {out.stderr}")
+    data = json.loads(out.stdout)
+    if not brief:
+        return data
+
+    def cyc(other, n, w, same=True, mf=0):
+        for c in data["cases"]:
+            if (c["other"] == other and c["n_other"] == n and c["waves_per_simd"] == w and c["mfma"] == mf
+                    and c["acc"] == "vgpr" and (c["placement"] == "same_wave") == same):
+                return c
+        return None
+
+    ex, fm, mf = cyc("v_exp_f32", 8, 2), cyc("v_fma_f32", 8, 2), cyc("none", 0, 2, mf=8)
+    mix = cyc("softmax_mix", 28, 2, mf=8)
+    # Two waves per SIMD, each issuing 8 of the op (or 8 matrix ops) per loop
+    # iteration: one SIMD issues 16 per iteration of either wave.
+    per = lambda c: round(c["cycles_per_iter_mfma_wave"] / 16, 2) if c else None
+    return {"exp_cycles": per(ex), "fma_cycles": per(fm), "mfma_32x32x16_bf16_cycles": per(mf),
+            "mfma_cycles_with_softmax_mix": per(mix),
+            "note": "shader-clock cycles one SIMD spends per wave64 instruction, two waves per SIMD; "
+                    "the mix is 28 exp/fma/max/convert ops beside each 8 matrix ops in the same wave"}
 
 
 def _time_dense(rbs, torch, np, shape, Q, K, V, stream, reps: int) -> float:

@@ -72,6 +72,12 @@ def build(verbose: bool = False) -> str:
     if verbose and text.strip():
         print(text)
     os.replace(tmp, OUT)
+    # The unit-rate probe: a program of its own (bench.py --unit-rates), not
+    # part of the library.
+    probe = os.path.join(PKG, "rbs_unit_rates")
+    _run([HIPCC, *[f for f in FLAGS if f not in ("-fPIC",)], os.path.join(CSRC, "unit_rates.hip"), "-o",
+          probe + ".tmp"])
+    os.replace(probe + ".tmp", probe)
     return OUT
 
 

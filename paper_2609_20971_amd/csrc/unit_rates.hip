@@ -1,0 +1,283 @@
+// Issue rates of the gfx950 instruction classes the selection and attention
+// kernels are built from, measured rather than assumed: the exponential
+// (v_exp_f32), the FMA, max3, bf16 packing, the bf16 dot product, LDS reads
+// and the 32x32x16 bf16 matrix op, each alone, and the matrix op mixed with
+// the others either in the same wave or in another wave of the same SIMD.
+//
+// Each workgroup asks for 96 KiB of LDS so that a compute unit holds one; its
+// 4 W waves sit W per SIMD (the SIMD of each wave is recorded from HW_ID).
+// Each wave times its loop with s_memtime (shader clock cycles).  Per case the
+// host reports the median wave's cycles per loop iteration, for the waves that
+// issue the matrix ops and for the other waves separately, and the shader
+// clock implied by the cycles over the kernel's event time.
+//
+// Build: hipcc --offload-arch=gfx950 -O3 unit_rates.hip -o rbs_unit_rates
+// Output: one JSON object on stdout.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <vector>
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+
+constexpr int kLdsBytes = 96 * 1024;
+
+// Instruction kinds of the non-matrix part of a loop iteration.
+// kMix: the online-softmax mix of the attention kernel per matrix op, cycling
+// exp, fma, exp, fma, max3, cvt, dot2 (per 8 matrix ops: 8 exp, 8 fma, 4 max3,
+// 4 cvt, 4 dot2 when 28 ops are asked for).
+// kExpFma: exp and fma alternating (do the exponential and the FMA share a pipe?).
+enum Kind { kNone, kExp, kFma, kMax3, kCvt, kDot2, kLds, kMix, kExpFma };
+const char* kKindName[] = {"none", "v_exp_f32", "v_fma_f32", "v_max3_f32", "v_cvt_pk_bf16_f32",
+                           "v_dot2c_f32_bf16", "ds_read_b128", "softmax_mix", "exp_fma_alternating"};
+
+template <int KIND>
+__device__ __forceinline__ void other_op(float* a, int k, float b, float c, const uint32_t* la) {
+  if constexpr (KIND == kExp) asm volatile("v_exp_f32 %0, %0" : "+v"(a[k & 7]));
+  if constexpr (KIND == kFma) asm volatile("v_fma_f32 %0, %0, %1, %2" : "+v"(a[k & 7]) : "v"(b), "v"(c));
+  if constexpr (KIND == kMax3) asm volatile("v_max3_f32 %0, %0, %1, %2" : "+v"(a[k & 7]) : "v"(b), "v"(c));
+  if constexpr (KIND == kCvt) asm volatile("v_cvt_pk_bf16_f32 %0, %0, %1" : "+v"(a[k & 7]) : "v"(b));
+  if constexpr (KIND == kDot2) asm volatile("v_dot2c_f32_bf16 %0, %1, %2" : "+v"(a[k & 7]) : "v"(b), "v"(c));
+  if constexpr (KIND == kExpFma) {
+    if (k & 1) other_op<kFma>(a, k, b, c, la);
+    else other_op<kExp>(a, k, b, c, la);
+  }
+  if constexpr (KIND == kMix) {
+    switch (k % 7) {
+      case 0: case 2: other_op<kExp>(a, k, b, c, la); break;
+      case 1: case 3: other_op<kFma>(a, k, b, c, la); break;
+      case 4: other_op<kMax3>(a, k, b, c, la); break;
+      case 5: other_op<kCvt>(a, k, b, c, la); break;
+      default: other_op<kDot2>(a, k, b, c, la); break;
+    }
+  }
+  if constexpr (KIND == kLds) {
+    // Conflict-free 16-byte reads from precomputed addresses; the data are
+    // discarded (the iteration ends with a wait for every LDS read).
+    uint4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(la[k & 7]));
+  }
+}
+
+// End of an iteration: every LDS read of the iteration has returned.
+template <int KIND>
+__device__ __forceinline__ void iteration_end() {
+  if constexpr (KIND == kLds) asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
+// One matrix op: accumulator in ordinary VGPRs (the compiler's choice), or
+// pinned to the accumulation registers (AGPRs) with inline assembly.
+template <bool AGPR>
+__device__ __forceinline__ void mfma_op(f32x16& acc, const bf16x8& x, const bf16x8& y) {
+  if constexpr (AGPR)
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(x), "v"(y));
+  else
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, acc, 0, 0, 0);
+}
+
+// One loop iteration: MF matrix ops and NO ops of KIND.  SAME: both in every
+// wave, interleaved (NO / MF others after each matrix op); otherwise the
+// first half of the waves issue the matrix ops and the second half the others.
+template <int MF, int KIND, int NO, bool SAME, bool AGPR = false>
+__global__ __launch_bounds__(512) void rate_kernel(float* out, unsigned long long* cycles, unsigned* hwid,
+                                                   int iters) {
+  extern __shared__ uint4 lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nw = blockDim.x >> 6;
+  float a[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) a[k] = 0.001f * (float)(tid + k);
+  const float b = 1.0001f, c = 0.5f;
+  f32x16 acc[4] = {};
+  bf16x8 x, y;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    x[e] = (__bf16)(0.01f * (float)(lane + e));
+    y[e] = (__bf16)(0.02f * (float)(lane - e));
+  }
+  for (int k = tid; k < 4096; k += blockDim.x) lds[k] = make_uint4(k, k + 1, k + 2, k + 3);  // 64 KiB
+  uint32_t la[8];  // LDS byte addresses: lane-consecutive 16-byte words, 1 KiB apart per op, in [0, 64 KiB)
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    la[k] = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint4*)(lds + ((lane + 64 * (k + 8 * (wave & 7))) & 4095));
+  const bool mfma_wave = SAME || MF == 0 || wave < nw / 2;
+  const bool other_wave = SAME || MF == 0 || wave >= nw / 2;
+  __syncthreads();
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+  for (int it = 0; it < iters; ++it) {
+    if constexpr (SAME) {
+      constexpr int per = MF > 0 ? NO / MF : NO;
+      constexpr int rest = MF > 0 ? NO - per * MF : 0;
+#pragma unroll
+      for (int m = 0; m < (MF > 0 ? MF : 1); ++m) {
+        if constexpr (MF > 0) mfma_op<AGPR>(acc[m & 3], x, y);
+#pragma unroll
+        for (int k = 0; k < per; ++k) other_op<KIND>(a, m * per + k, b, c, la);
+      }
+#pragma unroll
+      for (int k = 0; k < rest; ++k) other_op<KIND>(a, k, b, c, la);
+      iteration_end<KIND>();
+    } else {
+      if (mfma_wave) {
+#pragma unroll
+        for (int m = 0; m < MF; ++m) mfma_op<AGPR>(acc[m & 3], x, y);
+      }
+      if (other_wave) {
+#pragma unroll
+        for (int k = 0; k < NO; ++k) other_op<KIND>(a, k, b, c, la);
+        iteration_end<KIND>();
+      }
+    }
+  }
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) s += a[k];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += acc[k][e];
+  out[blockIdx.x * blockDim.x + tid] = s;
+  if (lane == 0) {
+    const int slot = blockIdx.x * nw + wave;
+    cycles[slot] = t1 - t0;
+    hwid[slot] = __builtin_amdgcn_s_getreg((31 << 11) | (0 << 6) | 4);  // HW_ID, 32 bits
+  }
+}
+
+struct Result {
+  double cyc_mfma_wave;   // median cycles per iteration, waves that issue the matrix ops
+  double cyc_other_wave;  // the same for the waves that issue the other ops (split cases)
+  double sclk_mhz;
+  double ms;
+  int simd_of_wave[8];  // SIMD of each wave of the first workgroup
+};
+
+template <int MF, int KIND, int NO, bool SAME, bool AGPR>
+bool run_case(int waves_per_simd, int iters, int n_wg, Result* r) {
+  const int threads = 256 * waves_per_simd;
+  const int nw = threads / 64;
+  const size_t n_thr = (size_t)n_wg * threads, n_waves = (size_t)n_wg * nw;
+  float* out = nullptr;
+  unsigned long long* cyc = nullptr;
+  unsigned* hw = nullptr;
+  auto kern = rate_kernel<MF, KIND, NO, SAME, AGPR>;
+  if (hipMalloc(&out, n_thr * sizeof(float)) != hipSuccess) return false;
+  if (hipMalloc(&cyc, n_waves * sizeof(unsigned long long)) != hipSuccess) return false;
+  if (hipMalloc(&hw, n_waves * sizeof(unsigned)) != hipSuccess) return false;
+  if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes) != hipSuccess)
+    return false;
+  hipEvent_t e0, e1;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return false;
+  hipLaunchKernelGGL(kern, dim3(n_wg), dim3(threads), kLdsBytes, 0, out, cyc, hw, iters / 10);
+  (void)hipEventRecord(e0, 0);
+  hipLaunchKernelGGL(kern, dim3(n_wg), dim3(threads), kLdsBytes, 0, out, cyc, hw, iters);
+  (void)hipEventRecord(e1, 0);
+  if (hipEventSynchronize(e1) != hipSuccess) return false;
+  float ms = 0.f;
+  (void)hipEventElapsedTime(&ms, e0, e1);
+  std::vector<unsigned long long> c(n_waves);
+  std::vector<unsigned> h(n_waves);
+  if (hipMemcpy(c.data(), cyc, n_waves * sizeof(unsigned long long), hipMemcpyDeviceToHost) != hipSuccess) return false;
+  if (hipMemcpy(h.data(), hw, n_waves * sizeof(unsigned), hipMemcpyDeviceToHost) != hipSuccess) return false;
+  std::vector<unsigned long long> cm, co;
+  for (size_t k = 0; k < n_waves; ++k) {
+    const int w = (int)(k % nw);
+    const bool first_half = w < nw / 2;
+    if (SAME || MF == 0 || first_half) cm.push_back(c[k]);
+    if (!SAME && MF > 0 && !first_half) co.push_back(c[k]);
+  }
+  std::sort(cm.begin(), cm.end());
+  std::sort(co.begin(), co.end());
+  const double med = (double)cm[cm.size() / 2];
+  r->cyc_mfma_wave = med / iters;
+  r->cyc_other_wave = co.empty() ? 0.0 : (double)co[co.size() / 2] / iters;
+  r->sclk_mhz = med / (ms * 1e3);
+  r->ms = ms;
+  for (int w = 0; w < nw && w < 8; ++w) r->simd_of_wave[w] = (int)((h[w] >> 4) & 3);
+  (void)hipFree(out);
+  (void)hipFree(cyc);
+  (void)hipFree(hw);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  return true;
+}
+
+}  // namespace
+
+int main() {
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0) != hipSuccess || cus <= 0) {
+    fprintf(stderr, "no device\n");
+    return 1;
+  }
+  const int iters = 20000;
+  printf("{\"cus\": %d, \"iters\": %d, \"mfma_cycles_nominal\": 32, \"cases\": [", cus, iters);
+  bool first = true;
+  auto emit = [&](int mf, int kind, int no, bool same, bool agpr, int w, const Result& r) {
+    printf("%s\n  {\"mfma\": %d, \"acc\": \"%s\", \"other\": \"%s\", \"n_other\": %d, \"placement\": \"%s\", "
+           "\"waves_per_simd\": %d, "
+           "\"cycles_per_iter_mfma_wave\": %.2f, \"cycles_per_iter_other_wave\": %.2f, \"sclk_mhz\": %.0f, "
+           "\"ms\": %.3f, \"simd_of_wave\": [",
+           first ? "" : ",", mf, agpr ? "agpr" : "vgpr", kKindName[kind], no, same ? "same_wave" : "other_wave", w,
+           r.cyc_mfma_wave,
+           r.cyc_other_wave, r.sclk_mhz, r.ms);
+    for (int k = 0; k < 4 * w && k < 8; ++k) printf("%s%d", k ? ", " : "", r.simd_of_wave[k]);
+    printf("]}");
+    first = false;
+  };
+  Result r;
+#define RBS_RATE_ACC(MF, KIND, NO, SAME, W, AGPR)                                            \
+  if (!run_case<MF, KIND, NO, SAME, AGPR>(W, iters, cus, &r)) {                               \
+    fprintf(stderr, "case %d %d %d %d %d failed\n", MF, KIND, NO, (int)SAME, (int)AGPR);      \
+    return 1;                                                                                 \
+  }                                                                                           \
+  emit(MF, KIND, NO, SAME, AGPR, W, r);
+#define RBS_RATE(MF, KIND, NO, SAME, W) RBS_RATE_ACC(MF, KIND, NO, SAME, W, false)
+  // Each kind alone: 8 independent ops per iteration, 1 and 2 waves per SIMD.
+  RBS_RATE(0, kExp, 8, true, 1)
+  RBS_RATE(0, kExp, 8, true, 2)
+  RBS_RATE(0, kFma, 8, true, 2)
+  RBS_RATE(0, kMax3, 8, true, 2)
+  RBS_RATE(0, kCvt, 8, true, 2)
+  RBS_RATE(0, kDot2, 8, true, 2)
+  RBS_RATE(0, kLds, 8, true, 2)
+  RBS_RATE(0, kExpFma, 16, true, 2)
+  RBS_RATE(0, kExpFma, 16, true, 1)
+  // Matrix ops alone.
+  RBS_RATE(8, kNone, 0, true, 1)
+  RBS_RATE(8, kNone, 0, true, 2)
+  // Matrix ops with other ops in the same wave (one wave per SIMD).
+  RBS_RATE(8, kExp, 8, true, 1)
+  RBS_RATE(8, kExp, 16, true, 1)
+  RBS_RATE(8, kFma, 16, true, 1)
+  RBS_RATE(8, kFma, 32, true, 1)
+  RBS_RATE(8, kLds, 8, true, 1)
+  // Matrix ops in one wave, other ops in the other wave of the same SIMD.
+  RBS_RATE(8, kExp, 32, false, 2)
+  RBS_RATE(8, kFma, 64, false, 2)
+  RBS_RATE(8, kMax3, 48, false, 2)
+  RBS_RATE(8, kLds, 32, false, 2)
+  // Accumulators in AGPRs.
+  RBS_RATE_ACC(8, kNone, 0, true, 1, true)
+  RBS_RATE_ACC(8, kExp, 16, true, 1, true)
+  RBS_RATE_ACC(8, kFma, 32, true, 1, true)
+  RBS_RATE_ACC(8, kExp, 32, false, 2, true)
+  RBS_RATE_ACC(8, kFma, 64, false, 2, true)
+  // The attention's softmax mix per 8 matrix ops (28 ops), one and two such
+  // waves per SIMD, accumulators in VGPRs and in AGPRs.
+  RBS_RATE(8, kMix, 28, true, 1)
+  RBS_RATE(8, kMix, 28, true, 2)
+  RBS_RATE_ACC(8, kMix, 28, true, 1, true)
+  RBS_RATE_ACC(8, kMix, 28, true, 2, true)
+  RBS_RATE(8, kMix, 14, true, 2)
+  RBS_RATE_ACC(8, kMix, 14, true, 2, true)
+#undef RBS_RATE
+#undef RBS_RATE_ACC
+  printf("\n]}\n");
+  return 0;
+}

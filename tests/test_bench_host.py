@@ -44,3 +44,25 @@ def test_more_than_one_gpu_is_refused_with_a_message():
                        timeout=120)
     assert r.returncode != 0
     assert "one GPU" in (r.stdout + r.stderr) or "1 GPU" in (r.stdout + r.stderr)
+
+
+def test_cpu_baseline_covers_every_kv_head_and_states_its_sample():
+    """The CPU oracle timing: statistics of all KV heads in full, the stated
+    row samples, the cores this process may use, and the CPU model."""
+    import os
+    import oracle
+    from synth import f64_from_bf16_bits, make_inputs
+    w = WORKLOADS["tiny-2k"].with_(seq_len=512)
+    inp = make_inputs(w)
+    C, R = oracle.block_stats(f64_from_bf16_bits(inp["k"]), w.block_size)
+    M = w.n_blocks
+    counts = np.tile(np.arange(1, M + 1, dtype=np.int32), (w.n_q_heads, 1))
+    indices = np.zeros((w.n_q_heads, M * (M + 1) // 2), dtype=np.int32)
+    for i in range(M):
+        indices[:, i * (i + 1) // 2:i * (i + 1) // 2 + i + 1] = np.arange(i + 1)
+    cb = bench.cpu_baseline(w, inp, counts, indices, 4, 2)
+    assert cb["cores"] == len(os.sched_getaffinity(0))
+    assert cb["kind"] == "oracle" and cb["unit"] == "ms/layer" and cb["value"] > 0
+    assert f"all {w.n_kv_heads} KV heads in full" in cb["sample"]
+    assert "selection for 4" in cb["sample"] and "attention (on the GPU's lists) for 2" in cb["sample"]
+    assert cb["cpu"]
