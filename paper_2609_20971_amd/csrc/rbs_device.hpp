@@ -42,6 +42,32 @@ __device__ __forceinline__ float half_max(float x) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// x of the lane selected by the DPP control kCtrl (quad permutations and row
+// rotations only: every lane has a source).
+template <int kCtrl>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xf, 0xf, false));
+}
+
+// Maximum / minimum of x over the 64 lanes, in every lane, without an LDS
+// round trip: lane ^ 1 and lane ^ 2 within each quad, rotations by 4 and 8
+// within each row of 16, then gfx950's row-pair and half-wave lane swaps.
+// Exact (order-independent) for max and min.
+template <bool kMax>
+__device__ __forceinline__ float wave_extreme(float x) {
+  auto pick = [](float a, float b) __attribute__((always_inline)) { return kMax ? fmaxf(a, b) : fminf(a, b); };
+  x = pick(x, dpp_f<0xb1>(x));   // quad_perm [1, 0, 3, 2]
+  x = pick(x, dpp_f<0x4e>(x));   // quad_perm [2, 3, 0, 1]
+  x = pick(x, dpp_f<0x124>(x));  // row_ror 4
+  x = pick(x, dpp_f<0x128>(x));  // row_ror 8
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = pick(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return pick(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+}
+__device__ __forceinline__ float wave_max(float x) { return wave_extreme<true>(x); }
+__device__ __forceinline__ float wave_min(float x) { return wave_extreme<false>(x); }
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // 32x32x16 MFMA wrappers: D = A(32x16) B(16x32) + C.

@@ -89,10 +89,51 @@ struct SelectCore {
   int64_t capacity;
 };
 
+// Slots of the dual selector's rescue-candidate list: a quarter of the blocks
+// (at least two compaction chunks of NT blocks, at most M); more candidates are
+// scored in several chunks.
+constexpr int select_cand_cap(int M, int NT) {
+  const int quarter = (M / 4 + kTile - 1) / kTile * kTile;
+  const int cap = quarter > 2 * NT ? quarter : 2 * NT;
+  return cap < M ? cap : M;
+}
+
+// LDS layout of select_block (byte offsets):
+//   cbuf[bufs][32 rows][17 chunks of 8 f16] | stage[2][NW][32] float4 | nq[BS] | L[M] |
+//   red_f[3 NW] | red_i[NW] (| cnt[2][NW], box) (| flags[M] bytes | cand[cap], dual)
+template <int BS, int MODE>
+struct SelectLds {
+  static constexpr int NW = BS / 32;
+  static constexpr size_t tile_bufs = MODE == kSelectBox ? 4 : 2;
+  static constexpr size_t stage = tile_bufs * kTileBytes;
+  static constexpr size_t nq = stage + 2 * NW * kTile * 16;
+  static constexpr size_t L = nq + BS * 4;
+  static constexpr size_t red_f(int M) { return L + (size_t)M * 4; }
+  static constexpr size_t red_i(int M) { return red_f(M) + 3 * NW * 4; }
+  static constexpr size_t flags(int M) { return red_i(M) + (MODE == kSelectBox ? 3 : 1) * NW * 4; }
+  static constexpr size_t cand(int M) { return flags(M) + (((size_t)M + 3) & ~(size_t)3); }
+  static constexpr size_t bytes(int M) {
+    return MODE == kSelectDual ? cand(M) + (size_t)select_cand_cap(M, BS * 2) * 4 : flags(M);
+  }
+};
+
 template <int BS, int MODE = kSelectDual>
 constexpr size_t select_smem_bytes(int M) {
-  return (MODE == kSelectBox ? 4 : 2) * kTileBytes + 2 * (BS / 32) * kTile * 16 + BS * 4 + 2 * (size_t)M * 4 +
-         3 * (BS / 32) * 4 + (MODE == kSelectBox ? 2 * (BS / 32) * 4 : 0) + (MODE == kSelectDual ? (size_t)M * 4 : 0);
+  return SelectLds<BS, MODE>::bytes(M);
+}
+
+// Largest x over the workgroup, in every thread.  red: NW floats of LDS, not
+// read by any thread between the previous use of the same slots and this call
+// without a barrier in between.
+template <int NW>
+__device__ __forceinline__ float block_max(float x, float* red) {
+  x = wave_max(x);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  float m = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) m = fmaxf(m, red[w]);
+  return m;
 }
 
 // Selection of query block i of query head h by the B/32 waves of the calling
@@ -104,20 +145,23 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
                                             __attribute__((address_space(3))) int32_t* list_lds) {
   constexpr int NW = BS / 32;
   constexpr int NT = NW * kWave;
+  using Lds = SelectLds<BS, MODE>;
   const uint16_t* __restrict__ Q = c.Q;
   const int N = c.N, M = c.M;
-  // Layout: cbuf[2][32 rows][17 chunks of 8 f16] (| hbuf[2][32][17], box) | stage[2][NW][32][4] | nq[BS] |
-  // L_base[M] | L_res[M] | red_f[2 NW] | red_i[NW] (| cnt[2][NW], box) (| cand[M], dual)
-  constexpr int kTileBufs = MODE == kSelectBox ? 4 : 2;
   f16x8* cbuf = reinterpret_cast<f16x8*>(smem_raw);
   f16x8* hbuf = cbuf + 2 * kTile * kRowChunks;
-  float4* stage = reinterpret_cast<float4*>(smem_raw + kTileBufs * kTileBytes);
-  float* nq_s = reinterpret_cast<float*>(smem_raw + kTileBufs * kTileBytes + 2 * NW * kTile * 16);
-  float* L_base = nq_s + BS;
-  float* L_res = L_base + M;
-  float* red_f = L_res + M;
-  int* red_i = reinterpret_cast<int*>(red_f + 2 * NW);
-  int* cand = red_i + NW;  // dual: blocks whose rescue score is computed
+  float4* stage = reinterpret_cast<float4*>(smem_raw + Lds::stage);
+  float* nq_s = reinterpret_cast<float*>(smem_raw + Lds::nq);
+  // Block scores: the base branch's (centroid, box), the rescue branch's
+  // (full-L2); dual: the base scores, and after the rescue pass each rescue
+  // candidate's exact rescue score in place of its base score.
+  float* L = reinterpret_cast<float*>(smem_raw + Lds::L);
+  float* red_f = reinterpret_cast<float*>(smem_raw + Lds::red_f(M));
+  int* red_i = reinterpret_cast<int*>(smem_raw + Lds::red_i(M));
+  // Dual: per block, bit 0 = selected by the base branch, bit 1 = L[b] is its
+  // rescue score (no uplift, or a rescue candidate).
+  uint8_t* flags = smem_raw + Lds::flags(M);
+  int* cand = reinterpret_cast<int*>(smem_raw + Lds::cand(M));  // dual: rescue candidates to score
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
@@ -153,46 +197,54 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       }
     }
   }
-  sq += wave_xor_f(sq, 32);
+  // The largest centroid norm among the candidates (dual): bounds every base
+  // logit of the row.
+  float cn_max = 0.f;
+  if constexpr (MODE == kSelectDual) {
+    for (int b = tid; b < n_cand; b += NT) cn_max = fmaxf(cn_max, cng[b]);
+  }
+  sq = half_sum(sq);
   const float nq = sqrtf(sq);
   if (half == 0) nq_s[t_local] = nq;
-  float nq_max = row_ok ? nq : 0.f, nq_mn = row_ok ? nq : INFINITY;
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) {
-    nq_max = fmaxf(nq_max, wave_xor_f(nq_max, m));
-    nq_mn = fminf(nq_mn, wave_xor_f(nq_mn, m));
-  }
+  const float nq_max = wave_max(row_ok ? nq : 0.f), nq_mn = wave_min(row_ok ? nq : INFINITY);
+  if constexpr (MODE == kSelectDual) cn_max = wave_max(cn_max);
   const bool wave_active = 32 * wave < nb;
   const bool wave_partial = 32 * wave + 32 > nb;
 
-  // Largest and smallest |q| of the query block, and per element the token's
-  // |q| minus the largest (the rescue exponent offsets, <= 0).
+  // Largest and smallest |q| of the query block (and the largest candidate
+  // centroid norm).
   if (lane == 0) {
     red_f[wave] = nq_max;
     red_f[NW + wave] = nq_mn;
+    red_f[2 * NW + wave] = cn_max;
   }
   __syncthreads();
-  float nq_row = red_f[0], nq_min = red_f[NW];
+  float nq_row = red_f[0], nq_min = red_f[NW], cn_row = red_f[2 * NW];
 #pragma unroll
   for (int w = 1; w < NW; ++w) {
     nq_row = fmaxf(nq_row, red_f[w]);
     nq_min = fminf(nq_min, red_f[NW + w]);
+    cn_row = fmaxf(cn_row, red_f[2 * NW + w]);
   }
+  // Per element of the MFMA result, the token's |q| minus the largest (the
+  // rescue exponent offsets, <= 0); loaded where a rescue pass needs them.
   float nqd[16];
+  auto load_nqd = [&]() __attribute__((always_inline)) {
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int t = 32 * wave + mfma_row(r, lane);
-    nqd[r] = (t < nb) ? nq_s[t] - nq_row : 0.f;
-  }
+    for (int r = 0; r < 16; ++r) {
+      const int t = 32 * wave + mfma_row(r, lane);
+      nqd[r] = (t < nb) ? nq_s[t] - nq_row : 0.f;
+    }
+  };
 
   // ---- Tile passes.  A pass scores tiles of 32 key blocks staged through LDS
   // (double buffered, one barrier per tile); id_at(t, r) is the block of row r
-  // of tile t, or -1.  The flags choose the branches whose scores it merges
-  // into L_base / L_res.  Every load is issued without a branch (a padding row
-  // reads block 0; its lane's results are never used), so no loaded value is
-  // merged at a branch join, where the compiler would wait for all loads in
-  // flight.  Vector types, not uint4: a struct copied from memory stays a
-  // memcpy that keeps the array out of registers.
+  // of tile t, or -1.  The flags choose the branch whose scores it writes to
+  // L.  Every load is issued without a branch (a padding row reads block 0;
+  // its lane's results are never used), so no loaded value is merged at a
+  // branch join, where the compiler would wait for all loads in flight.
+  // Vector types, not uint4: a struct copied from memory stays a memcpy that
+  // keeps the array out of registers.
   const int ld_row = tid >> 4, ld_chunk = tid & 15;  // NT >= 128 threads: rows ld_row, ld_row + NT/16, ...
   constexpr int kLdRowsPerPass = NT / 16;
   constexpr int kLdPasses = (kTile + kLdRowsPerPass - 1) / kLdRowsPerPass;
@@ -202,51 +254,52 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   float u_next = 0.f;   // uplift (or radius) of this lane's centroid in the next tile
   float cn_next = 0.f;  // and the norm of its scaled centroid (dual)
 
+  // Centroid rows of a tile into registers: a full tile of consecutive blocks
+  // from one uniform base and the lane's fixed offsets; otherwise by block id.
+  auto fetch_rows = [&](int tile, auto id_at) __attribute__((always_inline)) {
+    constexpr bool LINEAR = std::is_same_v<decltype(id_at), AllBlocks>;
+    if (LINEAR && tile * kTile + kTile <= n_cand) {
+      const _Float16* tg = cg + (size_t)tile * kTile * kHeadDim;
+#pragma unroll
+      for (int p = 0; p < kLdPasses; ++p) {
+        const int off = (ld_row + p * kLdRowsPerPass) * kHeadDim + 8 * ld_chunk;
+        pre[p] = *reinterpret_cast<const f16x8*>(tg + off);
+        if constexpr (MODE == kSelectBox)
+          preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)tile * kTile * kHeadDim + off);
+      }
+      return;
+    }
+#pragma unroll
+    for (int p = 0; p < kLdPasses; ++p) {
+      const int bb = max(id_at(tile, ld_row + p * kLdRowsPerPass), 0);
+      pre[p] = *reinterpret_cast<const f16x8*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk);
+      if constexpr (MODE == kSelectBox)
+        preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)bb * kHeadDim + 8 * ld_chunk);
+    }
+  };
+  auto store = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int p = 0; p < kLdPasses; ++p) {
+      const int r = ld_row + p * kLdRowsPerPass;
+      if (r < kTile) {
+        cbuf[(buf * kTile + r) * kRowChunks + ld_chunk] = pre[p];
+        if constexpr (MODE == kSelectBox) hbuf[(buf * kTile + r) * kRowChunks + ld_chunk] = preh[p];
+      }
+    }
+  };
+
   // PARTIAL: the query block is shorter than B (a sequence's last block), so
   // the rows of some wave must be masked; a workgroup-uniform choice, taken
   // outside the tile loop.
-  auto run_pass = [&](int n_tiles_p, auto id_at, auto flags, auto partial) __attribute__((always_inline)) {
-    constexpr bool BASE = decltype(flags)::base;
-    constexpr bool RES = decltype(flags)::res;
+  auto run_pass = [&](int n_tiles_p, auto id_at, auto flags_t, auto partial) __attribute__((always_inline)) {
+    constexpr bool BASE = decltype(flags_t)::base;
+    constexpr bool RES = decltype(flags_t)::res;
     constexpr bool PARTIAL = decltype(partial)::value;
-    constexpr bool LINEAR = std::is_same_v<decltype(id_at), AllBlocks>;
     auto fetch = [&](int tile) __attribute__((always_inline)) {
-      if (LINEAR && tile * kTile + kTile <= n_cand) {
-        // A full tile of consecutive blocks: one uniform base per tile and
-        // the lane's fixed offsets.
-        const _Float16* tg = cg + (size_t)tile * kTile * kHeadDim;
-#pragma unroll
-        for (int p = 0; p < kLdPasses; ++p) {
-          const int off = (ld_row + p * kLdRowsPerPass) * kHeadDim + 8 * ld_chunk;
-          pre[p] = *reinterpret_cast<const f16x8*>(tg + off);
-          if constexpr (MODE == kSelectBox)
-            preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)tile * kTile * kHeadDim + off);
-        }
-        const int lb = tile * kTile + l32;
-        if constexpr (kRescue) u_next = ug[lb];
-        if constexpr (MODE == kSelectDual) cn_next = cng[lb];
-        return;
-      }
-#pragma unroll
-      for (int p = 0; p < kLdPasses; ++p) {
-        const int bb = max(id_at(tile, ld_row + p * kLdRowsPerPass), 0);
-        pre[p] = *reinterpret_cast<const f16x8*>(cg + (size_t)bb * kHeadDim + 8 * ld_chunk);
-        if constexpr (MODE == kSelectBox)
-          preh[p] = *reinterpret_cast<const f16x8*>(hg + (size_t)bb * kHeadDim + 8 * ld_chunk);
-      }
+      fetch_rows(tile, id_at);
       const int lb = max(id_at(tile, l32), 0);
       if constexpr (kRescue) u_next = ug[lb];
       if constexpr (MODE == kSelectDual) cn_next = cng[lb];
-    };
-    auto store = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-      for (int p = 0; p < kLdPasses; ++p) {
-        const int r = ld_row + p * kLdRowsPerPass;
-        if (r < kTile) {
-          cbuf[(buf * kTile + r) * kRowChunks + ld_chunk] = pre[p];
-          if constexpr (MODE == kSelectBox) hbuf[(buf * kTile + r) * kRowChunks + ld_chunk] = preh[p];
-        }
-      }
     };
     if (n_tiles_p == 0) {
       __syncthreads();  // a pass always ends at a barrier: its callers read LDS written before it
@@ -347,7 +400,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
           sum += half ? p.w : p.y;
         }
         const float4 p0 = stage[(buf * NW) * kTile + l32];  // wave 0 is always active
-        (half ? L_res : L_base)[b] = (half ? p0.z : p0.x) + log2f(sum);
+        L[b] = (half ? p0.z : p0.x) + log2f(sum);
       } else if (mine) {
         float top = -INFINITY;
 #pragma unroll
@@ -362,51 +415,116 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
           const float m = half ? p.z : p.x, sv = half ? p.w : p.y;
           if (sv > 0.f) sum += sv * fast_exp2(m - top);
         }
-        (half ? L_res : L_base)[b] = top + log2f(sum);
+        L[b] = top + log2f(sum);
+      }
+    }
+    __syncthreads();
+  };
+
+  // Base pass of the dual selector for a row whose every base logit is
+  // bounded, nq_row max_b |c'_b| <= kPlainBound (Cauchy-Schwarz, as above):
+  // the tiles' unshifted exp2 sums without the per-tile bound test and
+  // without the uplift loads; each wave writes one float per block, and one
+  // wave in turn adds a tile's sums and takes the log2.  A sum has a term of
+  // at least 2^-kPlainBound from wave 0, so the log2's input is normal.
+  auto lean_base_pass = [&](auto partial) __attribute__((always_inline)) {
+    constexpr bool PARTIAL = decltype(partial)::value;
+    float* st = reinterpret_cast<float*>(stage);  // [2][NW][kTile]
+    const AllBlocks all{n_cand};
+    fetch_rows(0, all);
+    store(0);
+    __syncthreads();
+    for (int tile = 0; tile < n_tiles; ++tile) {
+      const int buf = tile & 1;
+      if (tile + 1 < n_tiles) fetch_rows(tile + 1, all);
+      if (wave_active) {
+        const f16x8* cb = cbuf + (buf * kTile + l32) * kRowChunks + half;
+        f16x8 op[8];
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) op[ks] = cb[2 * ks];
+        f32x16 acc = {};
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qa[ks], op[ks], acc);
+        if constexpr (PARTIAL) {
+          if (wave_partial) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              if (32 * wave + mfma_row(r, lane) >= nb) acc[r] = -INFINITY;
+          }
+        }
+        float sb = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r]);
+        sb = half_sum(sb);
+        if (half == 0) st[(buf * NW + wave) * kTile + l32] = sb;
+      } else if (half == 0) {
+        st[(buf * NW + wave) * kTile + l32] = 0.f;
+      }
+      if (tile + 1 < n_tiles) store(buf ^ 1);
+      __syncthreads();
+      const int b = tile * kTile + l32;
+      if (wave == (tile & (NW - 1)) && half == 0 && b < n_cand) {
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) sum += st[(buf * NW + w) * kTile + l32];
+        L[b] = __builtin_amdgcn_logf(sum);
       }
     }
     __syncthreads();
   };
 
   const AllBlocks all_blocks{n_cand};
-  // run_pass with the partial-block masking compiled in only where needed.
-  auto tile_pass = [&](int n_tiles_p, auto id_at, auto flags) __attribute__((always_inline)) {
+  // The passes with the partial-block masking compiled in only where needed.
+  auto tile_pass = [&](int n_tiles_p, auto id_at, auto flags_t) __attribute__((always_inline)) {
     if (nb < BS)
-      run_pass(n_tiles_p, id_at, flags, std::true_type{});
+      run_pass(n_tiles_p, id_at, flags_t, std::true_type{});
     else
-      run_pass(n_tiles_p, id_at, flags, std::false_type{});
+      run_pass(n_tiles_p, id_at, flags_t, std::false_type{});
   };
+
+  float thr_base = -INFINITY, thr_res = -INFINITY;
+  float* red_m = red_f;  // NW slots for block_max (the prologue's reads are behind the passes' barriers)
   if constexpr (MODE == kSelectDual) {
-    // Base scores of every candidate first.  The rescue branch then scores only
-    // the blocks that can reach its threshold: every token's rescue logit lies
-    // between its base logit plus nq_min u_b and plus nq_row u_b, so
-    // L_res(b) <= U(b) = L_base(b) + nq_row u_b, and the row's largest rescue
-    // score is at least LB = max_b L_base(b) + nq_min u_b.  A block with
-    // U(b) < LB + log2 tau_rescue can be neither selected by the rescue branch
-    // nor its maximum; a block with u_b = 0 has L_res(b) = L_base(b).  The
-    // remaining blocks (a few percent) get their exact rescue scores.
-    tile_pass(n_tiles, all_blocks, TilePass<true, false>{});
-    int n_c = 0;
-    if (c.rescue_all) {
-      for (int b = tid; b < n_cand; b += NT) L_res[b] = L_base[b];  // every block passes: scores unused
+    // Base scores of every candidate first.
+    if (nq_row * cn_row <= kPlainBound) {
+      if (nb < BS)
+        lean_base_pass(std::true_type{});
+      else
+        lean_base_pass(std::false_type{});
     } else {
-      float lbv = -INFINITY;
-      for (int b = tid; b < n_cand; b += NT) lbv = fmaxf(lbv, L_base[b] + nq_min * ug[b]);
-#pragma unroll
-      for (int m = 1; m < 64; m <<= 1) lbv = fmaxf(lbv, wave_xor_f(lbv, m));
-      if (lane == 0) red_f[wave] = lbv;
-      __syncthreads();
-      float LB = red_f[0];
-#pragma unroll
-      for (int w = 1; w < NW; ++w) LB = fmaxf(LB, red_f[w]);
-      const float cut = LB + c.log2_tau_rescue - kCandSlack;
+      tile_pass(n_tiles, all_blocks, TilePass<true, false>{});
+    }
+    // The rescue branch then scores only the blocks that can reach its
+    // threshold: every token's rescue logit lies between its base logit plus
+    // nq_min u_b and plus nq_row u_b, so L_res(b) <= U(b) = L_base(b) + nq_row
+    // u_b, and the row's largest rescue score is at least LB = max_b L_base(b)
+    // + nq_min u_b.  A block with U(b) < LB + log2 tau_rescue can be neither
+    // selected by the rescue branch nor its maximum; a block with u_b = 0 has
+    // L_res(b) = L_base(b).  The remaining blocks (a few percent) get their
+    // exact rescue scores, in chunks of at most select_cand_cap candidates.
+    float mb = -INFINITY, lbv = -INFINITY;
+    for (int b = tid; b < n_cand; b += NT) {
+      const float lb = L[b];
+      mb = fmaxf(mb, lb);
+      lbv = fmaxf(lbv, lb + nq_min * ug[b]);
+    }
+    mb = block_max<NW>(mb, red_m);
+    lbv = block_max<NW>(lbv, red_m + NW);
+    thr_base = mb + c.log2_tau_base;
+    if (!c.rescue_all) {
+      load_nqd();
+      const int cap = select_cand_cap(M, NT);
+      const float cut = lbv + c.log2_tau_rescue - kCandSlack;
+      float mres = -INFINITY;  // over the blocks whose L[b] is already their rescue score
+      int n_c = 0;
       for (int base = 0; base < n_cand; base += NT) {
         const int b = base + tid;
         bool is_cand = false;
         if (b < n_cand) {
-          const float u = ug[b], lbase = L_base[b];
-          is_cand = u > 0.f && lbase + nq_row * u >= cut;
-          L_res[b] = u > 0.f ? -INFINITY : lbase;  // candidates get their exact score below
+          const float u = ug[b], lb = L[b];
+          is_cand = u > 0.f && lb + nq_row * u >= cut;
+          flags[b] = (uint8_t)((lb >= thr_base ? 1 : 0) | (u > 0.f ? (is_cand ? 2 : 0) : 2));
+          if (!(u > 0.f)) mres = fmaxf(mres, lb);
         }
         const uint64_t ballot = __ballot(is_cand);
         const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(ballot >> 32),
@@ -423,45 +541,32 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         if (is_cand) cand[off + before] = b;
         n_c += pass_total;
         __syncthreads();
+        if (n_c > 0 && (n_c + NT > cap || base + NT >= n_cand)) {
+          tile_pass((n_c + kTile - 1) / kTile,
+                    [&](int t, int r) __attribute__((always_inline)) {
+                      const int s = t * kTile + r;
+                      return s < n_c ? cand[s] : -1;
+                    },
+                    TilePass<false, true>{});
+          for (int s = tid; s < n_c; s += NT) mres = fmaxf(mres, L[cand[s]]);
+          __syncthreads();  // the list is read before the next chunk overwrites it
+          n_c = 0;
+        }
       }
+      thr_res = block_max<NW>(mres, red_m + 2 * NW) + c.log2_tau_rescue;
     }
-    tile_pass((n_c + kTile - 1) / kTile,
-             [&](int t, int r) __attribute__((always_inline)) {
-               const int s = t * kTile + r;
-               return s < n_c ? cand[s] : -1;
-             },
-             TilePass<false, true>{});
   } else if constexpr (MODE == kSelectFullL2) {
+    load_nqd();
     tile_pass(n_tiles, all_blocks, TilePass<false, true>{});
+    float m = -INFINITY;
+    for (int b = tid; b < n_cand; b += NT) m = fmaxf(m, L[b]);
+    thr_res = block_max<NW>(m, red_m) + c.log2_tau_rescue;
   } else {
     tile_pass(n_tiles, all_blocks, TilePass<true, false>{});
+    float m = -INFINITY;
+    for (int b = tid; b < n_cand; b += NT) m = fmaxf(m, L[b]);
+    thr_base = block_max<NW>(m, red_m) + c.log2_tau_base;
   }
-
-  // ---- Row maxima of both branches.
-  float mb = -INFINITY, mres = -INFINITY;
-  for (int b = tid; b < n_cand; b += NT) {
-    mb = fmaxf(mb, L_base[b]);
-    mres = fmaxf(mres, L_res[b]);
-  }
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) {
-    mb = fmaxf(mb, wave_xor_f(mb, m));
-    mres = fmaxf(mres, wave_xor_f(mres, m));
-  }
-  if (lane == 0) {
-    red_f[wave] = mb;
-    red_f[NW + wave] = mres;
-  }
-  __syncthreads();
-  mb = red_f[0];
-  mres = red_f[NW];
-#pragma unroll
-  for (int w = 1; w < NW; ++w) {
-    mb = fmaxf(mb, red_f[w]);
-    mres = fmaxf(mres, red_f[NW + w]);
-  }
-  const float thr_base = mb + c.log2_tau_base;
-  const float thr_res = mres + c.log2_tau_rescue;
   const bool recent_row = i >= M - c.n_recent;
 
   // ---- Box: fixed budget, the k = max(1, ceil(rho |C_i|)) highest scores
@@ -477,9 +582,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     const int k = max(1, min(n_cand, (int)ceil((double)c.budget * (double)n_cand - 1e-12)));
     int* cnt = red_i + NW;  // [2][NW]
     for (int bit = 31, it = 0; bit >= 0; --bit, ++it) {
-      const uint32_t cand = kth_key | (1u << bit);
+      const uint32_t cand_key = kth_key | (1u << bit);
       int mine = 0;
-      for (int b = tid; b < n_cand; b += NT) mine += okey(L_base[b]) >= cand ? 1 : 0;
+      for (int b = tid; b < n_cand; b += NT) mine += okey(L[b]) >= cand_key ? 1 : 0;
 #pragma unroll
       for (int m = 1; m < 64; m <<= 1) mine += __shfl_xor(mine, m, kWave);
       int* cb = cnt + (it & 1) * NW;
@@ -488,7 +593,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       int total = 0;
 #pragma unroll
       for (int w = 0; w < NW; ++w) total += cb[w];
-      if (total >= k) kth_key = cand;
+      if (total >= k) kth_key = cand_key;
     }
   }
 
@@ -500,14 +605,16 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     bool sel = false;
     if (b < n_cand) {
       const bool forced = recent_row || b < c.n_sink || b > i - c.n_local;
-      if constexpr (MODE == kSelectDual)
-        sel = forced || c.base_all || c.rescue_all || L_base[b] >= thr_base || L_res[b] >= thr_res;
-      else if constexpr (MODE == kSelectCentroid)
-        sel = forced || c.base_all || L_base[b] >= thr_base;
-      else if constexpr (MODE == kSelectFullL2)
-        sel = forced || c.rescue_all || L_res[b] >= thr_res;
-      else {
-        const uint32_t u = __float_as_uint(L_base[b]);
+      if constexpr (MODE == kSelectDual) {
+        // flags are written only when the rescue threshold is in use.
+        const int f = c.rescue_all ? 0 : flags[b];
+        sel = forced || c.base_all || c.rescue_all || (f & 1) || ((f & 2) && L[b] >= thr_res);
+      } else if constexpr (MODE == kSelectCentroid) {
+        sel = forced || c.base_all || L[b] >= thr_base;
+      } else if constexpr (MODE == kSelectFullL2) {
+        sel = forced || c.rescue_all || L[b] >= thr_res;
+      } else {
+        const uint32_t u = __float_as_uint(L[b]);
         sel = forced || ((u & 0x80000000u) ? ~u : (u | 0x80000000u)) >= kth_key;
       }
     }
@@ -519,9 +626,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     int off = total, pass_total = 0;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
-      const int c = red_i[w];
-      if (w < wave) off += c;
-      pass_total += c;
+      const int cw = red_i[w];
+      if (w < wave) off += cw;
+      pass_total += cw;
     }
     if (sel) {
       out[off + before] = b;
