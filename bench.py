@@ -321,10 +321,14 @@ def main():
             step(events[k])
         torch.cuda.synchronize()
         wall_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
-    stage_ms = np.zeros(3)
-    for ev in events:
-        stage_ms += [ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])]
-    stage_ms /= args.steps
+    per_step = np.array([[ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])]
+                         for ev in events])
+    stage_ms = per_step.mean(axis=0)
+    # Medians beside the means: the first timed step starts on an idle GPU
+    # (the loop begins after a synchronize), so its first stage also holds the
+    # host's time to issue it; the later steps are queued behind the previous
+    # step's attention.
+    stage_med = np.median(per_step, axis=0)
     ms_per_step = float(stage_ms.sum())
     _log(f"[bench] timed {args.steps} steps: stats {stage_ms[0]:.3f} ms, select {stage_ms[1]:.3f} ms, "
          f"attention {stage_ms[2]:.3f} ms (wall {wall_ms:.3f} ms/step)")
@@ -438,13 +442,17 @@ def main():
         "dense_mfma_util_pct": round(100.0 * dense_tflops / PEAK_BF16_TFLOPS, 2) if dense_ms else None,
         "wall_ms_per_step": round(wall_ms, 4),
         "stages": {
-            "stats": {"ms": round(float(stage_ms[0]), 4), "alg_bytes": alg["stats_bytes"],
-                      "GBps": round(stats_gbps, 1), "hbm_frac": round(stats_gbps / PEAK_HBM_GBPS, 4)},
-            "select": {"ms": round(float(stage_ms[1]), 4), "alg_bytes": alg["select_bytes"],
+            "stats": {"ms": round(float(stage_ms[0]), 4), "median_ms": round(float(stage_med[0]), 4),
+                      "alg_bytes": alg["stats_bytes"],
+                      "GBps": round(stats_gbps, 1), "hbm_frac": round(stats_gbps / PEAK_HBM_GBPS, 4),
+                      "hbm_frac_median": round(alg["stats_bytes"] / (stage_med[0] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)},
+            "select": {"ms": round(float(stage_ms[1]), 4), "median_ms": round(float(stage_med[1]), 4),
+                       "alg_bytes": alg["select_bytes"],
                        "GBps": round(select_gbps, 1), "hbm_frac": round(select_gbps / PEAK_HBM_GBPS, 4),
                        "alg_flops": alg["select_flops"], "TFLOPs": round(select_tflops, 1),
                        "mfma_frac": round(select_tflops / PEAK_BF16_TFLOPS, 4)},
-            "attn": {"ms": round(float(stage_ms[2]), 4), "alg_flops": alg["attn_flops"],
+            "attn": {"ms": round(float(stage_ms[2]), 4), "median_ms": round(float(stage_med[2]), 4),
+                     "alg_flops": alg["attn_flops"],
                      "TFLOPs": round(attn_tflops, 1), "executed_pairs": counts_sum,
                      "causal_flops": causal_flops,
                      "exps": counts_sum * w.block_size * w.block_size},
