@@ -37,15 +37,23 @@
  *     query and key blocks use the same B, one of 64, 128, 256.
  *     Limits: 1 <= N <= 262144, M <= 4096.
  *   - The caller owns and allocates every buffer.  The library allocates
- *     nothing, never synchronises, and enqueues its kernels on `stream`
- *     (a hipStream_t; NULL means the default stream).  Results are valid once
- *     the stream reaches them.
+ *     nothing, never synchronises (outside debug mode, below), and enqueues
+ *     its kernels on `stream` (a hipStream_t; NULL means the default stream).
+ *     Results are valid once the stream reaches them.
  *   - Every device pointer must be 16-byte aligned.
  *   - Arguments are validated on the host before anything is launched; a
  *     failing call returns a status code, launches nothing and writes nothing.
  *     RBS_ERR_HIP means a launch was rejected by the runtime.
- *   - The library keeps no state between calls; calls on distinct streams are
- *     independent.
+ *   - The library keeps no state between calls (apart from the debug switch
+ *     and rbs_sparse_prefill_noalloc's counters); calls on distinct streams
+ *     are independent.
+ *   - Debug mode (rbs_set_debug, or RBS_DEBUG set to anything but "0" in the
+ *     environment when the library first looks): every call synchronises its
+ *     stream after its launches and returns RBS_ERR_HIP if a kernel failed,
+ *     and the selection calls first scan Q: the selector takes Q in f16, so an
+ *     element beyond +-65504 (or not finite) returns RBS_ERR_RANGE with
+ *     nothing else launched.  Outside debug mode such a Q gives unspecified
+ *     lists.  For development, not for graph capture.
  */
 #ifndef RBS_H
 #define RBS_H
@@ -64,7 +72,8 @@ enum {
   RBS_ERR_UNSUPPORTED = 3, /* head_dim != 128 or block size not 64/128/256    */
   RBS_ERR_ARG = 4,         /* tau outside [0,1], negative or zero window, ... */
   RBS_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned         */
-  RBS_ERR_HIP = 6          /* the HIP runtime rejected a kernel launch        */
+  RBS_ERR_HIP = 6,         /* the HIP runtime rejected a kernel launch        */
+  RBS_ERR_RANGE = 7        /* debug mode: a Q element outside the f16 range   */
 };
 
 typedef struct {
@@ -361,6 +370,10 @@ int rbs_dense_indices_varlen(const rbs_shape* shape, const rbs_batch* batch, int
 
 /* Static description of a status code. */
 const char* rbs_status_str(int status);
+
+/* Debug mode on (nonzero) or off; returns the previous setting.  Process-wide,
+ * for every device; see the notes at the top of this file. */
+int rbs_set_debug(int on);
 
 #ifdef __cplusplus
 }

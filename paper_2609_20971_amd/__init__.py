@@ -55,7 +55,9 @@ from ._lib import (  # noqa: F401
     rbs_sparse_prefill,
     rbs_sparse_prefill_noalloc,
     rbs_stats,
+    rbs_set_debug,
     rbs_status_str,
     rbs_summary_bytes,
     LIB_PATH,
+    RBS_ERR_RANGE,
 )

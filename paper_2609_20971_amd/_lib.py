@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 # comparing builds); the default is the in-tree one.
 LIB_PATH = os.environ.get("RBS_LIB_PATH") or os.path.join(_HERE, "librbs.so")
 
-RBS_OK, RBS_ERR_NULL, RBS_ERR_SHAPE, RBS_ERR_UNSUPPORTED, RBS_ERR_ARG, RBS_ERR_ALIGN, RBS_ERR_HIP = range(7)
+RBS_OK, RBS_ERR_NULL, RBS_ERR_SHAPE, RBS_ERR_UNSUPPORTED, RBS_ERR_ARG, RBS_ERR_ALIGN, RBS_ERR_HIP, RBS_ERR_RANGE = range(8)
 
 
 class RbsError(RuntimeError):
@@ -136,12 +136,22 @@ def load() -> ctypes.CDLL:
     lib.rbs_dense_indices_varlen.restype = ctypes.c_int
     lib.rbs_status_str.argtypes = [ctypes.c_int]
     lib.rbs_status_str.restype = ctypes.c_char_p
+    lib.rbs_set_debug.argtypes = [ctypes.c_int]
+    lib.rbs_set_debug.restype = ctypes.c_int
     _lib = lib
     return lib
 
 
 def rbs_status_str(status: int) -> str:
     return load().rbs_status_str(status).decode()
+
+
+def rbs_set_debug(on: bool) -> bool:
+    """Debug mode on or off (process-wide); returns the previous setting.  In
+    debug mode every call drains its stream and reports kernel failures, and
+    the selection calls reject a Q the selector's f16 operands cannot hold
+    (RBS_ERR_RANGE) before launching anything else."""
+    return bool(load().rbs_set_debug(1 if on else 0))
 
 
 def _check(fn: str, status: int):

@@ -3,6 +3,10 @@
 // rejected call launches and writes nothing.
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <atomic>
 
 #include "../../include/rbs.h"
 #include "rbs_launch.hpp"
@@ -66,6 +70,66 @@ int check_stats_ptrs(const rbs_stats* st) {
 }
 
 int from_hip(hipError_t e) { return e == hipSuccess ? RBS_OK : RBS_ERR_HIP; }
+
+// ---- Debug mode: synchronise after every call, and scan Q before selection.
+std::atomic<int> g_debug{-1};  // -1: the environment not read yet
+
+bool debug_on() {
+  int d = g_debug.load(std::memory_order_relaxed);
+  if (d < 0) {
+    const char* e = getenv("RBS_DEBUG");
+    int fresh = (e != nullptr && e[0] != '\0' && strcmp(e, "0") != 0) ? 1 : 0;
+    int expected = -1;
+    g_debug.compare_exchange_strong(expected, fresh);
+    d = g_debug.load(std::memory_order_relaxed);
+  }
+  return d > 0;
+}
+
+// The status of a call whose launches returned e: in debug mode the stream is
+// drained and any kernel failure reported.
+int finish(hipError_t e, void* stream) {
+  if (e != hipSuccess) return RBS_ERR_HIP;
+  if (!debug_on()) return RBS_OK;
+  if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return RBS_ERR_HIP;
+  return hipGetLastError() == hipSuccess ? RBS_OK : RBS_ERR_HIP;
+}
+
+__device__ unsigned int g_q_range_flag;
+
+// One thread per 16-byte chunk of Q ([H][N][128] through the strides): sets
+// the flag if a bf16 element's magnitude is 65536 or more (bits & 0x7fff >=
+// 0x4780: beyond f16's 65504, infinities and NaNs included).
+__global__ __launch_bounds__(256) void q_range_kernel(const uint16_t* __restrict__ Q, int64_t head, int64_t tok,
+                                                      int N, int64_t chunks) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= chunks) return;
+  const int64_t row = c >> 4;
+  const int64_t h = row / N, t = row - h * N;
+  const uint4 v = *reinterpret_cast<const uint4*>(Q + h * head + t * tok + 8 * (c & 15));
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  bool bad = false;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) bad |= (w[k] & 0x7fffu) >= 0x4780u || ((w[k] >> 16) & 0x7fffu) >= 0x4780u;
+  if (bad) atomicOr(&g_q_range_flag, 1u);
+}
+
+// Debug mode only: RBS_ERR_RANGE if Q holds an element the selector's f16
+// operands cannot represent.
+int check_q_range(const void* Q, int64_t head, int64_t tok, int H, int N, void* stream) {
+  if (!debug_on()) return RBS_OK;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const unsigned int zero = 0u;
+  if (hipStreamSynchronize(s) != hipSuccess) return RBS_ERR_HIP;
+  if (hipMemcpyToSymbol(HIP_SYMBOL(g_q_range_flag), &zero, sizeof zero) != hipSuccess) return RBS_ERR_HIP;
+  const int64_t chunks = (int64_t)H * N * 16;
+  hipLaunchKernelGGL(q_range_kernel, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(Q), head, tok, N, chunks);
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) return RBS_ERR_HIP;
+  unsigned int flag = 0u;
+  if (hipMemcpyFromSymbol(&flag, HIP_SYMBOL(g_q_range_flag), sizeof flag) != hipSuccess) return RBS_ERR_HIP;
+  return flag != 0u ? RBS_ERR_RANGE : RBS_OK;
+}
 
 // Shape rules of a batch (the per-sequence limits are the single-sequence
 // ones), and its sequence table.  T = shape->n_tokens must equal the sum.
@@ -145,7 +209,7 @@ int rbs_block_stats(const rbs_shape* shape, const void* K, const rbs_stats* stat
                                       rbs::summary_uplift_offset(shape->n_kv_heads, M));
   a.cnorm = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
                                      rbs::summary_cnorm_offset(shape->n_kv_heads, M));
-  return from_hip(rbs::launch_stats(a, static_cast<hipStream_t>(stream)));
+  return finish(rbs::launch_stats(a, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_stats_summarize(const rbs_shape* shape, const rbs_stats* stats, void* stream) {
@@ -159,11 +223,11 @@ int rbs_stats_summarize(const rbs_shape* shape, const rbs_stats* stats, void* st
     return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
   unsigned char* sum = static_cast<unsigned char*>(stats->summary);
-  return from_hip(rbs::launch_summarize(
+  return finish(rbs::launch_summarize(
       stats->centroids, stats->radii, stats->beta, shape->n_kv_heads, M, reinterpret_cast<_Float16*>(sum),
       reinterpret_cast<float*>(sum + rbs::summary_uplift_offset(shape->n_kv_heads, M)),
       reinterpret_cast<float*>(sum + rbs::summary_cnorm_offset(shape->n_kv_heads, M)),
-      static_cast<hipStream_t>(stream)));
+      static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats, float tau_base, float tau_rescue,
@@ -201,7 +265,9 @@ int rbs_select(const rbs_shape* shape, const void* Q, const rbs_stats* stats, fl
   a.counts = counts;
   a.indices = indices;
   a.capacity = rbs_index_capacity(M);
-  return from_hip(rbs::launch_select(a, static_cast<hipStream_t>(stream)));
+  rc = check_q_range(Q, st.q_head, st.q_tok, shape->n_q_heads, shape->n_tokens, stream);
+  if (rc != RBS_OK) return rc;
+  return finish(rbs::launch_select(a, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, const void* V, const int32_t* counts,
@@ -233,7 +299,7 @@ int rbs_sparse_prefill(const rbs_shape* shape, const void* Q, const void* K, con
   a.O = static_cast<uint16_t*>(O);
   a.lse = lse;
   a.queue = static_cast<int*>(workspace);
-  return from_hip(rbs::launch_attention(a, static_cast<hipStream_t>(stream)));
+  return finish(rbs::launch_attention(a, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_sparse_prefill_noalloc(const rbs_shape* shape, const void* Q, const void* K, const void* V,
@@ -264,7 +330,7 @@ int rbs_sparse_prefill_noalloc(const rbs_shape* shape, const void* Q, const void
   a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   a.O = static_cast<uint16_t*>(O);
   a.lse = lse;
-  return from_hip(rbs::launch_attention_noalloc(a, static_cast<hipStream_t>(stream)));
+  return finish(rbs::launch_attention_noalloc(a, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, const void* V, const rbs_stats* stats,
@@ -325,7 +391,9 @@ int rbs_select_attend(const rbs_shape* shape, const void* Q, const void* K, cons
   aa.O = static_cast<uint16_t*>(O);
   aa.lse = lse;
   aa.queue = static_cast<int*>(workspace);
-  return from_hip(rbs::launch_select_attend(sa, aa, static_cast<hipStream_t>(stream)));
+  rc = check_q_range(Q, st.q_head, st.q_tok, shape->n_q_heads, shape->n_tokens, stream);
+  if (rc != RBS_OK) return rc;
+  return finish(rbs::launch_select_attend(sa, aa, static_cast<hipStream_t>(stream)), stream);
 }
 
 size_t rbs_box_summary_bytes(const rbs_shape* shape) {
@@ -356,7 +424,7 @@ int rbs_block_box(const rbs_shape* shape, const void* K, const rbs_box* box, voi
   a.center16 = static_cast<_Float16*>(box->summary);
   a.half16 = reinterpret_cast<_Float16*>(static_cast<unsigned char*>(box->summary) +
                                          box_half_offset(shape->n_kv_heads, M));
-  return from_hip(rbs::launch_box(a, static_cast<hipStream_t>(stream)));
+  return finish(rbs::launch_box(a, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_select_variant(const rbs_shape* shape, const void* Q, const rbs_stats* stats, const rbs_box* box,
@@ -412,7 +480,9 @@ int rbs_select_variant(const rbs_shape* shape, const void* Q, const rbs_stats* s
   a.counts = counts;
   a.indices = indices;
   a.capacity = rbs_index_capacity(M);
-  return from_hip(rbs::launch_select(a, static_cast<hipStream_t>(stream)));
+  rc = check_q_range(Q, st.q_head, st.q_tok, shape->n_q_heads, shape->n_tokens, stream);
+  if (rc != RBS_OK) return rc;
+  return finish(rbs::launch_select(a, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices, void* stream) {
@@ -421,8 +491,8 @@ int rbs_dense_indices(const rbs_shape* shape, int32_t* counts, int32_t* indices,
   if (counts == nullptr || indices == nullptr) return RBS_ERR_NULL;
   if (!aligned16(counts) || !aligned16(indices)) return RBS_ERR_ALIGN;
   const int M = blocks_of(shape);
-  return from_hip(rbs::launch_dense_indices(shape->n_q_heads, M, rbs_index_capacity(M), counts, indices,
-                                            static_cast<hipStream_t>(stream)));
+  return finish(rbs::launch_dense_indices(shape->n_q_heads, M, rbs_index_capacity(M), counts, indices,
+                                            static_cast<hipStream_t>(stream)), stream);
 }
 
 int32_t rbs_varlen_blocks(const rbs_shape* shape, const rbs_batch* batch) {
@@ -469,7 +539,7 @@ int rbs_block_stats_varlen(const rbs_shape* shape, const rbs_batch* batch, const
                                       rbs::summary_uplift_offset(shape->n_kv_heads, M));
   a.cnorm = reinterpret_cast<float*>(static_cast<unsigned char*>(stats->summary) +
                                      rbs::summary_cnorm_offset(shape->n_kv_heads, M));
-  return from_hip(rbs::launch_stats_varlen(a, t, static_cast<hipStream_t>(stream)));
+  return finish(rbs::launch_stats_varlen(a, t, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_select_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* Q, const rbs_stats* stats,
@@ -508,7 +578,9 @@ int rbs_select_varlen(const rbs_shape* shape, const rbs_batch* batch, const void
   a.counts = counts;
   a.indices = indices;
   a.capacity = t.cap[t.n];
-  return from_hip(rbs::launch_select_varlen(a, t, static_cast<hipStream_t>(stream)));
+  rc = check_q_range(Q, st.q_head, st.q_tok, shape->n_q_heads, shape->n_tokens, stream);
+  if (rc != RBS_OK) return rc;
+  return finish(rbs::launch_select_varlen(a, t, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, const void* Q, const void* K,
@@ -540,7 +612,7 @@ int rbs_sparse_prefill_varlen(const rbs_shape* shape, const rbs_batch* batch, co
   a.O = static_cast<uint16_t*>(O);
   a.lse = lse;
   a.queue = static_cast<int*>(workspace);
-  return from_hip(rbs::launch_attention_varlen(a, t, static_cast<hipStream_t>(stream)));
+  return finish(rbs::launch_attention_varlen(a, t, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_dense_indices_varlen(const rbs_shape* shape, const rbs_batch* batch, int32_t* counts, int32_t* indices,
@@ -550,8 +622,8 @@ int rbs_dense_indices_varlen(const rbs_shape* shape, const rbs_batch* batch, int
   if (rc != RBS_OK) return rc;
   if (counts == nullptr || indices == nullptr) return RBS_ERR_NULL;
   if (!aligned16(counts) || !aligned16(indices)) return RBS_ERR_ALIGN;
-  return from_hip(
-      rbs::launch_dense_indices_varlen(shape->n_q_heads, t, counts, indices, static_cast<hipStream_t>(stream)));
+  return finish(
+      rbs::launch_dense_indices_varlen(shape->n_q_heads, t, counts, indices, static_cast<hipStream_t>(stream)), stream);
 }
 
 size_t rbs_fp8_vt_bytes(const rbs_shape* shape) {
@@ -566,9 +638,9 @@ int rbs_fp8_amax(const rbs_shape* shape, const void* Q, const void* K, const voi
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(amax)) return RBS_ERR_ALIGN;
   rbs::Strides st;
   strides_of(shape, &st);
-  return from_hip(rbs::launch_fp8_amax(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
+  return finish(rbs::launch_fp8_amax(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
                                        static_cast<const uint16_t*>(V), st, shape->n_tokens, shape->n_q_heads,
-                                       shape->n_kv_heads, amax, static_cast<hipStream_t>(stream)));
+                                       shape->n_kv_heads, amax, static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const void* V, const float* amax, void* Q8,
@@ -583,12 +655,12 @@ int rbs_fp8_pack(const rbs_shape* shape, const void* Q, const void* K, const voi
     return RBS_ERR_ALIGN;
   rbs::Strides st;
   strides_of(shape, &st);
-  return from_hip(rbs::launch_fp8_pack(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
+  return finish(rbs::launch_fp8_pack(static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
                                        static_cast<const uint16_t*>(V), st, shape->n_tokens, shape->n_q_heads,
                                        shape->n_kv_heads, shape->block_size, blocks_of(shape), amax,
                                        static_cast<uint8_t*>(Q8),
                                        static_cast<uint8_t*>(K8), static_cast<uint8_t*>(V8t),
-                                       static_cast<hipStream_t>(stream)));
+                                       static_cast<hipStream_t>(stream)), stream);
 }
 
 int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K8, const void* V8t,
@@ -608,11 +680,11 @@ int rbs_sparse_prefill_fp8(const rbs_shape* shape, const void* Q8, const void* K
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   rbs::Strides st;
   strides_of(shape, &st);
-  return from_hip(rbs::launch_attention_fp8(
+  return finish(rbs::launch_attention_fp8(
       static_cast<const uint8_t*>(Q8), static_cast<const uint8_t*>(K8), static_cast<const uint8_t*>(V8t), amax,
       shape->n_tokens, shape->n_q_heads, shape->n_kv_heads, shape->block_size, M, counts, indices,
       rbs_index_capacity(M), scale, static_cast<uint16_t*>(O), st.q_head, st.q_tok, lse,
-      static_cast<int*>(workspace), static_cast<hipStream_t>(stream)));
+      static_cast<int*>(workspace), static_cast<hipStream_t>(stream)), stream);
 }
 
 const char* rbs_status_str(int status) {
@@ -623,9 +695,16 @@ const char* rbs_status_str(int status) {
     case RBS_ERR_UNSUPPORTED: return "unsupported head_dim or block_size (need d = 128, B in {64, 128, 256})";
     case RBS_ERR_ARG: return "invalid argument (threshold outside [0, 1], window < 1, bad scale)";
     case RBS_ERR_ALIGN: return "device pointer not 16-byte aligned";
-    case RBS_ERR_HIP: return "HIP runtime rejected a kernel launch";
+    case RBS_ERR_HIP: return "HIP runtime rejected a kernel launch (in debug mode: or a kernel failed)";
+    case RBS_ERR_RANGE: return "a query element is beyond the selector's f16 range (+-65504) or not finite";
     default: return "unknown status";
   }
+}
+
+int rbs_set_debug(int on) {
+  const int prev = debug_on() ? 1 : 0;
+  g_debug.store(on != 0 ? 1 : 0, std::memory_order_relaxed);
+  return prev;
 }
 
 }  // extern "C"

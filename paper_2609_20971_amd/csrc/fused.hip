@@ -70,41 +70,43 @@ size_t fused_smem_bytes(int block_size, int n_blocks) {
   }
 }
 
+// The persistent form only at B = 128: at B = 64 and 256 it spills registers
+// and the per-item launch is faster (128K layer: 6.4 vs 6.9 ms, 105.6 vs 176.3
+// ms), so only select_attend_queue_kernel<128> is instantiated.
+template <int BS>
+static hipError_t launch_select_attend_bs(const SelectCore& sc, const AttnCore& ac, int total, size_t smem,
+                                          int* queue, hipStream_t s) {
+  if constexpr (BS == 128) {
+    if (queue != nullptr) {
+      hipError_t e = hipFuncSetAttribute((const void*)select_attend_queue_kernel<BS>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      if (e != hipSuccess) return e;
+      int grid = 0;
+      e = resident_grid<select_attend_queue_kernel<BS>>(BS * 2, total, &grid, smem);
+      if (e == hipSuccess) e = reset_queues(queue, s);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(select_attend_queue_kernel<BS>, dim3(grid), dim3(BS * 2), smem, s, sc, ac, total, queue);
+      return hipGetLastError();
+    }
+  }
+  hipError_t e = hipFuncSetAttribute((const void*)select_attend_kernel<BS>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(select_attend_kernel<BS>, dim3(total), dim3(BS * 2), smem, s, sc, ac);
+  return hipGetLastError();
+}
+
 hipError_t launch_select_attend(const SelectArgs& sa, const AttnArgs& aa, hipStream_t s) {
   const int total = sa.n_blocks * sa.n_q_heads;
   const SelectCore sc = make_select_core(sa);
   const AttnCore ac = make_attn_core(aa);
   const size_t smem = fused_smem_bytes(sa.block_size, sa.n_blocks);
-  int grid = 0;
-  // The persistent form only at B = 128: at B = 64 and 256 it spills registers
-  // and the per-item launch is faster (128K layer: 6.4 vs 6.9 ms, 105.6 vs 176.3 ms).
-#define RBS_FUSED_CASE(BSZ)                                                                                   \
-  case BSZ: {                                                                                                 \
-    if (aa.queue == nullptr || BSZ != 128) {                                                                  \
-      hipError_t e = hipFuncSetAttribute((const void*)select_attend_kernel<BSZ>,                              \
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);              \
-      if (e != hipSuccess) return e;                                                                          \
-      hipLaunchKernelGGL(select_attend_kernel<BSZ>, dim3(total), dim3(BSZ * 2), smem, s, sc, ac);             \
-    } else {                                                                                                  \
-      hipError_t e = hipFuncSetAttribute((const void*)select_attend_queue_kernel<BSZ>,                        \
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);              \
-      if (e != hipSuccess) return e;                                                                          \
-      e = resident_grid<select_attend_queue_kernel<BSZ>>(BSZ * 2, total, &grid, smem);                        \
-      if (e == hipSuccess) e = reset_queues(aa.queue, s);                                                     \
-      if (e != hipSuccess) return e;                                                                          \
-      hipLaunchKernelGGL(select_attend_queue_kernel<BSZ>, dim3(grid), dim3(BSZ * 2), smem, s, sc, ac, total,  \
-                         aa.queue);                                                                           \
-    }                                                                                                         \
-    break;                                                                                                    \
-  }
   switch (sa.block_size) {
-    RBS_FUSED_CASE(64)
-    RBS_FUSED_CASE(128)
-    RBS_FUSED_CASE(256)
+    case 64: return launch_select_attend_bs<64>(sc, ac, total, smem, aa.queue, s);
+    case 128: return launch_select_attend_bs<128>(sc, ac, total, smem, aa.queue, s);
+    case 256: return launch_select_attend_bs<256>(sc, ac, total, smem, aa.queue, s);
     default: return hipErrorInvalidValue;
   }
-#undef RBS_FUSED_CASE
-  return hipGetLastError();
 }
 
 }  // namespace rbs

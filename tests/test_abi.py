@@ -40,9 +40,27 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings():
     rbs, _ = _lib()
-    for code in range(7):
-        assert rbs.rbs_status_str(code)
+    for code in range(8):
+        assert rbs.rbs_status_str(code) != "unknown status"
     assert rbs.rbs_status_str(99) == "unknown status"
+
+
+def test_debug_switch_is_host_state_and_validation_still_comes_first():
+    """rbs_set_debug only flips a flag (no HIP call) and returns the previous
+    setting; in debug mode a rejected call still launches nothing."""
+    rbs, lib = _lib()
+    prev = rbs.rbs_set_debug(True)
+    try:
+        assert rbs.rbs_set_debug(True) is True
+        s = rbs.make_shape(1024, 4, 2, 64)
+        st = _stats(rbs)
+        assert lib.rbs_select(ctypes.byref(s), None, ctypes.byref(st), 0.9, 0.9, 1, 1, 0, FAKE, FAKE, None) == 1
+        assert lib.rbs_select(ctypes.byref(s), FAKE, ctypes.byref(st), 1.5, 0.9, 1, 1, 0, FAKE, FAKE, None) == 4
+        assert _fused(lib, s, st, Q=MIS) == 5
+        assert rbs.rbs_set_debug(False) is True
+        assert rbs.rbs_set_debug(False) is False
+    finally:
+        rbs.rbs_set_debug(prev)
 
 
 def test_capacity_and_summary_sizes():

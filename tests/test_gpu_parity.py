@@ -224,8 +224,9 @@ def test_qwen3_30b_128k_sampled():
     import torch
     import paper_2609_20971_amd as rbs
     w = WORKLOADS["qwen3-30b-a3b-128k"]
-    rows = H.sample_rows(w.n_q_heads, w.n_blocks, 24, seed=2, include=[(5, 1023), (31, 700), (0, 3)])
-    r, _ = _full_check(w, select_rows=rows, attn_rows=rows[:10])
+    rows = H.sample_rows(w.n_q_heads, w.n_blocks, 96, seed=2, include=[(5, 1023), (31, 700), (0, 3)])
+    attn = H.sample_rows(w.n_q_heads, w.n_blocks, 12, seed=7, include=[(5, 1023), (31, 700), (0, 3)])
+    r, _ = _full_check(w, select_rows=rows, attn_rows=attn)
     # The benchmark's (persistent) launch against one workgroup per (head,
     # query block) on the same lists: every output bit identical.
     lse = torch.empty_like(r["lse"])
