@@ -164,6 +164,29 @@ def test_mixed_shifted_and_unshifted_tiles():
     _full_check(w, inputs=inp, attn_rows=attn)
 
 
+def test_unshifted_sums_at_the_bound_b256():
+    """B = 256 (a block's sum adds eight waves' partial sums), every query
+    aligned with the longest select-ready centroid and scaled so that
+    |q| max_b |c'_b| sits just under the unshifted-sum bound (112, log2
+    units): the block of that centroid sums 256 terms near 2^108 each, which
+    must stay finite; the attention's fixed softmax reference (the sink
+    block's maximum) is exceeded far past its range, so it takes the exact
+    pass."""
+    from synth import bf16_bits_from_f32, f64_from_bf16_bits
+    w = WORKLOADS["tiny-2k"].with_(name="bound", seq_len=2048, block_size=256, n_q_heads=2, n_kv_heads=1,
+                                   needles_per_kv_head=2, seed=33)
+    inp = make_inputs(w)
+    K = f64_from_bf16_bits(inp["k"])[0]
+    cent = K.reshape(w.n_blocks, w.block_size, -1).mean(axis=1) * (np.log2(np.e) / np.sqrt(w.head_dim))
+    norms = np.linalg.norm(cent, axis=1)
+    b_star = int(np.argmax(norms))
+    q = cent[b_star] / norms[b_star] * (108.0 / norms[b_star])
+    inp["q"] = np.ascontiguousarray(np.broadcast_to(bf16_bits_from_f32(q.astype(np.float32)), inp["q"].shape))
+    _say(f"[parity] bound case: block {b_star}, |q| max|c'| = {np.linalg.norm(q) * norms[b_star]:.2f}")
+    M = w.n_blocks
+    _full_check(w, inputs=inp, attn_rows=H.sample_rows(w.n_q_heads, M, 4, seed=3, include=[(0, M - 1), (1, b_star)]))
+
+
 def test_dense_path_matches_dense_oracle():
     import torch
     import paper_2609_20971_amd as rbs
