@@ -53,7 +53,9 @@
  *     and the selection calls first scan Q: the selector takes Q in f16, so an
  *     element beyond +-65504 (or not finite) returns RBS_ERR_RANGE with
  *     nothing else launched.  Outside debug mode such a Q gives unspecified
- *     lists.  For development, not for graph capture.
+ *     lists.  For development: not for graph capture, and the range check's
+ *     flag is one per device, so concurrent debug-mode selection calls on one
+ *     device may report each other's out-of-range Q.
  */
 #ifndef RBS_H
 #define RBS_H
