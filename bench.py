@@ -578,10 +578,14 @@ def unit_rates(brief: bool = False):
     # Two waves per SIMD, each issuing 8 of the op (or 8 matrix ops) per loop
     # iteration: one SIMD issues 16 per iteration of either wave.
     per = lambda c: round(c["cycles_per_iter_mfma_wave"] / 16, 2) if c else None
+    loop = {c["schedule"]: c["mfma_busy"] for c in data.get("attention_block_loop", [])}
     return {"exp_cycles": per(ex), "fma_cycles": per(fm), "mfma_32x32x16_bf16_cycles": per(mf),
             "mfma_cycles_with_softmax_mix": per(mix),
+            "block_loop_mfma_busy": loop or None,
             "note": "shader-clock cycles one SIMD spends per wave64 instruction, two waves per SIMD; "
-                    "the mix is 28 exp/fma/max/convert ops beside each 8 matrix ops in the same wave"}
+                    "the mix is 28 exp/fma/max/convert ops beside each 8 matrix ops in the same wave; "
+                    "block_loop: matrix-busy fraction of the attention's block loop on LDS-resident "
+                    "tiles, free-running and as a barrier ping-pong"}
 
 
 def _time_dense(rbs, torch, np, shape, Q, K, V, stream, reps: int) -> float:

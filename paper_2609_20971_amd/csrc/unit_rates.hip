@@ -149,6 +149,149 @@ __global__ __launch_bounds__(512) void rate_kernel(float* out, unsigned long lon
   }
 }
 
+// The attention's block loop on LDS-resident tiles (no global memory): per
+// block and wave, S^T = K Q^T (32 matrix ops, K operands read from LDS), the
+// softmax (64 FMA + exp2, 32 bf16 conversions), then O^T += V^T P^T (32 matrix
+// ops, V^T through the LDS transpose read, 32 v_dot2c for the denominator).
+// Eight waves per workgroup, two per SIMD, one workgroup per CU.  PINGPONG 0:
+// every wave runs the loop freely with one barrier per block (as the kernel
+// does per tile).  PINGPONG 1: waves 0-3 and 4-7 alternate matrix and softmax
+// phases, a barrier at every phase boundary, so that on each SIMD one wave's
+// matrix ops meet the other's softmax.  Results are discarded.
+typedef short s16x4 __attribute__((__vector_size__(4 * sizeof(short))));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+template <int PINGPONG>
+__global__ __launch_bounds__(512) void block_loop_kernel(float* out, unsigned long long* cycles, int nblocks) {
+  __shared__ __align__(16) unsigned char kt[128 * 256];
+  __shared__ __align__(16) unsigned char vt[128 * 256];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  for (int k = tid; k < 128 * 256 / 4; k += 512) {
+    reinterpret_cast<uint32_t*>(kt)[k] = 0x3c003c00u ^ ((uint32_t)k * 2654435761u & 0x00ff00ffu);
+    reinterpret_cast<uint32_t*>(vt)[k] = 0x3c003c00u ^ ((uint32_t)k * 40503u & 0x00ff00ffu);
+  }
+  bf16x8 q[8];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q[ks][e] = (__bf16)(0.01f * (float)((lane + ks + e) & 15));
+  f32x16 o[4] = {};
+  f32x16 s[4];
+  bf16x8 pb[8];
+  float l_run = 0.f;
+  const int group = wave >> 2;
+  __syncthreads();
+  auto qk = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const int row = 32 * mt + l32;
+      s[mt] = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const uint4 raw = *reinterpret_cast<const uint4*>(kt + row * 256 + 16 * ((2 * ks + half) ^ (row & 15)));
+        bf16x8 a;
+        __builtin_memcpy(&a, &raw, 16);
+        s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, q[ks], s[mt], 0, 0, 0);
+      }
+    }
+  };
+  auto softmax = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[mt][r] = __builtin_amdgcn_exp2f(fmaf(s[mt][r], 0.1275f, -1.0f));
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pb[c][e] = (__bf16)s[c >> 1][8 * (c & 1) + e];
+  };
+  auto pv = [&]() __attribute__((always_inline)) {
+    const int vq = (lane & 15) >> 2, vsub = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1), vbyte = 8 * (lane & 1);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 pair = {pb[c][2 * e], pb[c][2 * e + 1]};
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+      }
+      const int row0 = 16 * c + 4 * half + vq;
+      const unsigned char* v0 = vt + row0 * 256 + vbyte;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        const int pc = 16 * ((4 * dt + vsub) ^ ((row0 & 3) << 2));
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v0 + pc));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(v0 + 8 * 256 + pc));
+        bf16x8 a;
+        __builtin_memcpy(&a, &lo, 8);
+        __builtin_memcpy(reinterpret_cast<unsigned char*>(&a) + 8, &hi, 8);
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[c], o[dt], 0, 0, 0);
+      }
+    }
+  };
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+  if constexpr (PINGPONG == 0) {
+    for (int n = 0; n < nblocks; ++n) {
+      qk();
+      softmax();
+      pv();
+      __syncthreads();
+    }
+  } else {
+    // Step t: a wave is in its matrix phase (PV of the previous block, QK of
+    // the next) when t + group is even, else in its softmax.
+    for (int t = 0; t < 2 * nblocks + 1; ++t) {
+      if (((t + group) & 1) == 0) {
+        if (t >= 2) pv();
+        qk();
+      } else if (t >= 1) {
+        softmax();
+      }
+      __syncthreads();
+    }
+  }
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+  float acc = l_run;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc += o[dt][r];
+  out[blockIdx.x * 512 + tid] = acc;
+  if (lane == 0) cycles[blockIdx.x * 8 + wave] = t1 - t0;
+}
+
+// Median cycles per block and wave of block_loop_kernel<PINGPONG> over n_wg
+// workgroups; false on a HIP error.
+template <int PINGPONG>
+bool run_block_loop(int n_wg, int nblocks, double* cyc_per_block, double* ms_out) {
+  float* out = nullptr;
+  unsigned long long* cyc = nullptr;
+  if (hipMalloc(&out, (size_t)n_wg * 512 * sizeof(float)) != hipSuccess) return false;
+  if (hipMalloc(&cyc, (size_t)n_wg * 8 * sizeof(unsigned long long)) != hipSuccess) return false;
+  hipEvent_t e0, e1;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return false;
+  hipLaunchKernelGGL(block_loop_kernel<PINGPONG>, dim3(n_wg), dim3(512), 0, 0, out, cyc, 4);
+  (void)hipEventRecord(e0, 0);
+  hipLaunchKernelGGL(block_loop_kernel<PINGPONG>, dim3(n_wg), dim3(512), 0, 0, out, cyc, nblocks);
+  (void)hipEventRecord(e1, 0);
+  if (hipEventSynchronize(e1) != hipSuccess) return false;
+  float ms = 0.f;
+  (void)hipEventElapsedTime(&ms, e0, e1);
+  std::vector<unsigned long long> c((size_t)n_wg * 8);
+  if (hipMemcpy(c.data(), cyc, c.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost) != hipSuccess)
+    return false;
+  std::sort(c.begin(), c.end());
+  *cyc_per_block = (double)c[c.size() / 2] / nblocks;
+  *ms_out = ms;
+  (void)hipFree(out);
+  (void)hipFree(cyc);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  return true;
+}
+
 struct Result {
   double cyc_mfma_wave;   // median cycles per iteration, waves that issue the matrix ops
   double cyc_other_wave;  // the same for the waves that issue the other ops (split cases)
@@ -278,6 +421,19 @@ int main() {
   RBS_RATE_ACC(8, kMix, 14, true, 2, true)
 #undef RBS_RATE
 #undef RBS_RATE_ACC
+  printf("\n], \"attention_block_loop\": [");
+  // Matrix-busy fraction of one SIMD: two waves, each 64 matrix ops of 32
+  // cycles per block.
+  for (int pp = 0; pp < 2; ++pp) {
+    double cpb = 0.0, ms = 0.0;
+    const bool ok = pp == 0 ? run_block_loop<0>(cus, 400, &cpb, &ms) : run_block_loop<1>(cus, 400, &cpb, &ms);
+    if (!ok) {
+      fprintf(stderr, "block loop %d failed\n", pp);
+      return 1;
+    }
+    printf("%s\n  {\"schedule\": \"%s\", \"cycles_per_block_per_wave\": %.1f, \"mfma_busy\": %.3f, \"ms\": %.3f}",
+           pp ? "," : "", pp ? "ping_pong_barriers" : "free_running", cpb, 2.0 * 64 * 32 / cpb, ms);
+  }
   printf("\n]}\n");
   return 0;
 }
