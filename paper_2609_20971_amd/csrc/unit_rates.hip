@@ -153,9 +153,10 @@ __global__ __launch_bounds__(512) void rate_kernel(float* out, unsigned long lon
 // block and wave, S^T = K Q^T (32 matrix ops, K operands read from LDS), the
 // softmax (64 FMA + exp2, 32 bf16 conversions), then O^T += V^T P^T (32 matrix
 // ops, V^T through the LDS transpose read, 32 v_dot2c for the denominator).
-// Eight waves per workgroup, two per SIMD, one workgroup per CU.  PINGPONG 0:
-// every wave runs the loop freely with one barrier per block (as the kernel
-// does per tile).  PINGPONG 1: waves 0-3 and 4-7 alternate matrix and softmax
+// Eight waves per workgroup (two per SIMD) or four (one per SIMD), one
+// workgroup per CU.  PINGPONG 0: every wave runs the loop freely with one
+// barrier per block (as the kernel does per tile).  PINGPONG 1 (eight waves
+// only): waves 0-3 and 4-7 alternate matrix and softmax
 // phases, a barrier at every phase boundary, so that on each SIMD one wave's
 // matrix ops meet the other's softmax.  Results are discarded.
 typedef short s16x4 __attribute__((__vector_size__(4 * sizeof(short))));
@@ -167,7 +168,7 @@ __global__ __launch_bounds__(512) void block_loop_kernel(float* out, unsigned lo
   __shared__ __align__(16) unsigned char vt[128 * 256];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
-  for (int k = tid; k < 128 * 256 / 4; k += 512) {
+  for (int k = tid; k < 128 * 256 / 4; k += (int)blockDim.x) {
     reinterpret_cast<uint32_t*>(kt)[k] = 0x3c003c00u ^ ((uint32_t)k * 2654435761u & 0x00ff00ffu);
     reinterpret_cast<uint32_t*>(vt)[k] = 0x3c003c00u ^ ((uint32_t)k * 40503u & 0x00ff00ffu);
   }
@@ -263,25 +264,27 @@ __global__ __launch_bounds__(512) void block_loop_kernel(float* out, unsigned lo
 }
 
 // Median cycles per block and wave of block_loop_kernel<PINGPONG> over n_wg
-// workgroups; false on a HIP error.
+// workgroups of `waves` waves (8, or 4 for PINGPONG 0); false on a HIP error.
 template <int PINGPONG>
-bool run_block_loop(int n_wg, int nblocks, double* cyc_per_block, double* ms_out) {
+bool run_block_loop(int n_wg, int waves, int nblocks, double* cyc_per_block, double* ms_out) {
   float* out = nullptr;
   unsigned long long* cyc = nullptr;
   if (hipMalloc(&out, (size_t)n_wg * 512 * sizeof(float)) != hipSuccess) return false;
   if (hipMalloc(&cyc, (size_t)n_wg * 8 * sizeof(unsigned long long)) != hipSuccess) return false;
   hipEvent_t e0, e1;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return false;
-  hipLaunchKernelGGL(block_loop_kernel<PINGPONG>, dim3(n_wg), dim3(512), 0, 0, out, cyc, 4);
+  hipLaunchKernelGGL(block_loop_kernel<PINGPONG>, dim3(n_wg), dim3(64 * waves), 0, 0, out, cyc, 4);
   (void)hipEventRecord(e0, 0);
-  hipLaunchKernelGGL(block_loop_kernel<PINGPONG>, dim3(n_wg), dim3(512), 0, 0, out, cyc, nblocks);
+  hipLaunchKernelGGL(block_loop_kernel<PINGPONG>, dim3(n_wg), dim3(64 * waves), 0, 0, out, cyc, nblocks);
   (void)hipEventRecord(e1, 0);
   if (hipEventSynchronize(e1) != hipSuccess) return false;
   float ms = 0.f;
   (void)hipEventElapsedTime(&ms, e0, e1);
-  std::vector<unsigned long long> c((size_t)n_wg * 8);
-  if (hipMemcpy(c.data(), cyc, c.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost) != hipSuccess)
+  std::vector<unsigned long long> all((size_t)n_wg * 8), c;
+  if (hipMemcpy(all.data(), cyc, all.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost) != hipSuccess)
     return false;
+  for (int w = 0; w < n_wg; ++w)
+    for (int k = 0; k < waves; ++k) c.push_back(all[(size_t)w * 8 + k]);
   std::sort(c.begin(), c.end());
   *cyc_per_block = (double)c[c.size() / 2] / nblocks;
   *ms_out = ms;
@@ -422,17 +425,20 @@ int main() {
 #undef RBS_RATE
 #undef RBS_RATE_ACC
   printf("\n], \"attention_block_loop\": [");
-  // Matrix-busy fraction of one SIMD: two waves, each 64 matrix ops of 32
-  // cycles per block.
-  for (int pp = 0; pp < 2; ++pp) {
+  // Matrix-busy fraction of one SIMD: its waves (two, or one), each 64
+  // matrix ops of 32 cycles per block.
+  const char* names[3] = {"free_running", "ping_pong_barriers", "free_running_one_wave_per_simd"};
+  for (int k = 0; k < 3; ++k) {
     double cpb = 0.0, ms = 0.0;
-    const bool ok = pp == 0 ? run_block_loop<0>(cus, 400, &cpb, &ms) : run_block_loop<1>(cus, 400, &cpb, &ms);
+    const int waves = k == 2 ? 4 : 8;
+    const bool ok = k == 1 ? run_block_loop<1>(cus, 8, 400, &cpb, &ms) : run_block_loop<0>(cus, waves, 400, &cpb, &ms);
     if (!ok) {
-      fprintf(stderr, "block loop %d failed\n", pp);
+      fprintf(stderr, "block loop %s failed\n", names[k]);
       return 1;
     }
-    printf("%s\n  {\"schedule\": \"%s\", \"cycles_per_block_per_wave\": %.1f, \"mfma_busy\": %.3f, \"ms\": %.3f}",
-           pp ? "," : "", pp ? "ping_pong_barriers" : "free_running", cpb, 2.0 * 64 * 32 / cpb, ms);
+    printf("%s\n  {\"schedule\": \"%s\", \"waves_per_simd\": %d, \"cycles_per_block_per_wave\": %.1f, "
+           "\"mfma_busy\": %.3f, \"ms\": %.3f}",
+           k ? "," : "", names[k], waves / 4, cpb, waves / 4 * 64.0 * 32 / cpb, ms);
   }
   printf("\n]}\n");
   return 0;
