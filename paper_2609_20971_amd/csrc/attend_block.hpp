@@ -14,7 +14,8 @@
 // free.  K feeds the A operand with 128-bit reads; V^T is read from row-major
 // V with the gfx950 LDS transpose read (ds_read_b64_tr_b16).  The two tiles
 // are pipelined against compute: the next block's K is fetched while this
-// block's softmax and PV run, the next V while the next QK^T runs.  Online
+// block's softmax and PV run, the next V while the next QK^T runs, each
+// tile's copies issued in pieces among the matrix and exponential steps.  Online
 // softmax in fp32 with exp2; P is rounded to bf16 for the PV product, and the
 // softmax denominator sums exactly those rounded values (v_dot2 with ones).  Causal
 // masking is applied on the diagonal block only; keys past N are masked in a
@@ -176,13 +177,48 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   const int64_t tile_stride = (int64_t)BS * c.kv_tok;  // elements between consecutive key blocks
   const uint32_t row_bytes = (uint32_t)(c.kv_tok * 2);
   const TileOffsets toff = tile_offsets(row_bytes, wave, lane);
-  // Copies of key block b's K or V tile (nb rows inside the sequence).
+  const uint32_t k_base = lds_offset(k_lds), v_base = lds_offset(v_lds);
+  // Copies of key block b's K or V tile (nb rows inside the sequence), all at once.
   auto copy_tile = [&](const uint16_t* base, int b, uint32_t lds_base, bool is_v) __attribute__((always_inline)) {
     const int nb = min(BS, N - b * BS);
     if (nb == BS)
       issue_tile_full(base + b * tile_stride, row_bytes, toff, lds_base, wave, is_v);
     else
       issue_tile(base + b * tile_stride, nb, row_bytes, lds_base, wave, lane, is_v);
+  };
+  // Inside the block loop a full tile's 8 copies per wave go out in pieces
+  // spread through the work instead of in one burst after the barrier that
+  // frees the tile: the CU's global -> LDS path takes one 1 KB copy about every
+  // 16 cycles, so a workgroup's 32-copy burst held each wave at issue for
+  // ~500 cycles.  kCopyHead copies are issued right after that barrier, the
+  // rest in pairs after the matrix steps of QK^T (V) or after the exponential
+  // steps (K), and whatever remains after the last step.
+  constexpr int kCopyHead = 4;
+  const uint32_t k_wave = __builtin_amdgcn_readfirstlane(k_base + (uint32_t)(32 * wave) * 256u);
+  const uint32_t v_wave = __builtin_amdgcn_readfirstlane(v_base + (uint32_t)(32 * wave) * 256u);
+  // Copies j and j + 1 (of 8) of key block b's full K or V tile.
+  auto copy_pair = [&](const uint16_t* base, int b, bool is_v, int j) __attribute__((always_inline)) {
+    const unsigned char* t = reinterpret_cast<const unsigned char*>(base + b * tile_stride);
+    const uint32_t lw = is_v ? v_wave : k_wave;
+    lds_dma16(t + (size_t)j * 4u * row_bytes, is_v ? toff.v : toff.k[j & 3], lw + (uint32_t)j * 1024u);
+    lds_dma16(t + (size_t)(j + 1) * 4u * row_bytes, is_v ? toff.v : toff.k[(j + 1) & 3],
+              lw + (uint32_t)(j + 1) * 1024u);
+  };
+  // The pair issued after step mt of KT (none past the last step or the 8th copy).
+  auto step_pair = [&](const uint16_t* base, int b, bool is_v, int mt) __attribute__((always_inline)) {
+    if (mt < KT - 1 && kCopyHead + 2 * mt < 8) {
+      __builtin_amdgcn_sched_barrier(0);
+      copy_pair(base, b, is_v, kCopyHead + 2 * mt);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  auto rest_pairs = [&](const uint16_t* base, int b, bool is_v) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = kCopyHead + 2 * (KT - 1); j < 8; j += 2) copy_pair(base, b, is_v, j);
+  };
+  auto head_pairs = [&](const uint16_t* base, int b, bool is_v) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < kCopyHead; j += 2) copy_pair(base, b, is_v, j);
   };
 
   // Per-lane LDS read bases.  K: row 32mt + l32 of the step, chunk 2ks + half.
@@ -191,8 +227,6 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   const int vq = (lane & 15) >> 2;
   const int vsub = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);  // chunk within the dt group
   const int vbyte = 8 * (lane & 1);
-
-  const uint32_t k_base = lds_offset(k_lds), v_base = lds_offset(v_lds);
 
   // Softmax reference.  The first pass fixes it at the row maximum of the
   // first listed block (a sink block, usually, or the diagonal) and computes
@@ -216,18 +250,21 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   // load is off the critical path.
   int kb_ahead = count > 1 ? list_at(1) : 0;
   if (count > 0) {
-    const int nk0 = min(BS, N - kb * BS);
     copy_tile(kg, kb, k_base, false);
     copy_tile(vg, kb, v_base, true);
   }
+  bool v_spread = false;  // this block's V: kCopyHead copies issued, the rest due during QK^T
   for (int n = 0; n < count; ++n) {
     const bool has_next = n + 1 < count;
     const int kb_next = has_next ? min(max(kb_ahead, 0), i) : 0;
     kb_ahead = n + 2 < count ? list_at(n + 2) : 0;
     const int nk = min(BS, N - kb * BS);
     const bool diag = kb == i;
+    const bool next_full = has_next && N - kb_next * BS >= BS;  // the next tiles go out in pieces
 
-    RBS_WAIT_VMCNT(8);  // this block's K has landed (its V may still be in flight)
+    // This block's K has landed; behind it, the V copies issued so far may
+    // still be in flight.
+    if (v_spread) RBS_WAIT_VMCNT(kCopyHead); else RBS_WAIT_VMCNT(8);
     __syncthreads();
 
     // Softmax steps of a block kept as a loop: unrolled, B = 256's two steps
@@ -248,10 +285,14 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
           __builtin_memcpy(&a, &raw, 16);
           s[mt] = mfma_bf16(a, qreg[ks], s[mt]);
         }
+        if (v_spread && sub == 0) step_pair(vg, kb, true, mt);
       }
+      if (v_spread && sub == 0) rest_pairs(vg, kb, true);
       if (sub == BS / SUB - 1) {
         __syncthreads();  // every wave is done with this K tile
-        if (has_next)
+        if (next_full)
+          head_pairs(kg, kb_next, false);
+        else if (has_next)
           copy_tile(kg, kb_next, k_base, false);
       }
       if (diag || nk < BS) {
@@ -294,10 +335,14 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
         }
       }
       const float shift = ms_run == -INFINITY ? 0.f : ms_run;
+      const bool k_spread = next_full && sub == BS / SUB - 1;
 #pragma unroll
-      for (int mt = 0; mt < KT; ++mt)
+      for (int mt = 0; mt < KT; ++mt) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[mt][r] = fast_exp2(fmaf(s[mt][r], scale_log2, -shift));
+        if (k_spread) step_pair(kg, kb_next, false, mt);
+      }
+      if (k_spread) rest_pairs(kg, kb_next, false);
       if (sub == 0) {
         // This block's V has landed.  The next block's K copies are already
         // in flight behind it only when the block has a single step.
@@ -334,7 +379,10 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
       }
     }
     __syncthreads();  // every wave is done with this V tile
-    if (has_next)
+    v_spread = next_full;
+    if (next_full)
+      head_pairs(vg, kb_next, true);
+    else if (has_next)
       copy_tile(vg, kb_next, v_base, true);
     kb = kb_next;
   }
