@@ -119,9 +119,20 @@ __device__ __forceinline__ void issue_tile_full(const uint16_t* tile_base, uint3
 // Rescale threshold of the online softmax, in log2 units.
 constexpr float kRescaleSlack = 8.0f;
 // Fixed-reference pass: the largest denominator share a lane may reach (2^64)
-// for the pass's result to stand; past it (or on inf / NaN) the item is
-// computed again with the running maximum.
+// in one softmax step for the pass's result to stand; past it (or on inf /
+// NaN) the item is computed again with the running maximum.
 constexpr float kFixedRefBound = 18446744073709551616.0f;
+// Fixed-reference pass: once a lane's denominator share passes 2^32, the
+// query's O and denominator are scaled down by a power of two and its
+// reference raised by the same exponent (exact: no rounding).
+constexpr float kLazyRescaleAt = 4294967296.0f;
+// Fixed-reference pass: the reference sits this far (log2 units) above the
+// first block's row maximum, and after a rescale above the query's
+// denominator, so that a later block's logits may exceed the previous ones by
+// up to ~64 + kRefMargin before the pass is abandoned.  Exponentials more than
+// ~126 - kRefMargin below the first block's maximum flush to zero (relative
+// weight under 2^-78).
+constexpr float kRefMargin = 48.0f;
 
 // Arguments of one attention pass, shared by the stand-alone and the fused kernel.
 struct AttnCore {
@@ -231,18 +242,29 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   // Softmax reference.  The first pass fixes it at the row maximum of the
   // first listed block (a sink block, usually, or the diagonal) and computes
   // no maximum for the other blocks: exponentials of later, larger logits
-  // simply exceed 1.  The denominator shares bound every exponential, so when
-  // each stays within kFixedRefBound the pass's O and LSE stand (P keeps its
-  // relative precision at any magnitude, and O its range for |v| < 2^45).
-  // Otherwise every wave of the workgroup computes the item again with the
-  // running maximum of the online softmax (raised lazily: only when a block's
-  // maximum exceeds it by more than kRescaleSlack).
+  // simply exceed 1 (the reference sits kRefMargin above that maximum).  When a
+  // lane's denominator share passes kLazyRescaleAt, the reference moves up by
+  // a whole exponent and O and the shares are scaled down by the same power of
+  // two.  The shares bound every exponential of a
+  // step, so when each stays within kFixedRefBound the pass's O and LSE stand
+  // (P keeps its relative precision at any magnitude, and O its range for
+  // |v| < 2^45).  Otherwise every wave of the workgroup computes the item
+  // again with the running maximum of the online softmax (raised lazily: only
+  // when a block's maximum exceeds it by more than kRescaleSlack).
   float ms_run, l_run;  // reference maximum (log2 units); this lane's share of the denominator
   f32x16 o[4];
+  // Fixed-reference pass: set by a wave whose shares left the range, read by
+  // every wave after the block's last barrier, so that the workgroup stops the
+  // pass at that block instead of finishing it.
+  __shared__ int stop_fixed;
   for (int pass = 0; pass < 2; ++pass) {
   const bool exact = pass == 1;
   ms_run = -INFINITY;
   l_run = 0.f;
+  bool out_of_range = false;  // fixed-reference pass: some step took a share past kFixedRefBound
+  // Every lane stores the same value (a branch here cost the block loop its
+  // registers); no wave reads it before the first block's barriers.
+  stop_fixed = 0;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x16{};
   int kb = count > 0 ? min(max(list_at(0), 0), i) : 0;
@@ -324,7 +346,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
         // more than kRescaleSlack, so the exponentials stay below 2^kRescaleSlack.
         const float mxs = mx * scale_log2;
         if (__any(mxs > ms_run + kRescaleSlack)) {
-          const float ms_new = fmaxf(ms_run, mxs);
+          const float ms_new = exact ? fmaxf(ms_run, mxs) : mxs + kRefMargin;
           const float alpha = ms_new == ms_run ? 1.f : fast_exp2(ms_run - ms_new);
           ms_run = ms_new;
           l_run *= alpha;
@@ -377,14 +399,39 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
           o[dt] = mfma_bf16(a, pb, o[dt]);
         }
       }
+      if (!exact && __any(!(l_run <= kLazyRescaleAt))) {
+        // A later block's logits exceed the reference: move the reference up
+        // by the exponent of the query's denominator (the same in the two
+        // lanes that hold the query) and scale O and the shares down by that
+        // power of two.  Shares past kFixedRefBound mean this step's O may
+        // have left fp32's range: the item is computed again.
+        if (__any(!(l_run <= kFixedRefBound))) {
+          out_of_range = true;
+          stop_fixed = 1;
+        }
+        const float l_tot = l_run + wave_xor_f(l_run, 32);
+        const int k = l_tot > kLazyRescaleAt ? __builtin_amdgcn_frexp_expf(l_tot) + (int)kRefMargin : 0;
+        const float f = __builtin_amdgcn_ldexpf(1.0f, -k);
+        ms_run += (float)k;
+        l_run *= f;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[dt][r] *= f;
+      }
     }
     __syncthreads();  // every wave is done with this V tile
+    const int stop = exact ? 0 : stop_fixed;  // used after the copies below, which hide the read
     v_spread = next_full;
     if (next_full)
       head_pairs(vg, kb_next, true);
     else if (has_next)
       copy_tile(vg, kb_next, v_base, true);
     kb = kb_next;
+    if (__builtin_amdgcn_readfirstlane(stop) != 0) {
+      RBS_WAIT_VMCNT(0);  // the next block's copies land before the tiles are reused
+      n = count;          // ends the pass here
+    }
   }
   if (exact) break;
   // Did any lane of the workgroup leave the fixed reference's range?  The
@@ -392,7 +439,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   // tile take one flag per wave.
   {
     int* flags = reinterpret_cast<int*>(k_lds);
-    const bool bad = __any(!(l_run <= kFixedRefBound));
+    const bool bad = __any(out_of_range || !(l_run <= kFixedRefBound));
     if (lane == 0) flags[wave] = bad ? 1 : 0;
     __syncthreads();
     int any_bad = 0;
