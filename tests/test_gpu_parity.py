@@ -169,9 +169,9 @@ def test_unshifted_sums_at_the_bound_b256():
     aligned with the longest select-ready centroid and scaled so that
     |q| max_b |c'_b| sits just under the unshifted-sum bound (112, log2
     units): the block of that centroid sums 256 terms near 2^108 each, which
-    must stay finite; the attention's fixed softmax reference (the sink
-    block's maximum) is exceeded far past its range, so it takes the exact
-    pass."""
+    must stay finite; in the attention, later blocks exceed the fixed softmax
+    reference (taken from the sink block) by far more than fp32's exponent
+    range near 1, which its power-of-two rescales absorb without a restart."""
     from synth import bf16_bits_from_f32, f64_from_bf16_bits
     w = WORKLOADS["tiny-2k"].with_(name="bound", seq_len=2048, block_size=256, n_q_heads=2, n_kv_heads=1,
                                    needles_per_kv_head=2, seed=33)
