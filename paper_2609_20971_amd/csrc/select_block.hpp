@@ -341,19 +341,23 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         }
         // Per lane (key block b) and branch, a (shift, sum of exp2) pair over
         // this wave's tokens: S_b = exp2(shift) * sum.
+        // (Sums start from their first term: an added 0 is an instruction the
+        // compiler must keep, since 0 + -0 is not -0.)
         float mx = -INFINITY, sb = 0.f, mr = -INFINITY, sr = 0.f;
         if constexpr (BASE) {
           if (plain_tile) {
             mx = 0.f;
+            sb = fast_exp2(acc[0]);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r]);
+            for (int r = 1; r < 16; ++r) sb += fast_exp2(acc[r]);
           } else {
             mx = acc[0];
 #pragma unroll
             for (int r = 1; r < 16; ++r) mx = fmaxf(mx, acc[r]);
             mx = half_max(mx);
+            sb = fast_exp2(acc[0] - mx);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
+            for (int r = 1; r < 16; ++r) sb += fast_exp2(acc[r] - mx);
           }
           sb = half_sum(sb);
         }
@@ -362,8 +366,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
           const float u = b >= 0 ? u_cur * u_scale : 0.f;
           if (plain_tile) {
             mr = nq_row * u;
+            sr = fast_exp2(fmaf(nqd[0], u, acc[0]));
 #pragma unroll
-            for (int r = 0; r < 16; ++r) sr += fast_exp2(fmaf(nqd[r], u, acc[r]));
+            for (int r = 1; r < 16; ++r) sr += fast_exp2(fmaf(nqd[r], u, acc[r]));
           } else {
             float v[16];
             float mv = -INFINITY;
@@ -374,8 +379,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
             }
             mv = half_max(mv);
             mr = mv + nq_row * u;
+            sr = fast_exp2(v[0] - mv);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) sr += fast_exp2(v[r] - mv);
+            for (int r = 1; r < 16; ++r) sr += fast_exp2(v[r] - mv);
           }
           sr = half_sum(sr);
         }
@@ -393,13 +399,13 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       const bool mine = wave == (tile & (NW - 1)) && b >= 0 && (half ? RES : BASE);
       if (mine && plain_tile) {
         // Every wave used the same shift: S_b = exp2(shift) * (sum of the sums).
-        float sum = 0.f;
+        const float4 p0 = stage[(buf * NW) * kTile + l32];  // wave 0 is always active
+        float sum = half ? p0.w : p0.y;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) {
+        for (int w = 1; w < NW; ++w) {
           const float4 p = stage[(buf * NW + w) * kTile + l32];
           sum += half ? p.w : p.y;
         }
-        const float4 p0 = stage[(buf * NW) * kTile + l32];  // wave 0 is always active
         L[b] = (half ? p0.z : p0.x) + log2f(sum);
       } else if (mine) {
         float top = -INFINITY;
@@ -452,9 +458,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
               if (32 * wave + mfma_row(r, lane) >= nb) acc[r] = -INFINITY;
           }
         }
-        float sb = 0.f;
+        float sb = fast_exp2(acc[0]);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sb += fast_exp2(acc[r]);
+        for (int r = 1; r < 16; ++r) sb += fast_exp2(acc[r]);
         sb = half_sum(sb);
         if (half == 0) st[(buf * NW + wave) * kTile + l32] = sb;
       } else if (half == 0) {
@@ -464,9 +470,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       __syncthreads();
       const int b = tile * kTile + l32;
       if (wave == (tile & (NW - 1)) && half == 0 && b < n_cand) {
-        float sum = 0.f;
+        float sum = st[(buf * NW) * kTile + l32];
 #pragma unroll
-        for (int w = 0; w < NW; ++w) sum += st[(buf * NW + w) * kTile + l32];
+        for (int w = 1; w < NW; ++w) sum += st[(buf * NW + w) * kTile + l32];
         L[b] = __builtin_amdgcn_logf(sum);
       }
     }
