@@ -6,7 +6,8 @@
 // 32 query tokens 32w..32w+31 of the block.  Q_i is read from HBM once and
 // held in registers as f16 (bf16 -> f16 is exact in the normal range).
 // Candidate key blocks 0..i are scored in tiles of 32 centroids staged through
-// LDS (double buffered, one barrier per tile):
+// LDS (double buffered, one barrier per tile; at B = 64 one buffer and two
+// barriers per tile, which frees a sixth of the workgroup's LDS):
 //
 //   S = Q_i C'^T on the f16 MFMA (32x32x16), where C' = c_b log2(e)/sqrt(d)
 //   is the select-ready centroid written by the statistics stage, so S holds
@@ -104,7 +105,10 @@ constexpr int select_cand_cap(int M, int NT) {
 template <int BS, int MODE>
 struct SelectLds {
   static constexpr int NW = BS / 32;
-  static constexpr size_t tile_bufs = MODE == kSelectBox ? 4 : 2;
+  // Centroid tile buffers.  At B = 64 the dual selector's occupancy is set by
+  // LDS, not registers: one buffer (and a second barrier per tile) lets 7
+  // workgroups share a CU instead of 5 (3.5 waves per SIMD instead of 2.5).
+  static constexpr size_t tile_bufs = MODE == kSelectBox ? 4 : (BS == 64 && MODE == kSelectDual ? 1 : 2);
   static constexpr size_t stage = tile_bufs * kTileBytes;
   static constexpr size_t nq = stage + 2 * NW * kTile * 16;
   static constexpr size_t L = nq + BS * 4;
@@ -146,6 +150,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   constexpr int NW = BS / 32;
   constexpr int NT = NW * kWave;
   using Lds = SelectLds<BS, MODE>;
+  constexpr bool kSingle = Lds::tile_bufs == 1;  // one centroid tile buffer: a second barrier per tile
   const uint16_t* __restrict__ Q = c.Q;
   const int N = c.N, M = c.M;
   f16x8* cbuf = reinterpret_cast<f16x8*>(smem_raw);
@@ -238,7 +243,8 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   };
 
   // ---- Tile passes.  A pass scores tiles of 32 key blocks staged through LDS
-  // (double buffered, one barrier per tile); id_at(t, r) is the block of row r
+  // (double buffered, one barrier per tile; with one buffer, the next tile is
+  // stored after that barrier and a second one follows); id_at(t, r) is the block of row r
   // of tile t, or -1.  The flags choose the branch whose scores it writes to
   // L.  Every load is issued without a branch (a padding row reads block 0;
   // its lane's results are never used), so no loaded value is merged at a
@@ -323,7 +329,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       if constexpr (MODE == kSelectDual) plain_tile = __all(b < 0 || nq_row * (cn_cur + u_cur) <= kPlainBound);
       if (wave_active) {
         f32x16 acc = {};
-        const f16x8* cb = cbuf + (buf * kTile + l32) * kRowChunks + half;
+        const f16x8* cb = cbuf + ((kSingle ? 0 : buf) * kTile + l32) * kRowChunks + half;
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) acc = mfma_f16(qa[ks], cb[2 * ks], acc);
         if constexpr (MODE == kSelectBox) {
@@ -389,10 +395,11 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       } else if (half == 0) {
         stage[(buf * NW + wave) * kTile + l32] = make_float4(-INFINITY, 0.f, -INFINITY, 0.f);
       }
-      if (tile + 1 < n_tiles_p) store(buf ^ 1);
+      if (!kSingle && tile + 1 < n_tiles_p) store(buf ^ 1);
       u_cur = u_next;
       cn_cur = cn_next;
       __syncthreads();
+      if (kSingle && tile + 1 < n_tiles_p) store(0);
       // Merge the waves' partial sums of this tile (lanes 0-31 base, 32-63
       // rescue), by one wave in turn: the waves of a workgroup sit on
       // different SIMDs, and a fixed merging wave would load one SIMD more.
@@ -423,6 +430,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         }
         L[b] = top + log2f(sum);
       }
+      if constexpr (kSingle) __syncthreads();  // the next tile is in place
     }
     __syncthreads();
   };
@@ -444,7 +452,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       const int buf = tile & 1;
       if (tile + 1 < n_tiles) fetch_rows(tile + 1, all);
       if (wave_active) {
-        const f16x8* cb = cbuf + (buf * kTile + l32) * kRowChunks + half;
+        const f16x8* cb = cbuf + ((kSingle ? 0 : buf) * kTile + l32) * kRowChunks + half;
         f16x8 op[8];
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) op[ks] = cb[2 * ks];
@@ -466,8 +474,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       } else if (half == 0) {
         st[(buf * NW + wave) * kTile + l32] = 0.f;
       }
-      if (tile + 1 < n_tiles) store(buf ^ 1);
+      if (!kSingle && tile + 1 < n_tiles) store(buf ^ 1);
       __syncthreads();
+      if (kSingle && tile + 1 < n_tiles) store(0);
       const int b = tile * kTile + l32;
       if (wave == (tile & (NW - 1)) && half == 0 && b < n_cand) {
         float sum = st[(buf * NW) * kTile + l32];
@@ -475,6 +484,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         for (int w = 1; w < NW; ++w) sum += st[(buf * NW + w) * kTile + l32];
         L[b] = __builtin_amdgcn_logf(sum);
       }
+      if constexpr (kSingle) __syncthreads();  // the next tile is in place
     }
     __syncthreads();
   };
