@@ -90,32 +90,38 @@ struct SelectCore {
   int64_t capacity;
 };
 
-// Slots of the dual selector's rescue-candidate list: a quarter of the blocks
+// Slots of the dual selector's rescue-candidate list: an eighth of the blocks
 // (at least two compaction chunks of NT blocks, at most M); more candidates are
 // scored in several chunks.
 constexpr int select_cand_cap(int M, int NT) {
-  const int quarter = (M / 4 + kTile - 1) / kTile * kTile;
-  const int cap = quarter > 2 * NT ? quarter : 2 * NT;
+  const int eighth = (M / 8 + kTile - 1) / kTile * kTile;
+  const int cap = eighth > 2 * NT ? eighth : 2 * NT;
   return cap < M ? cap : M;
 }
 
 // LDS layout of select_block (byte offsets):
-//   cbuf[bufs][32 rows][17 chunks of 8 f16] | stage[2][NW][32] float4 | nq[BS] | L[M] |
-//   red_f[3 NW] | red_i[NW] (| cnt[2][NW], box) (| flags[M] bytes | cand[cap], dual)
+//   cbuf[bufs][32 rows][17 chunks of 8 f16] | stage[bufs][NW][32] float4 | nq[BS] | L[M] |
+//   red_f[3 NW] | red_i[NW] (| cnt[2][NW], box) (| flags[2][ceil(M/64)] bit masks | cand[cap], dual)
 template <int BS, int MODE>
 struct SelectLds {
   static constexpr int NW = BS / 32;
-  // Centroid tile buffers.  At B = 64 the dual selector's occupancy is set by
-  // LDS, not registers: one buffer (and a second barrier per tile) lets 7
-  // workgroups share a CU instead of 5 (3.5 waves per SIMD instead of 2.5).
+  // Centroid tile and stage buffers.  At B = 64 the dual selector's occupancy
+  // is set by LDS, not registers: one buffer of each (and a second barrier
+  // per tile) lets 8 workgroups share a CU instead of 5 (4 waves per SIMD
+  // instead of 2.5).
   static constexpr size_t tile_bufs = MODE == kSelectBox ? 4 : (BS == 64 && MODE == kSelectDual ? 1 : 2);
+  static constexpr size_t stage_bufs = tile_bufs == 1 ? 1 : 2;
   static constexpr size_t stage = tile_bufs * kTileBytes;
-  static constexpr size_t nq = stage + 2 * NW * kTile * 16;
+  static constexpr size_t nq = stage + stage_bufs * NW * kTile * 16;
   static constexpr size_t L = nq + BS * 4;
   static constexpr size_t red_f(int M) { return L + (size_t)M * 4; }
   static constexpr size_t red_i(int M) { return red_f(M) + 3 * NW * 4; }
-  static constexpr size_t flags(int M) { return red_i(M) + (MODE == kSelectBox ? 3 : 1) * NW * 4; }
-  static constexpr size_t cand(int M) { return flags(M) + (((size_t)M + 3) & ~(size_t)3); }
+  // Dual: per 64 blocks, two 64-bit masks (selected by the base branch; L[b]
+  // holds the block's rescue score), 8-byte aligned; one pair per wave and
+  // NT-block chunk of the candidate listing, which covers ceil(M / NT) chunks.
+  static constexpr size_t flag_words(int M) { return (size_t)((M + 2 * BS - 1) / (2 * BS)) * NW; }
+  static constexpr size_t flags(int M) { return (red_i(M) + (MODE == kSelectBox ? 3 : 1) * NW * 4 + 7) & ~(size_t)7; }
+  static constexpr size_t cand(int M) { return flags(M) + flag_words(M) * 16; }
   static constexpr size_t bytes(int M) {
     return MODE == kSelectDual ? cand(M) + (size_t)select_cand_cap(M, BS * 2) * 4 : flags(M);
   }
@@ -163,9 +169,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   float* L = reinterpret_cast<float*>(smem_raw + Lds::L);
   float* red_f = reinterpret_cast<float*>(smem_raw + Lds::red_f(M));
   int* red_i = reinterpret_cast<int*>(smem_raw + Lds::red_i(M));
-  // Dual: per block, bit 0 = selected by the base branch, bit 1 = L[b] is its
-  // rescue score (no uplift, or a rescue candidate).
-  uint8_t* flags = smem_raw + Lds::flags(M);
+  // Dual: per 64 blocks, [0] bit b % 64 = block b selected by the base
+  // branch, [1] = L[b] is its rescue score (no uplift, or a rescue candidate).
+  uint64_t* flags = reinterpret_cast<uint64_t*>(smem_raw + Lds::flags(M));
   int* cand = reinterpret_cast<int*>(smem_raw + Lds::cand(M));  // dual: rescue candidates to score
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -317,6 +323,7 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
     __syncthreads();
     for (int tile = 0; tile < n_tiles_p; ++tile) {
       const int buf = tile & 1;
+      const int sbuf = kSingle ? 0 : buf;  // stage buffer
       if (tile + 1 < n_tiles_p) fetch(tile + 1);
       const int b = id_at(tile, l32);
       // The dual selector skips the per-block shift when every exponent of
@@ -391,9 +398,9 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
           }
           sr = half_sum(sr);
         }
-        if (half == 0) stage[(buf * NW + wave) * kTile + l32] = make_float4(mx, sb, mr, sr);
+        if (half == 0) stage[(sbuf * NW + wave) * kTile + l32] = make_float4(mx, sb, mr, sr);
       } else if (half == 0) {
-        stage[(buf * NW + wave) * kTile + l32] = make_float4(-INFINITY, 0.f, -INFINITY, 0.f);
+        stage[(sbuf * NW + wave) * kTile + l32] = make_float4(-INFINITY, 0.f, -INFINITY, 0.f);
       }
       if (!kSingle && tile + 1 < n_tiles_p) store(buf ^ 1);
       u_cur = u_next;
@@ -406,11 +413,11 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       const bool mine = wave == (tile & (NW - 1)) && b >= 0 && (half ? RES : BASE);
       if (mine && plain_tile) {
         // Every wave used the same shift: S_b = exp2(shift) * (sum of the sums).
-        const float4 p0 = stage[(buf * NW) * kTile + l32];  // wave 0 is always active
+        const float4 p0 = stage[(sbuf * NW) * kTile + l32];  // wave 0 is always active
         float sum = half ? p0.w : p0.y;
 #pragma unroll
         for (int w = 1; w < NW; ++w) {
-          const float4 p = stage[(buf * NW + w) * kTile + l32];
+          const float4 p = stage[(sbuf * NW + w) * kTile + l32];
           sum += half ? p.w : p.y;
         }
         L[b] = (half ? p0.z : p0.x) + log2f(sum);
@@ -418,13 +425,13 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
         float top = -INFINITY;
 #pragma unroll
         for (int w = 0; w < NW; ++w) {
-          const float4 p = stage[(buf * NW + w) * kTile + l32];
+          const float4 p = stage[(sbuf * NW + w) * kTile + l32];
           top = fmaxf(top, half ? p.z : p.x);
         }
         float sum = 0.f;
 #pragma unroll
         for (int w = 0; w < NW; ++w) {
-          const float4 p = stage[(buf * NW + w) * kTile + l32];
+          const float4 p = stage[(sbuf * NW + w) * kTile + l32];
           const float m = half ? p.z : p.x, sv = half ? p.w : p.y;
           if (sv > 0.f) sum += sv * fast_exp2(m - top);
         }
@@ -443,13 +450,14 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
   // at least 2^-kPlainBound from wave 0, so the log2's input is normal.
   auto lean_base_pass = [&](auto partial) __attribute__((always_inline)) {
     constexpr bool PARTIAL = decltype(partial)::value;
-    float* st = reinterpret_cast<float*>(stage);  // [2][NW][kTile]
+    float* st = reinterpret_cast<float*>(stage);  // [stage buffers][NW][kTile]
     const AllBlocks all{n_cand};
     fetch_rows(0, all);
     store(0);
     __syncthreads();
     for (int tile = 0; tile < n_tiles; ++tile) {
       const int buf = tile & 1;
+      const int sbuf = kSingle ? 0 : buf;  // stage buffer
       if (tile + 1 < n_tiles) fetch_rows(tile + 1, all);
       if (wave_active) {
         const f16x8* cb = cbuf + ((kSingle ? 0 : buf) * kTile + l32) * kRowChunks + half;
@@ -470,18 +478,18 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
 #pragma unroll
         for (int r = 1; r < 16; ++r) sb += fast_exp2(acc[r]);
         sb = half_sum(sb);
-        if (half == 0) st[(buf * NW + wave) * kTile + l32] = sb;
+        if (half == 0) st[(sbuf * NW + wave) * kTile + l32] = sb;
       } else if (half == 0) {
-        st[(buf * NW + wave) * kTile + l32] = 0.f;
+        st[(sbuf * NW + wave) * kTile + l32] = 0.f;
       }
       if (!kSingle && tile + 1 < n_tiles) store(buf ^ 1);
       __syncthreads();
       if (kSingle && tile + 1 < n_tiles) store(0);
       const int b = tile * kTile + l32;
       if (wave == (tile & (NW - 1)) && half == 0 && b < n_cand) {
-        float sum = st[(buf * NW) * kTile + l32];
+        float sum = st[(sbuf * NW) * kTile + l32];
 #pragma unroll
-        for (int w = 1; w < NW; ++w) sum += st[(buf * NW + w) * kTile + l32];
+        for (int w = 1; w < NW; ++w) sum += st[(sbuf * NW + w) * kTile + l32];
         L[b] = __builtin_amdgcn_logf(sum);
       }
       if constexpr (kSingle) __syncthreads();  // the next tile is in place
@@ -535,12 +543,19 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       int n_c = 0;
       for (int base = 0; base < n_cand; base += NT) {
         const int b = base + tid;
-        bool is_cand = false;
+        bool is_cand = false, base_sel = false, res_in_l = false;
         if (b < n_cand) {
           const float u = ug[b], lb = L[b];
           is_cand = u > 0.f && lb + nq_row * u >= cut;
-          flags[b] = (uint8_t)((lb >= thr_base ? 1 : 0) | (u > 0.f ? (is_cand ? 2 : 0) : 2));
+          base_sel = lb >= thr_base;
+          res_in_l = !(u > 0.f) || is_cand;
           if (!(u > 0.f)) mres = fmaxf(mres, lb);
+        }
+        // The wave's 64 blocks are base + 64 wave .. + 63: one word of each mask.
+        const uint64_t m_base = __ballot(base_sel), m_res = __ballot(res_in_l);
+        if (lane == 0) {
+          flags[2 * ((base >> 6) + wave)] = m_base;
+          flags[2 * ((base >> 6) + wave) + 1] = m_res;
         }
         const uint64_t ballot = __ballot(is_cand);
         const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(ballot >> 32),
@@ -623,8 +638,10 @@ __device__ __forceinline__ int select_block(const SelectCore& c, int h, int i, u
       const bool forced = recent_row || b < c.n_sink || b > i - c.n_local;
       if constexpr (MODE == kSelectDual) {
         // flags are written only when the rescue threshold is in use.
-        const int f = c.rescue_all ? 0 : flags[b];
-        sel = forced || c.base_all || c.rescue_all || (f & 1) || ((f & 2) && L[b] >= thr_res);
+        const int w64 = b >> 6, bit = b & 63;
+        const bool in_base = !c.rescue_all && ((flags[2 * w64] >> bit) & 1);
+        const bool in_res = !c.rescue_all && ((flags[2 * w64 + 1] >> bit) & 1) && L[b] >= thr_res;
+        sel = forced || c.base_all || c.rescue_all || in_base || in_res;
       } else if constexpr (MODE == kSelectCentroid) {
         sel = forced || c.base_all || L[b] >= thr_base;
       } else if constexpr (MODE == kSelectFullL2) {
