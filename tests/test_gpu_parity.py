@@ -102,6 +102,9 @@ def test_edge_shapes(variant):
     dict(seq_len=6000, block_size=64, n_q_heads=4, n_kv_heads=2, seed=11),         # 94 blocks, ragged
     dict(seq_len=9000, block_size=256, n_q_heads=4, n_kv_heads=1, seed=12),        # 36 blocks, two softmax steps per block
     dict(seq_len=8191, block_size=128, n_q_heads=8, n_kv_heads=2, seed=13),        # 64 blocks, one row short
+    # 266 blocks at B = 64: late rows list their candidates in three 128-block
+    # chunks, the last one partial (block masks spanning chunk ends).
+    dict(seq_len=17000, block_size=64, n_q_heads=4, n_kv_heads=2, seed=14),
 ])
 def test_multiblock_rows(variant):
     """Rows spanning many key blocks at every block size: selection on all rows,
