@@ -129,10 +129,10 @@ constexpr float kLazyRescaleAt = 4294967296.0f;
 // Fixed-reference pass: the reference sits this far (log2 units) above the
 // first block's row maximum, and after a rescale above the query's
 // denominator, so that a later block's logits may exceed the previous ones by
-// up to ~64 + kRefMargin before the pass is abandoned.  Exponentials more than
+// up to ~58 + kRefMargin before the pass is abandoned.  Exponentials more than
 // ~126 - kRefMargin below the first block's maximum flush to zero (relative
-// weight under 2^-78).
-constexpr float kRefMargin = 48.0f;
+// weight under 2^-62).
+constexpr float kRefMargin = 64.0f;
 
 // Arguments of one attention pass, shared by the stand-alone and the fused kernel.
 struct AttnCore {
