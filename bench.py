@@ -46,6 +46,8 @@ def parse():
                    help="also time the steps with a write of this many GiB of scratch between them, outside "
                         "the timed events, so that no step finds the previous one's data in L2 or the Infinity "
                         "Cache (0 skips)")
+    p.add_argument("--no-tau-sweep", dest="tau_sweep", action="store_false",
+                   help="skip the attention times of the same layer selected at tighter thresholds")
     p.add_argument("--no-extra-configs", action="store_true",
                    help="skip the compact lines for the other workloads (128K at B = 64 and 256, 32K, the "
                         "64-head 64K layer)")
@@ -402,6 +404,34 @@ def main():
         dense_ms = _time_dense(rbs, torch, np, shape, Q, K, V, stream, args.dense_reps)
         _log(f"[bench] dense attention {dense_ms:.3f} ms")
 
+    # Context for the density: the same layer selected at tighter thresholds.
+    # The attention's time follows the executed block pairs; the headline
+    # line keeps the workload's own thresholds.
+    tau_sweep = None
+    if args.tau_sweep:
+        tau_sweep = []
+        tcounts, tindices = rbs.allocate_lists(shape, dev)
+        for tb, tr in TAU_SWEEP:
+            rbs.rbs_select(shape, Q, stats, tb, tr, w.n_sink, w.n_local, w.n_recent, tcounts, tindices,
+                           stream=stream)
+            ts = []
+            for _ in range(3):
+                a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a_ev.record(stream)
+                rbs.rbs_sparse_prefill(shape, Q, K, V, tcounts, tindices, 0.0, O, stream=stream)
+                b_ev.record(stream)
+                torch.cuda.synchronize()
+                ts.append(a_ev.elapsed_time(b_ev))
+            t_ms = float(np.median(ts))
+            n_exec = int(tcounts.sum().item())
+            t_flops = algorithmic(w, n_exec)["attn_flops"]
+            tau_sweep.append({"tau_base": tb, "tau_rescue": tr, "density": round(n_exec / alg["pairs"], 6),
+                              "attn_ms": round(t_ms, 4),
+                              "attn_mfma_frac": round(t_flops / (t_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                              "attn_speedup_vs_dense": round(dense_ms / t_ms, 3) if dense_ms else None})
+            _log(f"[bench] tau ({tb}, {tr}): {tau_sweep[-1]}")
+        del tcounts, tindices
+
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -469,6 +499,7 @@ def main():
         "mfma_frac_at_sclk": (round(attn_tflops / (PEAK_BF16_TFLOPS * sclk_summary["median"] / PEAK_SCLK_MHZ), 4)
                               if sclk_summary else None),
         "copy_GBps": round(copy_gbps, 1),
+        "tau_sweep": tau_sweep,
     }
 
     rates = unit_rates(brief=True)
@@ -489,6 +520,12 @@ def main():
         _log(f"[bench] CPU oracle measured {cb.pop('measured_s'):.1f}s")
         result["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in cb.items()}
     print(json.dumps(result), flush=True)
+
+
+# Threshold pairs (tau_base, tau_rescue) of the density context: the
+# workload's own, then tighter ones (relative thresholds closer to 1 keep
+# fewer blocks).
+TAU_SWEEP = ((0.9, 0.95), (0.95, 0.975), (0.97, 0.985), (0.99, 0.995))
 
 
 # The other workloads of the benchmark's configurations, one compact line
@@ -566,26 +603,40 @@ def unit_rates(brief: bool = False):
     if not brief:
         return data
 
-    def cyc(other, n, w, same=True, mf=0):
+    def cyc(other, n, w, same=True, mf=0, chains=4):
         for c in data["cases"]:
             if (c["other"] == other and c["n_other"] == n and c["waves_per_simd"] == w and c["mfma"] == mf
-                    and c["acc"] == "vgpr" and (c["placement"] == "same_wave") == same):
+                    and c["acc"] == "vgpr" and (c["placement"] == "same_wave") == same
+                    and c.get("acc_chains", 4) == chains):
                 return c
         return None
 
     ex, fm, mf = cyc("v_exp_f32", 8, 2), cyc("v_fma_f32", 8, 2), cyc("none", 0, 2, mf=8)
     mix = cyc("softmax_mix", 28, 2, mf=8)
+    chain = cyc("none", 0, 1, mf=8, chains=1)  # one wave per SIMD, 8 ops into one accumulator
     # Two waves per SIMD, each issuing 8 of the op (or 8 matrix ops) per loop
     # iteration: one SIMD issues 16 per iteration of either wave.
     per = lambda c: round(c["cycles_per_iter_mfma_wave"] / 16, 2) if c else None
     loop = {c["schedule"]: c["mfma_busy"] for c in data.get("attention_block_loop", [])}
+    # LDS read rate of a compute unit: its 4 SIMDs x 2 waves each read 16
+    # ops of `size` bytes per iteration (a lower bound: each iteration also
+    # waits for its reads).
+    lds = lambda c, size: round(4 * 2 * 16 * size / c["cycles_per_iter_mfma_wave"], 1) if c else None
     return {"exp_cycles": per(ex), "fma_cycles": per(fm), "mfma_32x32x16_bf16_cycles": per(mf),
             "mfma_cycles_with_softmax_mix": per(mix),
+            "mfma_cycles_dependent_chain": (round(chain["cycles_per_iter_mfma_wave"] / 8, 2) if chain else None),
+            "lds_read_bytes_per_clk_per_cu": {"ds_read_b128": lds(cyc("ds_read_b128", 16, 2), 1024),
+                                              "ds_read_b64_tr_b16": lds(cyc("ds_read_b64_tr_b16", 16, 2), 512)},
             "block_loop_mfma_busy": loop or None,
             "note": "shader-clock cycles one SIMD spends per wave64 instruction, two waves per SIMD; "
                     "the mix is 28 exp/fma/max/convert ops beside each 8 matrix ops in the same wave; "
-                    "block_loop: matrix-busy fraction of the attention's block loop on LDS-resident "
-                    "tiles, free-running and as a barrier ping-pong"}
+                    "dependent_chain: one wave per SIMD, each matrix op accumulating into the previous one's "
+                    "result; "
+                    "lds: bytes per shader clock one compute unit's LDS returned to 8 waves reading "
+                    "conflict-free words; block_loop: matrix-busy fraction of the attention's block "
+                    "loop on LDS-resident tiles (one workgroup per CU): free-running, as a barrier "
+                    "ping-pong, with one wave per SIMD, and with 64-key softmax steps at two and "
+                    "three waves per SIMD"}
 
 
 def _time_dense(rbs, torch, np, shape, Q, K, V, stream, reps: int) -> float:

@@ -253,6 +253,11 @@ def test_qwen3_30b_128k_sampled():
     rows = H.sample_rows(w.n_q_heads, w.n_blocks, 96, seed=2, include=[(5, 1023), (31, 700), (0, 3)])
     attn = H.sample_rows(w.n_q_heads, w.n_blocks, 12, seed=7, include=[(5, 1023), (31, 700), (0, 3)])
     r, _ = _full_check(w, select_rows=rows, attn_rows=attn)
+    # Every row's list, not only the sampled ones: ascending, unique, causal,
+    # holding the forced blocks.
+    every = [(h, i) for h in range(w.n_q_heads) for i in range(w.n_blocks)]
+    H.check_lists(H.gpu_rows(r["counts"], r["indices"], every), w.n_blocks, w.n_sink, w.n_local, w.n_recent)
+    _say(f"[parity] {w.name}: all {len(every)} lists well formed")
     # The benchmark's (persistent) launch against one workgroup per (head,
     # query block) on the same lists: every output bit identical.
     lse = torch.empty_like(r["lse"])
