@@ -270,6 +270,23 @@ def test_qwen3_30b_128k_sampled():
 
 
 @pytest.mark.slow
+def test_qwen3_30b_128k_low_density_sampled():
+    """The headline layer at tighter thresholds (3% density, near the paper's
+    operating point): sampled rows against the oracle, every list well formed."""
+    w = WORKLOADS["qwen3-30b-a3b-128k"]
+    tau = (0.95, 0.975)
+    rows = H.sample_rows(w.n_q_heads, w.n_blocks, 48, seed=5, include=[(7, 1023), (20, 512)])
+    attn = H.sample_rows(w.n_q_heads, w.n_blocks, 8, seed=6, include=[(7, 1023)])
+    r, _ = _full_check(w, tau=tau, select_rows=rows, attn_rows=attn)
+    every = [(h, i) for h in range(w.n_q_heads) for i in range(w.n_blocks)]
+    lists = H.gpu_rows(r["counts"], r["indices"], every)
+    H.check_lists(lists, w.n_blocks, w.n_sink, w.n_local, w.n_recent)
+    density = sum(len(v) for v in lists.values()) / (w.n_q_heads * w.n_blocks * (w.n_blocks + 1) / 2)
+    _say(f"[parity] {w.name} tau={tau}: density {density:.4f}, all {len(every)} lists well formed")
+    assert density < 0.1
+
+
+@pytest.mark.slow
 @pytest.mark.parametrize("name", ["qwen3-30b-a3b-128k-b64", "qwen3-30b-a3b-128k-b256"])
 def test_qwen3_30b_128k_other_block_sizes_sampled(name):
     """The 128K layer at 64- and 256-token blocks; sampled rows."""
