@@ -637,10 +637,11 @@ def unit_rates(brief: bool = False):
                     "dependent_chain: one wave per SIMD, each matrix op accumulating into the previous one's "
                     "result; "
                     "lds: bytes per shader clock one compute unit's LDS returned to 8 waves reading "
-                    "conflict-free words; block_loop: matrix-busy fraction of the attention's block "
-                    "loop on LDS-resident tiles (one workgroup per CU): free-running, as a barrier "
-                    "ping-pong, with one wave per SIMD, and with 64-key softmax steps at two and "
-                    "three waves per SIMD"}
+                    "conflict-free words; block_loop: busy fraction of the matrix unit over the 64 QK^T and "
+                    "PV ops per block of the attention's block loop on LDS-resident tiles (one workgroup "
+                    "per CU; denominator on the matrix core, as the kernel): free-running, as a barrier "
+                    "ping-pong, with one wave per SIMD, with 64-key softmax steps at two and three waves "
+                    "per SIMD, and free-running with the denominator summed by v_dot2"}
 
 
 def _time_dense(rbs, torch, np, shape, Q, K, V, stream, reps: int) -> float:

@@ -17,7 +17,8 @@
 // block's softmax and PV run, the next V while the next QK^T runs, each
 // tile's copies issued in pieces among the matrix and exponential steps.  Online
 // softmax in fp32 with exp2; P is rounded to bf16 for the PV product, and the
-// softmax denominator sums exactly those rounded values (v_dot2 with ones).  Causal
+// softmax denominator sums exactly those rounded values, on the matrix core
+// (0/1 rows times the P operand, fp32 accumulation).  Causal
 // masking is applied on the diagonal block only; keys past N are masked in a
 // short last block (their rows are loaded as copies of the last valid key).
 #pragma once
@@ -251,7 +252,23 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   // |v| < 2^45).  Otherwise every wave of the workgroup computes the item
   // again with the running maximum of the online softmax (raised lazily: only
   // when a block's maximum exceeds it by more than kRescaleSlack).
-  float ms_run, l_run;  // reference maximum (log2 units); this lane's share of the denominator
+  float ms_run;  // reference maximum (log2 units)
+  // Denominator on the matrix core.  Read as the B operand of the 16x16x32
+  // op, lane l's P register (query l % 32, 8 keys of the chunk) sits in column
+  // l % 16 at k-group l / 16, so k-groups 0 and 2 hold the chunk's 16 keys of
+  // query l % 16 and groups 1 and 3 those of query l % 16 + 16.  A row m of
+  // A selecting the k-groups of parity m % 2 sums them: lane l finds its own
+  // query's sum in element (l / 16) % 2 of the accumulator (rows 4 (l / 16)
+  // .. + 3 of column l % 16).  It replaces 32 v_dot2 per block and wave by
+  // 8 matrix ops of a quarter of the PV op's size.
+  f32x4 lacc;
+  bf16x8 lsel;
+  {
+    const __bf16 v = (((lane >> 4) & 1) == (lane & 1)) ? (__bf16)1.0f : (__bf16)0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) lsel[e] = v;
+  }
+  auto l_of = [&]() __attribute__((always_inline)) { return ((lane >> 4) & 1) ? lacc[1] : lacc[0]; };
   f32x16 o[4];
   // Fixed-reference pass: set by a wave whose shares left the range, read by
   // every wave after the block's last barrier, so that the workgroup stops the
@@ -260,7 +277,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   for (int pass = 0; pass < 2; ++pass) {
   const bool exact = pass == 1;
   ms_run = -INFINITY;
-  l_run = 0.f;
+  lacc = f32x4{};
   bool out_of_range = false;  // fixed-reference pass: some step took a share past kFixedRefBound
   // Every lane stores the same value (a branch here cost the block loop its
   // registers); no wave reads it before the first block's barriers.
@@ -349,7 +366,8 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
           const float ms_new = exact ? fmaxf(ms_run, mxs) : mxs + kRefMargin;
           const float alpha = ms_new == ms_run ? 1.f : fast_exp2(ms_run - ms_new);
           ms_run = ms_new;
-          l_run *= alpha;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) lacc[e] *= alpha;
 #pragma unroll
           for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -376,15 +394,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
         bf16x8 pb;
 #pragma unroll
         for (int e = 0; e < 8; ++e) pb[e] = (__bf16)s[c >> 1][8 * (c & 1) + e];
-        {
-          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-          const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bf16x2 pair = {pb[2 * e], pb[2 * e + 1]};
-            l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
-          }
-        }
+        lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lsel, pb, lacc, 0, 0, 0);
         const int row0 = kbase + 16 * c + 4 * half + vq;
         const unsigned char* v0 = v_lds + row0 * 256 + vbyte;
         const unsigned char* v1 = v0 + 8 * 256;
@@ -399,21 +409,22 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
           o[dt] = mfma_bf16(a, pb, o[dt]);
         }
       }
-      if (!exact && __any(!(l_run <= kLazyRescaleAt))) {
+      if (!exact && __any(!(l_of() <= kLazyRescaleAt))) {
         // A later block's logits exceed the reference: move the reference up
         // by the exponent of the query's denominator (the same in the two
         // lanes that hold the query) and scale O and the shares down by that
         // power of two.  Shares past kFixedRefBound mean this step's O may
         // have left fp32's range: the item is computed again.
-        if (__any(!(l_run <= kFixedRefBound))) {
+        if (__any(!(l_of() <= kFixedRefBound))) {
           out_of_range = true;
           stop_fixed = 1;
         }
-        const float l_tot = l_run + wave_xor_f(l_run, 32);
+        const float l_tot = l_of();
         const int k = l_tot > kLazyRescaleAt ? __builtin_amdgcn_frexp_expf(l_tot) + (int)kRefMargin : 0;
         const float f = __builtin_amdgcn_ldexpf(1.0f, -k);
         ms_run += (float)k;
-        l_run *= f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) lacc[e] *= f;
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -439,7 +450,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   // tile take one flag per wave.
   {
     int* flags = reinterpret_cast<int*>(k_lds);
-    const bool bad = __any(out_of_range || !(l_run <= kFixedRefBound));
+    const bool bad = __any(out_of_range || !(l_of() <= kFixedRefBound));
     if (lane == 0) flags[wave] = bad ? 1 : 0;
     __syncthreads();
     int any_bad = 0;
@@ -450,7 +461,7 @@ __device__ __forceinline__ void attend_block(const AttnCore& c, int h, int i, in
   }
   }
 
-  const float l_tot = l_run + wave_xor_f(l_run, 32);
+  const float l_tot = l_of();
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   if (q_ok) {
     uint16_t* orow = c.O + h * c.q_head + (int64_t)qpos * c.q_tok;

@@ -23,6 +23,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
 
 constexpr int kLdsBytes = 96 * 1024;
 
@@ -167,7 +168,8 @@ __global__ __launch_bounds__(512) void rate_kernel(float* out, unsigned long lon
 // The attention's block loop on LDS-resident tiles (no global memory): per
 // block and wave, S^T = K Q^T (32 matrix ops, K operands read from LDS), the
 // softmax (64 FMA + exp2, 32 bf16 conversions), then O^T += V^T P^T (32 matrix
-// ops, V^T through the LDS transpose read, 32 v_dot2c for the denominator).
+// ops, V^T through the LDS transpose read) and the denominator: 8 16x16x32
+// matrix ops of 0/1 rows times P (MDEN, as the kernel), or 32 v_dot2c.
 // One workgroup per CU of 4*WPS waves (WPS per SIMD).  KSTEP keys per softmax
 // step: 128 as the kernel, or 64 (two half steps per block, half the S and P
 // registers, which is what three waves per SIMD need).  PINGPONG 0: every wave
@@ -182,7 +184,7 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 constexpr int kLoopMaxThreads = 1024;  // per-workgroup stride of the outputs
 constexpr int kLoopMaxWaves = 16;
 
-template <int PINGPONG, int KSTEP, int WPS>
+template <int PINGPONG, int KSTEP, int WPS, bool MDEN>
 __global__ __launch_bounds__(256 * WPS) __attribute__((amdgpu_waves_per_eu(WPS < 2 ? 2 : WPS))) void block_loop_kernel(float* out, unsigned long long* cycles, int nblocks) {
   static_assert(KSTEP == 64 || KSTEP == 128, "64 or 128 keys per step");
   static_assert(PINGPONG == 0 || (KSTEP == 128 && WPS == 2), "ping-pong with the kernel's shape only");
@@ -206,6 +208,10 @@ __global__ __launch_bounds__(256 * WPS) __attribute__((amdgpu_waves_per_eu(WPS <
   f32x16 s[MT];
   bf16x8 pb[PC];
   float l_run = 0.f;
+  f32x4 lacc = {};
+  bf16x8 lsel;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) lsel[e] = (((lane >> 4) & 1) == (lane & 1)) ? (__bf16)1.0f : (__bf16)0.0f;
   const int group = wave >> 2;
   __syncthreads();
   auto qk = [&](int st) __attribute__((always_inline)) {
@@ -236,12 +242,16 @@ __global__ __launch_bounds__(256 * WPS) __attribute__((amdgpu_waves_per_eu(WPS <
     const int vq = (lane & 15) >> 2, vsub = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1), vbyte = 8 * (lane & 1);
 #pragma unroll
     for (int c = 0; c < PC; ++c) {
-      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+      if constexpr (MDEN) {
+        lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lsel, pb[c], lacc, 0, 0, 0);
+      } else {
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bf16x2 pair = {pb[c][2 * e], pb[c][2 * e + 1]};
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+        for (int e = 0; e < 4; ++e) {
+          const bf16x2 pair = {pb[c][2 * e], pb[c][2 * e + 1]};
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+        }
       }
       const int row0 = KSTEP * st + 16 * c + 4 * half + vq;
       const unsigned char* v0 = vt + row0 * 256 + vbyte;
@@ -282,7 +292,7 @@ __global__ __launch_bounds__(256 * WPS) __attribute__((amdgpu_waves_per_eu(WPS <
     }
   }
   const unsigned long long t1 = __builtin_amdgcn_s_memtime();
-  float acc = l_run;
+  float acc = l_run + lacc[0] + lacc[1];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -293,7 +303,7 @@ __global__ __launch_bounds__(256 * WPS) __attribute__((amdgpu_waves_per_eu(WPS <
 
 // Median cycles per block and wave of block_loop_kernel over n_wg workgroups;
 // false on a HIP error.
-template <int PINGPONG, int KSTEP, int WPS>
+template <int PINGPONG, int KSTEP, int WPS, bool MDEN = true>
 bool run_block_loop(int n_wg, int nblocks, double* cyc_per_block, double* ms_out) {
   constexpr int waves = 4 * WPS;
   float* out = nullptr;
@@ -302,7 +312,7 @@ bool run_block_loop(int n_wg, int nblocks, double* cyc_per_block, double* ms_out
   if (hipMalloc(&cyc, (size_t)n_wg * kLoopMaxWaves * sizeof(unsigned long long)) != hipSuccess) return false;
   hipEvent_t e0, e1;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return false;
-  auto kern = block_loop_kernel<PINGPONG, KSTEP, WPS>;
+  auto kern = block_loop_kernel<PINGPONG, KSTEP, WPS, MDEN>;
   // The tiles take 64 KiB of static LDS; the rest of kLdsBytes is asked for
   // dynamically so that a compute unit holds one workgroup whatever the
   // register count allows (two four-wave workgroups would otherwise share one).
@@ -481,6 +491,7 @@ int main() {
       {"free_running_one_wave_per_simd", 128, 1, run_block_loop<0, 128, 1>},
       {"free_running_half_steps", 64, 2, run_block_loop<0, 64, 2>},
       {"free_running_half_steps_three_waves_per_simd", 64, 3, run_block_loop<0, 64, 3>},
+      {"free_running_dot2_denominator", 128, 2, run_block_loop<0, 128, 2, false>},
   };
   for (size_t k = 0; k < sizeof(loops) / sizeof(loops[0]); ++k) {
     double cpb = 0.0, ms = 0.0;
