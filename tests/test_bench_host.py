@@ -66,3 +66,41 @@ def test_cpu_baseline_covers_every_kv_head_and_states_its_sample():
     assert f"all {w.n_kv_heads} KV heads in full" in cb["sample"]
     assert "selection for 4" in cb["sample"] and "attention (on the GPU's lists) for 2" in cb["sample"]
     assert cb["cpu"]
+
+
+def test_density_context_starts_with_the_workloads_thresholds():
+    """The threshold sweep repeats the headline pair first (its attention time
+    calibrates the others), holds the paper's default pair, and keeps every
+    pair inside [0, 1]."""
+    w = WORKLOADS["qwen3-30b-a3b-128k"]
+    assert bench.TAU_SWEEP[0] == (w.tau_base, w.tau_rescue)
+    assert (0.22, 0.18) in bench.TAU_SWEEP
+    assert all(0.0 <= t <= 1.0 for pair in bench.TAU_SWEEP for t in pair)
+
+
+def test_unit_rate_summary_reads_the_probe_cases(monkeypatch, tmp_path):
+    """The brief unit-rate summary picks the right cases out of the probe's
+    JSON: per-instruction cycles at two waves per SIMD, the dependent chain at
+    one wave, and the LDS read rates (4 SIMDs x 2 waves x 16 reads per
+    iteration)."""
+    import json
+
+    def case(other, n, w, cyc, mf=0, chains=4):
+        return {"mfma": mf, "acc": "vgpr", "acc_chains": chains, "other": other, "n_other": n,
+                "placement": "same_wave", "waves_per_simd": w, "cycles_per_iter_mfma_wave": cyc,
+                "cycles_per_iter_other_wave": 0.0, "sclk_mhz": 2000, "ms": 1.0, "simd_of_wave": []}
+    data = {"cases": [case("v_exp_f32", 8, 2, 152.0), case("v_fma_f32", 8, 2, 64.0),
+                      case("none", 0, 2, 512.0, mf=8), case("none", 0, 1, 256.0, mf=8, chains=1),
+                      case("none", 0, 1, 999.0, mf=8), case("softmax_mix", 28, 2, 760.0, mf=8),
+                      case("ds_read_b128", 16, 2, 512.0), case("ds_read_b64_tr_b16", 16, 2, 256.0)],
+            "attention_block_loop": [{"schedule": "free_running", "mfma_busy": 0.75}]}
+    probe = tmp_path / "probe"
+    probe.write_text("#!/bin/sh\ncat <<'JSON'\n" + json.dumps(data) + "\nJSON\n")
+    probe.chmod(0o755)
+    monkeypatch.setattr(bench, "UNIT_RATES_BIN", str(probe))
+    r = bench.unit_rates(brief=True)
+    assert r["exp_cycles"] == 9.5 and r["fma_cycles"] == 4.0 and r["mfma_32x32x16_bf16_cycles"] == 32.0
+    assert r["mfma_cycles_dependent_chain"] == 32.0
+    assert r["mfma_cycles_with_softmax_mix"] == 47.5
+    assert r["lds_read_bytes_per_clk_per_cu"] == {"ds_read_b128": 256.0, "ds_read_b64_tr_b16": 256.0}
+    assert r["block_loop_mfma_busy"] == {"free_running": 0.75}
